@@ -1,0 +1,173 @@
+"""fp64 CPU oracle for the MASW hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke check and the CPU-baseline leg of the
+benchmark may import this package.  The product (the HIP library and its
+Python binding) never does, and this package never imports the product.
+
+The arithmetic lives in ``oracle.c`` (plain C, double precision, textbook
+definitions, no blocking or online rescaling).  This module only marshals
+numpy arrays into it, and composes two of its routines into the memory-slot
+K/V materialisation:
+
+    memory_update = oracle_project (Sec. 3.2 projection equations)
+                    followed by oracle_rope on the K half only, at the slot's
+                    position id (Sec. 3.2, memory update cycle: a slot shares
+                    the position id of the raw token after it).
+
+``masw_sets`` holds the visible-set simulator written from the paper's set
+definitions (Sec. 3.1 and 3.2).
+
+Every function here has a pin in ``tests/test_oracle_pins.py``.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_fp = ctypes.POINTER(ctypes.c_float)
+_ip = ctypes.POINTER(ctypes.c_int)
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    i, d = ctypes.c_int, ctypes.c_double
+    lib.oracle_attend.argtypes = [i, i, _dp, i, _dp, _dp, d, _dp, _dp, _dp]
+    lib.oracle_attend_batched.argtypes = [i, i, i, i, _dp, i, _ip, _dp, _dp, d, _dp, _dp]
+    lib.oracle_verify.argtypes = [i, i, i, i, i, _dp, i, _ip, _dp, _dp, d, _dp, _dp]
+    lib.oracle_project.argtypes = [i, i, i, _dp, _dp, _dp]
+    lib.oracle_rope.argtypes = [i, i, i, _dp, _ip, d]
+    lib.oracle_argmax.argtypes = [i, i, _fp, _ip]
+    lib.oracle_accept_greedy.argtypes = [i, i, i, _fp, _ip, _ip, _ip]
+    for f in ("oracle_attend", "oracle_attend_batched", "oracle_verify", "oracle_project",
+              "oracle_rope", "oracle_argmax", "oracle_accept_greedy"):
+        getattr(lib, f).restype = None
+    _lib = lib
+    return lib
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a, t):
+    return a.ctypes.data_as(t)
+
+
+def attend(q, k, v, scale, with_wsum=False):
+    """Attention of the G query rows q [G, d] over one key list k, v [n, d].
+
+    Returns (o [G, d], lse [G]) and, if asked, the sum of the normalised
+    softmax weights per row (exactly 1 in real arithmetic)."""
+    lib = _load()
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    G, d = q.shape
+    n = k.shape[0]
+    assert k.shape == (n, d) and v.shape == (n, d)
+    o = np.zeros((G, d))
+    lse = np.zeros(G)
+    ws = np.zeros(G)
+    lib.oracle_attend(G, d, _ptr(q, _dp), n, _ptr(k, _dp), _ptr(v, _dp), float(scale),
+                      _ptr(o, _dp), _ptr(lse, _dp), _ptr(ws, _dp))
+    return (o, lse, ws) if with_wsum else (o, lse)
+
+
+def attend_batched(q, k, v, n, scale):
+    """q [B, Hq, d]; k, v [B, Hkv, nmax, d] with rows 0..n[b]-1 used.
+
+    Returns o [B, Hq, d], lse [B, Hq]; head h reads KV head h // (Hq // Hkv)."""
+    lib = _load()
+    q, k, v, n = _f64(q), _f64(k), _f64(v), _i32(n)
+    B, Hq, d = q.shape
+    _, Hkv, nmax, _ = k.shape
+    o = np.zeros((B, Hq, d))
+    lse = np.zeros((B, Hq))
+    lib.oracle_attend_batched(B, Hq, Hkv, d, _ptr(q, _dp), nmax, _ptr(n, _ip), _ptr(k, _dp),
+                              _ptr(v, _dp), float(scale), _ptr(o, _dp), _ptr(lse, _dp))
+    return o, lse
+
+
+def verify(q, k, v, length, scale):
+    """q [B, T, Hq, d]; k, v [B, Hkv, cap, d] (natural row layout) with the T
+    new tokens at rows len-T..len-1.  Returns o [B, T, Hq, d], lse [B, T, Hq]."""
+    lib = _load()
+    q, k, v, length = _f64(q), _f64(k), _f64(v), _i32(length)
+    B, T, Hq, d = q.shape
+    _, Hkv, cap, _ = k.shape
+    o = np.zeros((B, T, Hq, d))
+    lse = np.zeros((B, T, Hq))
+    lib.oracle_verify(B, T, Hq, Hkv, d, _ptr(q, _dp), cap, _ptr(length, _ip), _ptr(k, _dp),
+                      _ptr(v, _dp), float(scale), _ptr(o, _dp), _ptr(lse, _dp))
+    return o, lse
+
+
+def project(x, w):
+    """y = x W^T for x [R, D], w [N, D]."""
+    lib = _load()
+    x, w = _f64(x), _f64(w)
+    R, D = x.shape
+    N = w.shape[0]
+    assert w.shape[1] == D
+    y = np.zeros((R, N))
+    lib.oracle_project(R, D, N, _ptr(x, _dp), _ptr(w, _dp), _ptr(y, _dp))
+    return y
+
+
+def rope(k, pos, base):
+    """Rotate-half RoPE of k [R, H, d] at integer positions pos [R] (returns a copy)."""
+    lib = _load()
+    k = _f64(k).copy()
+    pos = _i32(pos)
+    R, H, d = k.shape
+    lib.oracle_rope(R, H, d, _ptr(k, _dp), _ptr(pos, _ip), float(base))
+    return k
+
+
+def memory_update(x, w, pos, hkv, d, base):
+    """K/V of new memory slots from their hidden states.
+
+    x [R, D] slot hidden states, w [2*hkv*d, D] = [W_K,g rows ; W_V,g rows],
+    pos [R] position ids.  Returns (k [R, hkv, d], v [R, hkv, d]): the K half
+    is rotated at pos, the V half is not."""
+    y = project(x, w)
+    R = y.shape[0]
+    k = y[:, : hkv * d].reshape(R, hkv, d)
+    v = y[:, hkv * d:].reshape(R, hkv, d)
+    return rope(k, pos, base), v.copy()
+
+
+def argmax(logits):
+    """Row argmax of float32 logits [rows, V] (ties -> lowest, NaN highest)."""
+    lib = _load()
+    x = np.ascontiguousarray(logits, dtype=np.float32)
+    rows, V = x.shape
+    out = np.zeros(rows, dtype=np.int32)
+    lib.oracle_argmax(rows, V, _ptr(x, _fp), _ptr(out, _ip))
+    return out
+
+
+def accept_greedy(logits, draft):
+    """logits [B, T, V] float32, draft [B, T-1] int -> (n_accept [B], next [B])."""
+    lib = _load()
+    x = np.ascontiguousarray(logits, dtype=np.float32)
+    B, T, V = x.shape
+    dr = _i32(draft).reshape(B, T - 1) if T > 1 else np.zeros((B, 0), np.int32)
+    dr = np.ascontiguousarray(dr)
+    na = np.zeros(B, dtype=np.int32)
+    nx = np.zeros(B, dtype=np.int32)
+    lib.oracle_accept_greedy(B, T, V, _ptr(x, _fp), _ptr(dr, _ip), _ptr(na, _ip), _ptr(nx, _ip))
+    return na, nx
