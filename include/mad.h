@@ -1,0 +1,195 @@
+/*
+ * mad.h -- C ABI of libmad: the data-parallel hot path of memory-augmented
+ * sliding-window (MASW) drafting for long-context speculative decoding, on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes (paper: "Strong Drafts Need Compact Memories"):
+ *   - the draft model's per-step decode attention over its compact memory
+ *     (sink + memory slots, then the exact local window)          Sec. 3.1
+ *   - the memory adaptor's update: mirrored K/V projection of new slot
+ *     hidden states, RoPE at the slot's position id, append-only write Sec. 3.2
+ *   - the target's (gamma+1)-query verify attention over its full KV  Sec. 2.1, 3.3
+ *   - the greedy accept/reject rule                                  Sec. 2.1, 4.1
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are DEVICE memory owned by the caller, row-major; a key/value row
+ *     (head_dim elements) is contiguous.  Per-sequence lengths, starts,
+ *     positions and fire flags are HOST arrays, copied into kernel arguments,
+ *     so every argument is validated synchronously before anything is
+ *     enqueued; on an error nothing is launched and no buffer is touched.
+ *   - dtype: MAD_F32 or MAD_BF16 (inputs and outputs share it; arithmetic
+ *     accumulates in fp32; lse outputs are always fp32).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue
+ *     work and return; nothing synchronises the host.
+ *   - Workspace `ws`: device scratch of at least mad_workspace_bytes(...)
+ *     bytes.  It holds split partial results and arrival counters.  It must be
+ *     zero-filled once before its first use; every call leaves the counters at
+ *     zero again when its kernels finish.  Calls that share a workspace must
+ *     be ordered (same stream); concurrent calls on one workspace race.
+ *   - The library allocates no device memory and keeps no state besides a
+ *     thread-local error string.  No C++ exception crosses the ABI.
+ *   - Return value: MAD_OK or a negative MAD_E* code; mad_last_error() then
+ *     describes the failure.
+ *   - Limits: B <= MAD_MAX_BATCH; head_dim in {64, 128}; 1 <= Hq/Hkv <= 16.
+ */
+#ifndef MAD_H
+#define MAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MAD_OK 0
+#define MAD_EINVAL (-1)  /* bad pointer, shape, length, capacity or workspace argument */
+#define MAD_ENOTSUP (-2) /* valid but unsupported: head_dim, group size, dtype */
+#define MAD_EHIP (-3)    /* a HIP launch failed; the message carries hipGetErrorString */
+#define MAD_EWS (-4)     /* workspace smaller than mad_workspace_bytes() asks */
+
+#define MAD_F32 0
+#define MAD_BF16 1
+
+#define MAD_MAX_BATCH 64
+#define MAD_MAX_UPDATE_ROWS 64 /* B * n_new per mad_memory_update call */
+#define MAD_MAX_VERIFY_ROWS 64 /* T * (Hq / Hkv) per mad_verify_attn call */
+
+#define MAD_OP_DECODE 0
+#define MAD_OP_UPDATE 1
+#define MAD_OP_VERIFY 2
+#define MAD_OP_ACCEPT 3
+
+/*
+ * A per-sequence, per-KV-head run of key/value rows in device memory.
+ * Row i of sequence b, KV head h lives at
+ *     k + b * seq_stride + h * head_stride + i * head_dim   (elements of dtype)
+ * and likewise for v.  seq_stride may be 0 (every sequence index aliases the
+ * same buffer, e.g. several queries of one sequence with different visible
+ * ranges); head_stride >= cap * head_dim.
+ *   cap    rows available per (sequence, head)
+ *   start  HOST int32[B], ring start of each sequence (NULL = all 0); used by
+ *          the local window only, must satisfy 0 <= start < cap
+ *   len    HOST int32[B], number of valid rows, 0 <= len <= cap
+ */
+typedef struct mad_kv_view {
+    void *k;
+    void *v;
+    int64_t seq_stride;
+    int64_t head_stride;
+    int32_t cap;
+    const int32_t *start;
+    const int32_t *len;
+} mad_kv_view;
+
+/*
+ * Draft decode attention over the compact memory (Sec. 3.1: the working
+ * memory M_t = M_sink u M_local,t u M_slot,t; the draft reads only this
+ * compact memory, Sec. 3.3).  For each sequence b and query head h, with
+ * G = Hq / Hkv and KV head c = h / G (consecutive query heads share a KV head):
+ *
+ *   keys  = mem rows [0, mem.len[b])                       (sinks, then slots)
+ *         ++ window rows i = 0 .. win.len[b]-1 at ring row (win.start[b] + i) % win.cap
+ *         ++ the new token (k_new, v_new) when k_new != NULL
+ *   out[b][h] = sum_j softmax_j(scale * q[b][h] . K_j) V_j,
+ *   lse[b][h] = log sum_j exp(scale * q[b][h] . K_j)        (natural log)
+ *
+ * When k_new/v_new are given ([B][Hkv][d], dtype) the new token's K/V are
+ * also written into the window ring at row (start + len) % cap -- the append
+ * of the current token into the local window in the same pass (Sec. 3.2);
+ * this requires win.len[b] + 1 <= win.cap.  Eviction is the caller's
+ * bookkeeping: advancing win.start / shrinking win.len; evicted rows stay in
+ * the ring until overwritten, which is what the raw-KV rollback window keeps.
+ *   q    device [B][Hq][d], dtype          out  device [B][Hq][d], dtype
+ *   lse  device fp32 [B][Hq] or NULL
+ *   mem  linear view (start ignored) or NULL = empty; win  ring view or NULL
+ * A sequence with no keys at all gets out = 0 and lse = -inf.
+ * The full-KV draft (the uncompressed comparison) is the same call with an
+ * empty mem and the whole prefix in the window.
+ * Supports dtype F32 and BF16, d in {64, 128}, G in {1, 2, 4, 8, 16}.
+ */
+int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                          const mad_kv_view *mem, const mad_kv_view *win,
+                          const void *k_new, const void *v_new,
+                          void *out, float *lse,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Memory update by the memory adaptor (Sec. 3.2, projection and KV
+ * materialisation): for every firing sequence b and slot i < n_new,
+ *   [k~ | v] = x[b][i] . [W_K,g ; W_V,g]^T          (mirrored projections)
+ *   k        = RoPE(k~, pos[b][i])                   (rotate-half pairs (j, j+d/2),
+ *              angle pos * base^(-2j/d), computed in fp64)
+ * and the pair is appended at mem row mem.len[b] + i (append-only: rows below
+ * mem.len[b] are never written).  The caller then raises mem.len[b] by n_new.
+ *   x      device [B][n_new][D], dtype (slot hidden states entering the layer)
+ *   w_kv   device [2*Hkv*d][D], dtype: the Hkv*d rows of W_K,g then the Hkv*d
+ *          rows of W_V,g (one row per output feature, nn.Linear layout)
+ *   pos    HOST int32[B][n_new] position ids (a slot shares the id of the raw
+ *          token after it)
+ *   fire   HOST uint8[B] or NULL (= all fire); fire[b] == 0 leaves sequence b
+ *          untouched (the per-sequence mask of heterogeneous batches, Sec. 4.1)
+ *   mem    linear view to append to; requires mem.len[b] + n_new <= mem.cap
+ * B * n_new <= MAD_MAX_UPDATE_ROWS; D a multiple of 64; d in {64, 128}.
+ * BF16 runs the projection on the matrix cores; F32 on the vector ALUs.
+ */
+int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const uint8_t *fire,
+                      int B, int n_new, int D, int Hkv, int d, int dtype, double rope_base,
+                      const mad_kv_view *mem, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Target verify attention (Sec. 2.1: the target scores the drafted block in
+ * one parallel pass; Sec. 3.3: over its full KV cache).  The T = gamma+1 new
+ * tokens' K/V are already stored at rows len[b]-T .. len[b]-1; query t sees
+ * rows 0 .. len[b]-T+t (the prefix and new tokens 0..t).
+ *   q     device [B][T][Hq][d], BF16      out device [B][T][Hq][d], BF16
+ *   lse   device fp32 [B][T][Hq] or NULL
+ *   k     device keys, rows of d:    k  + b*seq_stride + h*head_stride + i*d
+ *   vt    device values TRANSPOSED, one run of cap keys per feature:
+ *                                    vt + b*seq_stride + h*head_stride + c*cap + i
+ *         (the verifier's V cache is kept key-contiguous per feature so that
+ *         both products of attention feed the matrix cores straight from HBM)
+ *   len   HOST int32[B], T <= len[b] <= cap; cap a multiple of 8
+ * T * G <= MAD_MAX_VERIFY_ROWS; d in {64, 128}; dtype BF16 only.
+ */
+int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
+                    const void *k, const void *vt, int64_t seq_stride, int64_t head_stride,
+                    int32_t cap, const int32_t *len,
+                    void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Greedy accept/reject (Sec. 2.1; greedy decoding at temperature 0, Sec. 4.1).
+ * For each sequence b, with am[t] = argmax_v logits[b][t][v] (ties -> lowest
+ * index, a NaN ranks above every number):
+ *   n_accept[b] = first t < T-1 with draft_tok[b][t] != am[t], else T-1
+ *   next_tok[b] = am[n_accept[b]]   (the correction, or the bonus token)
+ * The iteration emits n_accept[b] + 1 tokens.
+ *   logits    device [B][T][V], dtype F32 or BF16
+ *   draft_tok device int32 [B][T-1] (may be NULL when T == 1)
+ *   n_accept, next_tok  device int32 [B]
+ * V >= 1, T >= 1.
+ */
+int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok,
+                      int B, int T, int V, int32_t *n_accept, int32_t *next_tok,
+                      void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:
+ *   DECODE: B, Hq, Hkv, d                       (T, max_keys ignored)
+ *   UPDATE: B = rows (B * n_new), Hq = D, Hkv, d (T, max_keys ignored)
+ *   VERIFY: B, Hq, Hkv, d, T                    (max_keys ignored)
+ *   ACCEPT: B, T, max_keys = V                  (Hq, Hkv, d ignored)
+ * Returns 0 for an unknown op or invalid sizes.
+ */
+size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max_keys);
+
+/* Thread-local description of the last failure in this thread ("" if none). */
+const char *mad_last_error(void);
+
+/* Library version string. */
+const char *mad_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MAD_H */

@@ -1,0 +1,253 @@
+"""MI355X-native hot path of memory-augmented sliding-window (MASW) drafting.
+
+Thin ctypes binding over libmad.so (C ABI in include/mad.h).  This module
+only marshals arguments -- tensor pointers, strides, host length arrays and
+the current HIP stream -- into the C entry points; every step of the path
+runs in the library's HIP kernels.  PyTorch provides device memory and
+streams.  If libmad.so is missing the import fails: there is no fallback.
+
+Entry points (same names as the C ABI, without the ``mad_`` prefix):
+    draft_decode_attn   draft decode attention over sink+slots | window ring (+ append)
+    memory_update       mirrored K/V projection + RoPE + append of new memory slots
+    verify_attn         target (gamma+1)-query verify attention over the full KV
+    accept_greedy       greedy accept/reject
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmad.so")
+
+MAD_OK, MAD_EINVAL, MAD_ENOTSUP, MAD_EHIP, MAD_EWS = 0, -1, -2, -3, -4
+MAD_F32, MAD_BF16 = 0, 1
+MAD_OP_DECODE, MAD_OP_UPDATE, MAD_OP_VERIFY, MAD_OP_ACCEPT = 0, 1, 2, 3
+MAX_BATCH = 64
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+
+
+class _KVView(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("seq_stride", ctypes.c_int64), ("head_stride", ctypes.c_int64),
+                ("cap", ctypes.c_int32), ("start", _i32p), ("len", _i32p)]
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_30252_amd.build` "
+                          "(the hot path has no CPU fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, f, d, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double, ctypes.c_size_t
+    kvp = ctypes.POINTER(_KVView)
+    lib.mad_draft_decode_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, vp, vp, vp, sz, vp]
+    lib.mad_memory_update.argtypes = [vp, vp, _i32p, _u8p, i, i, i, i, i, i, d, kvp, vp, sz, vp]
+    lib.mad_verify_attn.argtypes = [vp, i, i, i, i, i, i, f, vp, vp, ctypes.c_int64, ctypes.c_int64,
+                                    ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
+    lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
+    lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
+    lib.mad_workspace_bytes.restype = sz
+    lib.mad_last_error.restype = ctypes.c_char_p
+    lib.mad_version.restype = ctypes.c_char_p
+    for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy"):
+        getattr(lib, fn).restype = ctypes.c_int
+    return lib
+
+
+lib = _load_library()
+
+
+class MadError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libmad error {code}: {msg}")
+        self.code = code
+
+
+def _check(rc):
+    if rc != MAD_OK:
+        raise MadError(rc, lib.mad_last_error().decode())
+
+
+def version() -> str:
+    return lib.mad_version().decode()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return MAD_BF16
+    if t.dtype == torch.float32:
+        return MAD_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _host_i32(vals, n) -> ctypes.Array:
+    arr = (ctypes.c_int32 * max(n, 1))()
+    for j, x in enumerate(vals):
+        arr[j] = int(x)
+    return arr
+
+
+@dataclass
+class KV:
+    """A [B, Hkv, cap, d] pair of K/V tensors (any strides with contiguous
+    rows) plus per-sequence host lengths and, for a ring, start offsets."""
+    k: torch.Tensor
+    v: torch.Tensor
+    length: Sequence[int]
+    start: Optional[Sequence[int]] = None
+
+    def view(self, B):
+        k, v = self.k, self.v
+        if k.dim() != 4 or k.shape != v.shape or k.stride() != v.stride():
+            raise ValueError("K and V must be [B, Hkv, cap, d] tensors with identical strides")
+        if k.stride(3) != 1 or k.stride(2) != k.shape[3]:
+            raise ValueError("K/V rows must be contiguous")
+        self._len = _host_i32(self.length, B)
+        self._start = _host_i32(self.start, B) if self.start is not None else None
+        return _KVView(k.data_ptr(), v.data_ptr(), k.stride(0) if k.shape[0] > 1 else 0, k.stride(1),
+                       k.shape[2], self._start, self._len)
+
+
+class Workspace:
+    """Zero-filled device scratch for split partials and arrival counters.
+
+    The kernels leave the counters at zero when they finish, so one workspace
+    serves any number of calls issued in order on one stream."""
+
+    def __init__(self, device=None):
+        self.device = torch.device(device or "cuda")
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+_default_ws = {}
+
+
+def _ws_for(device, nbytes, ws):
+    if ws is not None:
+        if ws.numel() < nbytes:
+            raise ValueError(f"workspace of {ws.numel()} bytes < {nbytes} needed")
+        return ws
+    key = torch.device(device).index
+    w = _default_ws.get(key)
+    if w is None:
+        w = _default_ws[key] = Workspace(device)
+    return w.get(nbytes)
+
+
+def workspace_bytes(op, B=1, Hq=1, Hkv=1, d=64, T=1, max_keys=0) -> int:
+    return int(lib.mad_workspace_bytes(op, B, Hq, Hkv, d, T, max_keys))
+
+
+def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
+                      k_new: Optional[torch.Tensor] = None, v_new: Optional[torch.Tensor] = None,
+                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                      scale: Optional[float] = None, ws: Optional[torch.Tensor] = None):
+    """q [B, Hq, d] -> (out [B, Hq, d], lse [B, Hq] fp32).
+
+    Attends over mem rows [0, len) then the window ring rows start..start+len-1
+    (mod cap) then the new token (k_new/v_new [B, Hkv, d], which is also
+    written into the ring at row (start + len) % cap)."""
+    B, Hq, d = q.shape
+    Hkv = (mem.k if mem is not None else win.k).shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    if scale is None:
+        scale = d ** -0.5
+    mv = mem.view(B) if mem is not None else None
+    wv = win.view(B) if win is not None else None
+    nbytes = workspace_bytes(MAD_OP_DECODE, B, Hq, Hkv, d)
+    w = _ws_for(q.device, nbytes, ws)
+    rc = lib.mad_draft_decode_attn(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
+                                   ctypes.byref(mv) if mv is not None else None,
+                                   ctypes.byref(wv) if wv is not None else None,
+                                   _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(lse),
+                                   _ptr(w), w.numel(), _stream(q.device))
+    _check(rc)
+    return out, lse
+
+
+def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None,
+                  rope_base: float = 500000.0, ws: Optional[torch.Tensor] = None):
+    """x [B, n_new, D] slot hidden states, w_kv [2*Hkv*d, D]; pos host [B][n_new].
+
+    Appends the slots' K (rotated at pos) and V at mem rows len[b]..len[b]+n_new-1
+    of every firing sequence.  The caller then raises its lengths."""
+    B, n_new, D = x.shape
+    Hkv, d = mem.k.shape[1], mem.k.shape[3]
+    mv = mem.view(B)
+    flat = [int(p) for row in pos for p in row]
+    pos_arr = _host_i32(flat, B * n_new)
+    fire_arr = None
+    if fire is not None:
+        fire_arr = (ctypes.c_uint8 * B)(*[1 if f else 0 for f in fire])
+    nbytes = workspace_bytes(MAD_OP_UPDATE, B * n_new, D, Hkv, d)
+    w = _ws_for(x.device, nbytes, ws)
+    rc = lib.mad_memory_update(_ptr(x), _ptr(w_kv), pos_arr, fire_arr, B, n_new, D, Hkv, d,
+                               _dtype_code(x), float(rope_base), ctypes.byref(mv),
+                               _ptr(w), w.numel(), _stream(x.device))
+    _check(rc)
+
+
+def verify_attn(q: torch.Tensor, k: torch.Tensor, vt: torch.Tensor, length, out=None, lse=None,
+                scale: Optional[float] = None, ws: Optional[torch.Tensor] = None):
+    """q [B, T, Hq, d]; k [B, Hkv, cap, d]; vt [B, Hkv, d, cap] (values stored
+    key-contiguous per feature); the T new tokens sit at rows len-T..len-1.
+    Returns (out [B, T, Hq, d], lse [B, T, Hq])."""
+    B, T, Hq, d = q.shape
+    Hkv, cap = k.shape[1], k.shape[2]
+    if vt.shape != (B, Hkv, d, cap):
+        raise ValueError(f"vt must be [B, Hkv, d, cap] = {(B, Hkv, d, cap)}, got {tuple(vt.shape)}")
+    if k.stride(3) != 1 or k.stride(2) != d or vt.stride(3) != 1 or vt.stride(2) != cap:
+        raise ValueError("k rows and vt feature runs must be contiguous")
+    if k.stride(0) != vt.stride(0) or k.stride(1) != vt.stride(1):
+        raise ValueError("k and vt must share sequence and head strides")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=q.device)
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace_bytes(MAD_OP_VERIFY, B, Hq, Hkv, d, T)
+    w = _ws_for(q.device, nbytes, ws)
+    rc = lib.mad_verify_attn(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), _ptr(k), _ptr(vt),
+                             k.stride(0) if B > 1 else 0, k.stride(1), cap, _host_i32(length, B),
+                             _ptr(out), _ptr(lse), _ptr(w), w.numel(), _stream(q.device))
+    _check(rc)
+    return out, lse
+
+
+def accept_greedy(logits: torch.Tensor, draft_tok: Optional[torch.Tensor], n_accept=None, next_tok=None,
+                  ws: Optional[torch.Tensor] = None):
+    """logits [B, T, V] (fp32 or bf16), draft_tok int32 [B, T-1] on the device.
+    Returns (n_accept int32 [B], next_tok int32 [B]) on the device."""
+    B, T, V = logits.shape
+    dev = logits.device
+    if n_accept is None:
+        n_accept = torch.empty(B, dtype=torch.int32, device=dev)
+    if next_tok is None:
+        next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+    nbytes = workspace_bytes(MAD_OP_ACCEPT, B, 1, 1, 64, T, V)
+    w = _ws_for(dev, nbytes, ws)
+    rc = lib.mad_accept_greedy(_ptr(logits), _dtype_code(logits), _ptr(draft_tok), B, T, V,
+                               _ptr(n_accept), _ptr(next_tok), _ptr(w), w.numel(), _stream(dev))
+    _check(rc)
+    return n_accept, next_tok

@@ -1,0 +1,174 @@
+// mad_api.hip -- the C ABI of libmad: argument validation, split planning,
+// workspace accounting and kernel launch.  Every check runs on the host before
+// anything is enqueued; no exception leaves this file.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "mad_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return MAD_OK;
+}
+
+int hip_status(hipError_t e, const char *what) {
+    if (e != hipSuccess) return fail(MAD_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int elem_size(int dtype) { return dtype == MAD_BF16 ? 2 : 4; }
+
+bool pow2_group(int G) { return G == 1 || G == 2 || G == 4 || G == 8 || G == 16; }
+
+// Common shape checks for attention entry points.
+int check_heads(int B, int Hq, int Hkv, int d, int dtype) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0)
+        return fail(MAD_EINVAL, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+    if (dtype != MAD_F32 && dtype != MAD_BF16) return fail(MAD_ENOTSUP, "dtype %d not supported", dtype);
+    if (d != 64 && d != 128) return fail(MAD_ENOTSUP, "head_dim %d not supported (64 or 128)", d);
+    if (!pow2_group(Hq / Hkv)) return fail(MAD_ENOTSUP, "group size %d not supported (1,2,4,8,16)", Hq / Hkv);
+    return MAD_OK;
+}
+
+// Validate a kv view for B sequences; `ring` enables the start array check.
+int check_view(const mad_kv_view *v, const char *name, int B, int Hkv, int d, int dtype, bool ring,
+               bool need_write_room) {
+    if (!v->k || !v->v) return fail(MAD_EINVAL, "%s: null k or v", name);
+    if (!aligned16(v->k) || !aligned16(v->v)) return fail(MAD_EINVAL, "%s: k/v not 16-byte aligned", name);
+    if (v->cap < 1) return fail(MAD_EINVAL, "%s: cap=%d", name, v->cap);
+    if (!v->len) return fail(MAD_EINVAL, "%s: null len", name);
+    const int vec = 16 / elem_size(dtype);
+    if (v->seq_stride < 0 || v->head_stride < (int64_t)v->cap * d || v->seq_stride % vec || v->head_stride % vec)
+        return fail(MAD_EINVAL, "%s: bad strides (seq %lld, head %lld) for cap %d, d %d", name,
+                    (long long)v->seq_stride, (long long)v->head_stride, v->cap, d);
+    if (v->seq_stride != 0 && v->seq_stride < (int64_t)Hkv * v->head_stride && B > 1)
+        return fail(MAD_EINVAL, "%s: seq_stride %lld overlaps heads", name, (long long)v->seq_stride);
+    for (int b = 0; b < B; ++b) {
+        int len = v->len[b];
+        int room = need_write_room ? 1 : 0;
+        if (len < 0 || len + room > v->cap)
+            return fail(MAD_EINVAL, "%s: len[%d]=%d (+%d) exceeds cap %d", name, b, len, room, v->cap);
+        if (ring && v->start) {
+            int st = v->start[b];
+            if (st < 0 || st >= v->cap) return fail(MAD_EINVAL, "%s: start[%d]=%d outside [0, cap)", name, b, st);
+        }
+    }
+    return MAD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *mad_last_error(void) { return g_err; }
+
+const char *mad_version(void) { return "libmad 0.1 (gfx950)"; }
+
+size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max_keys) {
+    (void)max_keys;
+    switch (op) {
+        case MAD_OP_DECODE:
+            if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128)) return 0;
+            return mad::decode_ws_bytes(B, Hq, Hkv, d);
+        default:
+            (void)T;
+            return 0;
+    }
+}
+
+int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                          const mad_kv_view *mem, const mad_kv_view *win, const void *k_new,
+                          const void *v_new, void *out, float *lse, void *ws, size_t ws_bytes,
+                          void *stream) {
+    int rc = check_heads(B, Hq, Hkv, d, dtype);
+    if (rc) return rc;
+    if (!q || !out) return fail(MAD_EINVAL, "null q or out");
+    if (!aligned16(q) || !aligned16(out)) return fail(MAD_EINVAL, "q/out not 16-byte aligned");
+    if ((k_new == nullptr) != (v_new == nullptr)) return fail(MAD_EINVAL, "k_new and v_new must both be given or both null");
+    if (k_new && (!aligned16(k_new) || !aligned16(v_new))) return fail(MAD_EINVAL, "k_new/v_new not 16-byte aligned");
+    if (k_new && !win) return fail(MAD_EINVAL, "k_new needs a window ring to append to");
+    if (!(scale > 0.f) || scale != scale) return fail(MAD_EINVAL, "scale must be positive");
+    if (mem && (rc = check_view(mem, "mem", B, Hkv, d, dtype, false, false))) return rc;
+    if (win && (rc = check_view(win, "win", B, Hkv, d, dtype, true, k_new != nullptr))) return rc;
+    const int G = Hq / Hkv;
+
+    mad::DecodeArgs a;
+    memset(&a, 0, sizeof(a));
+    int n_keys[MAD_MAX_BATCH];
+    for (int b = 0; b < B; ++b) {
+        a.mlen[b] = mem ? mem->len[b] : 0;
+        a.wlen[b] = win ? win->len[b] : 0;
+        a.wstart[b] = (win && win->start) ? win->start[b] : 0;
+        n_keys[b] = a.mlen[b] + a.wlen[b] + (k_new ? 1 : 0);
+    }
+    mad::DecodePlan p = mad::plan_decode(B, Hkv, n_keys);
+    size_t need = p.n_splits > 1 ? mad::decode_ws_bytes(B, Hq, Hkv, d) : 0;
+    if (need > 0) {
+        if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
+        if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
+        if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
+    }
+    a.q = q;
+    a.out = out;
+    a.lse = lse;
+    if (mem) {
+        a.mk = mem->k; a.mv = mem->v; a.m_seq = mem->seq_stride; a.m_head = mem->head_stride;
+    }
+    if (win) {
+        a.wk = win->k; a.wv = win->v; a.w_seq = win->seq_stride; a.w_head = win->head_stride;
+        a.w_cap = win->cap;
+    } else {
+        a.w_cap = 1;
+    }
+    a.kn = k_new;
+    a.vn = v_new;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.units = p.units;
+    a.n_splits = p.n_splits;
+    a.chunk = p.chunk;
+    if (need > 0) {
+        size_t units = (size_t)p.units;
+        char *base = (char *)ws;
+        a.counters = (unsigned *)base;
+        size_t fill = (mad::kDecodeTargetWGs + units - 1) / units;
+        if (fill > (size_t)mad::kDecodeMaxSplits) fill = mad::kDecodeMaxSplits;
+        a.part_o = (float *)(base + mad::align256(units * 4));
+        a.part_ml = (float *)(base + mad::align256(units * 4) + mad::align256(units * fill * G * d * 4));
+    }
+    return hip_status(mad::launch_decode(a, dtype, d, G, (hipStream_t)stream), "decode launch");
+}
+
+int mad_memory_update(const void *, const void *, const int32_t *, const uint8_t *, int, int, int, int,
+                      int, int, double, const mad_kv_view *, void *, size_t, void *) {
+    return fail(MAD_ENOTSUP, "mad_memory_update: not built yet");
+}
+
+int mad_verify_attn(const void *, int, int, int, int, int, int, float, const void *, const void *, int64_t,
+                    int64_t, int32_t, const int32_t *, void *, float *, void *, size_t, void *) {
+    return fail(MAD_ENOTSUP, "mad_verify_attn: not built yet");
+}
+
+int mad_accept_greedy(const void *, int, const int32_t *, int, int, int, int32_t *, int32_t *, void *, size_t,
+                      void *) {
+    return fail(MAD_ENOTSUP, "mad_accept_greedy: not built yet");
+}
+
+}  // extern "C"

@@ -1,0 +1,112 @@
+// mad_device.h -- small device helpers shared by the libmad kernels (gfx950).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mad {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// bf16 is carried as raw uint16_t bits; conversions are written out.
+struct bf16_t {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// Element type traits: T = float or bf16_t; a 16-byte vector holds VEC elements.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    static constexpr int VEC = 4;
+    __device__ __forceinline__ static float load1(const float *p) { return *p; }
+    __device__ __forceinline__ static void store1(float *p, float v) { *p = v; }
+};
+template <> struct Elem<bf16_t> {
+    static constexpr int VEC = 8;
+    __device__ __forceinline__ static float load1(const bf16_t *p) { return bf16_to_f32(p->bits); }
+    __device__ __forceinline__ static void store1(bf16_t *p, float v) { p->bits = f32_to_bf16(v); }
+};
+
+// Unpack a 16-byte vector into fp32 values.
+__device__ __forceinline__ void unpack16(const uint4 &u, float (&f)[4], float) {
+    f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+    f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+}
+__device__ __forceinline__ void unpack16(const uint4 &u, float (&f)[8], bf16_t) {
+    f[0] = bf16_lo(u.x); f[1] = bf16_hi(u.x); f[2] = bf16_lo(u.y); f[3] = bf16_hi(u.y);
+    f[4] = bf16_lo(u.z); f[5] = bf16_hi(u.z); f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
+}
+
+// Cross-lane exchange inside a wave64.  Patterns 1 and 2 use DPP quad
+// permutes, 4 and 8 use DPP row mirrors (valid for sum/max reductions over
+// aligned groups), 16 and 32 use ds_swizzle / permute through the LDS crossbar.
+template <int X> __device__ __forceinline__ float xor_lane(float v);
+template <> __device__ __forceinline__ float xor_lane<1>(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));
+}
+template <> __device__ __forceinline__ float xor_lane<2>(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));
+}
+// row_half_mirror: lane i of each 8-lane half row <-> lane 7-i.  After the
+// groups of 4 are reduced this pairs every lane with the other quad.
+template <> __device__ __forceinline__ float xor_lane<4>(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, true));
+}
+// row_mirror: lane i of each 16-lane row <-> lane 15-i (pairs the two halves of
+// the row once each half is reduced).
+template <> __device__ __forceinline__ float xor_lane<8>(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, true));
+}
+template <> __device__ __forceinline__ float xor_lane<16>(float v) {
+    // ds_swizzle bitmask mode inside 32-lane halves: and 0x1f, or 0, xor 0x10.
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
+}
+template <> __device__ __forceinline__ float xor_lane<32>(float v) {
+    return __shfl_xor(v, 32, 64);
+}
+
+// Reduce over aligned groups of N consecutive lanes (N a power of two <= 64).
+// Valid only as an all-reduce of a commutative, associative op when applied
+// from the smallest pattern upward (the mirrors rely on it).
+template <int N> __device__ __forceinline__ float group_sum(float v) {
+    if constexpr (N >= 2) v += xor_lane<1>(v);
+    if constexpr (N >= 4) v += xor_lane<2>(v);
+    if constexpr (N >= 8) v += xor_lane<4>(v);
+    if constexpr (N >= 16) v += xor_lane<8>(v);
+    if constexpr (N >= 32) v += xor_lane<16>(v);
+    if constexpr (N >= 64) v += xor_lane<32>(v);
+    return v;
+}
+
+// Reduce over lanes that share (lane % STRIDE), i.e. across the 64/STRIDE
+// groups of STRIDE lanes.  Uses exchanges with partners lane ^ k for k >=
+// STRIDE; every pattern here is a true xor for k >= 16 and a mirror for
+// k in {4, 8}.  Mirrors do not preserve (lane % STRIDE), so for STRIDE < 16
+// the generic permute is used instead.
+template <int STRIDE> __device__ __forceinline__ float strided_max(float v) {
+    #pragma unroll
+    for (int k = STRIDE; k < 64; k <<= 1) v = fmaxf(v, __shfl_xor(v, k, 64));
+    return v;
+}
+template <int STRIDE> __device__ __forceinline__ float strided_sum(float v) {
+    #pragma unroll
+    for (int k = STRIDE; k < 64; k <<= 1) v += __shfl_xor(v, k, 64);
+    return v;
+}
+
+}  // namespace mad
