@@ -4,7 +4,8 @@ Thin ctypes binding over libmad.so (C ABI in include/mad.h).  This module
 only marshals arguments -- tensor pointers, strides, host length arrays and
 the current HIP stream -- into the C entry points; every step of the path
 runs in the library's HIP kernels.  PyTorch provides device memory and
-streams.  If libmad.so is missing the import fails: there is no fallback.
+streams.  The library is loaded on first use; if libmad.so is missing that
+first call raises: there is no fallback.
 
 Entry points (same names as the C ABI, without the ``mad_`` prefix):
     draft_decode_attn   draft decode attention over sink+slots | window ring (+ append)
@@ -37,7 +38,13 @@ class _KVView(ctypes.Structure):
                 ("cap", ctypes.c_int32), ("start", _i32p), ("len", _i32p)]
 
 
+_LIB = None
+
+
 def _load_library():
+    global _LIB
+    if _LIB is not None:
+        return _LIB
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_30252_amd.build` "
                           "(the hot path has no CPU fallback)")
@@ -55,10 +62,8 @@ def _load_library():
     lib.mad_version.restype = ctypes.c_char_p
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy"):
         getattr(lib, fn).restype = ctypes.c_int
+    _LIB = lib
     return lib
-
-
-lib = _load_library()
 
 
 class MadError(RuntimeError):
@@ -69,11 +74,11 @@ class MadError(RuntimeError):
 
 def _check(rc):
     if rc != MAD_OK:
-        raise MadError(rc, lib.mad_last_error().decode())
+        raise MadError(rc, _load_library().mad_last_error().decode())
 
 
 def version() -> str:
-    return lib.mad_version().decode()
+    return _load_library().mad_version().decode()
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -152,7 +157,7 @@ def _ws_for(device, nbytes, ws):
 
 
 def workspace_bytes(op, B=1, Hq=1, Hkv=1, d=64, T=1, max_keys=0) -> int:
-    return int(lib.mad_workspace_bytes(op, B, Hq, Hkv, d, T, max_keys))
+    return int(_load_library().mad_workspace_bytes(op, B, Hq, Hkv, d, T, max_keys))
 
 
 def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
@@ -176,7 +181,7 @@ def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
     wv = win.view(B) if win is not None else None
     nbytes = workspace_bytes(MAD_OP_DECODE, B, Hq, Hkv, d)
     w = _ws_for(q.device, nbytes, ws)
-    rc = lib.mad_draft_decode_attn(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
+    rc = _load_library().mad_draft_decode_attn(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
                                    ctypes.byref(mv) if mv is not None else None,
                                    ctypes.byref(wv) if wv is not None else None,
                                    _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(lse),
@@ -201,7 +206,7 @@ def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None,
         fire_arr = (ctypes.c_uint8 * B)(*[1 if f else 0 for f in fire])
     nbytes = workspace_bytes(MAD_OP_UPDATE, B * n_new, D, Hkv, d)
     w = _ws_for(x.device, nbytes, ws)
-    rc = lib.mad_memory_update(_ptr(x), _ptr(w_kv), pos_arr, fire_arr, B, n_new, D, Hkv, d,
+    rc = _load_library().mad_memory_update(_ptr(x), _ptr(w_kv), pos_arr, fire_arr, B, n_new, D, Hkv, d,
                                _dtype_code(x), float(rope_base), ctypes.byref(mv),
                                _ptr(w), w.numel(), _stream(x.device))
     _check(rc)
@@ -228,7 +233,7 @@ def verify_attn(q: torch.Tensor, k: torch.Tensor, vt: torch.Tensor, length, out=
         scale = d ** -0.5
     nbytes = workspace_bytes(MAD_OP_VERIFY, B, Hq, Hkv, d, T)
     w = _ws_for(q.device, nbytes, ws)
-    rc = lib.mad_verify_attn(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), _ptr(k), _ptr(vt),
+    rc = _load_library().mad_verify_attn(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), _ptr(k), _ptr(vt),
                              k.stride(0) if B > 1 else 0, k.stride(1), cap, _host_i32(length, B),
                              _ptr(out), _ptr(lse), _ptr(w), w.numel(), _stream(q.device))
     _check(rc)
@@ -247,7 +252,7 @@ def accept_greedy(logits: torch.Tensor, draft_tok: Optional[torch.Tensor], n_acc
         next_tok = torch.empty(B, dtype=torch.int32, device=dev)
     nbytes = workspace_bytes(MAD_OP_ACCEPT, B, 1, 1, 64, T, V)
     w = _ws_for(dev, nbytes, ws)
-    rc = lib.mad_accept_greedy(_ptr(logits), _dtype_code(logits), _ptr(draft_tok), B, T, V,
+    rc = _load_library().mad_accept_greedy(_ptr(logits), _dtype_code(logits), _ptr(draft_tok), B, T, V,
                                _ptr(n_accept), _ptr(next_tok), _ptr(w), w.numel(), _stream(dev))
     _check(rc)
     return n_accept, next_tok

@@ -6,107 +6,104 @@
 // (the working memory M_t of Sec. 3.1) and appends the new token's K/V to the
 // window ring in the same pass (Sec. 3.2).
 //
-// Work decomposition (split-K / flash-decoding):
-//   grid = n_splits * units workgroups, units = B * Hkv, 1-D.  Workgroup w
-//   handles unit u = w % units and split s = w / units, a contiguous range of
-//   `chunk` keys.  When units is a multiple of 8 every split of one unit lands
-//   on the same XCD (workgroups are dealt round-robin to the 8 XCDs), so a
-//   unit's partial results and its arrival counter stay in one L2.
-//   Inside a workgroup (256 threads) keys stream through LDS in tiles:
-//     1. every thread loads 16-byte pieces of the tile's K and V rows into
-//        registers (coalesced, issued one tile ahead of use) and stores them to
-//        LDS; K rows are XOR-swizzled by 16-byte chunk to keep the QK reads
-//        bank-conflict free;
-//     2. QK: thread <-> (key, query head) pair, full dot product from LDS with
-//        the query kept in registers (K is read once from HBM and shared by
-//        the G heads of the group);
-//     3. online softmax: per-head tile max by wave shuffles + a 4-wave LDS
-//        exchange, exp2 of pre-scaled scores, running (max, sum) rescaling;
-//     4. PV: thread <-> (feature pair, key subset) accumulating all G heads,
-//        V read once from LDS per thread and key.
-//   The last workgroup of a unit to finish (arrival counter) merges the
-//   n_splits partial (o, max, sum) triples with the log-sum-exp rule and
-//   writes the output, so the whole operation is a single launch.
+// Work decomposition (split-K / flash-decoding), grid = n_splits * units
+// workgroups of 256 threads, units = B * Hkv; workgroup w handles unit
+// u = w % units and the s = w / units-th range of `chunk` keys.
+//
+// Inside a workgroup keys stream through LDS in tiles of 8 KB of K + 8 KB of V
+// (64 keys for bf16, head_dim 64):
+//   * loads go straight from HBM into LDS (global_load_lds_dwordx4, 16 bytes a
+//     lane, no VGPR round trip) through a 4-stage ring, so up to three tiles
+//     are in flight while one is consumed; K rows are XOR-swizzled by 16-byte
+//     chunk on the way in so the QK reads are bank-conflict free;
+//   * QK: one wave per query head of the GQA group, one lane per key; the
+//     full head_dim dot product comes from LDS (K is read once from HBM and
+//     shared by the G heads);
+//   * online softmax on exp2 of pre-scaled scores; the per-head tile max is a
+//     single in-wave DPP/swizzle reduction; for the PV product the
+//     probabilities are rounded to bf16 and packed in key pairs (the softmax
+//     normaliser keeps the fp32 values);
+//   * PV: thread <-> (feature pair, key subset) for all G heads at once, two
+//     keys per v_dot2_f32_bf16 (fp32 accumulation);
+//   * the last workgroup of a unit (one arrival counter per unit, on its own
+//     256-byte line) pulls every split's partial (o, max, sum) into LDS with
+//     device-coherent direct loads in a single round trip and merges them with
+//     the log-sum-exp rule.
+#include <type_traits>
+
 #include "mad_device.h"
 #include "mad_internal.h"
 
 namespace mad {
 
 constexpr int kNT = 256;
+constexpr int kStages = 4;
+constexpr int kStageBytes = 16384;   // 8 KB of K + 8 KB of V
 
 template <typename T, int D, int G>
 struct DecodeCfg {
     static constexpr int ESZ = (int)sizeof(T);
-    static constexpr int VEC = 16 / ESZ;                        // elements per 16-byte chunk
-    static constexpr int CPR = D / VEC;                         // chunks per row
-    static constexpr int TILE = (16384 / (D * ESZ)) < 64 ? (16384 / (D * ESZ)) : 64;
-    static constexpr int RPL = kNT / CPR;                       // rows per load sweep
-    static constexpr int NLD = TILE / RPL;                      // load sweeps per tile
-    static constexpr int SW = (CPR < 8 ? CPR : 8) - 1;          // swizzle mask
-    static constexpr int PAIRS = TILE * G;
-    static constexpr int PPT = (PAIRS + kNT - 1) / kNT;         // score pairs per thread
-    static constexpr int DP = D / 2;                            // feature pairs
-    static constexpr int KS = kNT / DP;                         // key subsets in PV
-    static constexpr int KPS = TILE / KS;                       // keys per subset per tile
-    static constexpr int NW = kNT / 64;
-    // LDS carve-up (bytes): a fixed head for reductions, then one region
-    // shared by the tile buffers, the final reduction and the split merge.
-    static constexpr int SZ_HEAD = ((2 * NW + 2) * G * 4 + 15) / 16 * 16;
-    static constexpr int SZ_K = TILE * D * ESZ;
-    static constexpr int SZ_TILE = 2 * SZ_K + TILE * G * 4;
-    static constexpr int SZ_FIN = KS * G * D * 4;
-    static constexpr int SZ_CMB = kDecodeMaxSplits * G * 8;
-    static constexpr int SZ_UNI = SZ_TILE > SZ_FIN ? (SZ_TILE > SZ_CMB ? SZ_TILE : SZ_CMB)
-                                                   : (SZ_FIN > SZ_CMB ? SZ_FIN : SZ_CMB);
-    static constexpr int SMEM = SZ_HEAD + SZ_UNI;
-    static_assert((2 * NW + 2) * G * 4 <= SZ_HEAD, "lds head");
-    static_assert(D % VEC == 0 && kNT % CPR == 0 && TILE % RPL == 0, "tile shape");
-    static_assert(kNT % DP == 0 && TILE % KS == 0, "pv shape");
-    static_assert(kNT % G == 0, "group");
+    static constexpr int RB = D * ESZ;                 // bytes per K/V row
+    static constexpr int TILE = 8192 / RB;             // keys per tile
+    static constexpr int CPR = RB / 16;                // 16-byte chunks per row
+    static constexpr int SW = (CPR < 8 ? CPR : 8) - 1; // K swizzle mask
+    static constexpr int RPI = 1024 / RB;              // rows per wave load (64 lanes x 16 B)
+    static constexpr int LPT = 2;                      // K (and V) loads per thread per tile
+    static constexpr int PAIRS = TILE * G;             // (head, key) score pairs per tile
+    static constexpr int PPT = (PAIRS + kNT - 1) / kNT;
+    static constexpr int DP = D / 2;                   // feature pairs
+    static constexpr int KS = kNT / DP;                // key subsets in PV
+    static constexpr int KPS = TILE / KS;              // keys per subset per tile
+    static constexpr bool BF = std::is_same<T, bf16_t>::value;
+    // LDS layout: [stages | P | alpha | fin | O]; the merge reuses [stages]
+    static constexpr int OFF_P = kStages * kStageBytes;
+    static constexpr int SZ_P = TILE * G * 4;
+    static constexpr int OFF_ALPHA = OFF_P + SZ_P;
+    static constexpr int OFF_FIN = OFF_ALPHA + G * 4;
+    static constexpr int OFF_O = OFF_FIN + G * 8;
+    static constexpr int SZ_O = KS * G * D * 4;
+    static constexpr int SMEM = OFF_O + SZ_O;
+    static_assert(TILE * RB == 8192 && kNT / 64 * LPT * 1024 == 8192, "tile = 8 KB per tensor");
+    static_assert(KPS % 2 == 0 && kNT % DP == 0 && TILE % KS == 0, "pv shape");
+    static_assert(PAIRS % TILE == 0 && (kNT % TILE == 0), "score pair groups");
 };
 
-// q . k over one 16-byte chunk (VEC elements), q held as fp32 (F32) or as
-// packed bf16 pairs (BF16), accumulated in fp32.
-__device__ __forceinline__ float chunk_dot(const float *qf, const uint4 &kv, float acc, float) {
-    acc = fmaf(qf[0], __uint_as_float(kv.x), acc);
-    acc = fmaf(qf[1], __uint_as_float(kv.y), acc);
-    acc = fmaf(qf[2], __uint_as_float(kv.z), acc);
-    acc = fmaf(qf[3], __uint_as_float(kv.w), acc);
-    return acc;
+// vmcnt(n) for n in {0, 4, 8, 12} (the tile loads are the only vector memory
+// operations in flight inside the pipeline; 4 per tile and thread).
+__device__ __forceinline__ void wait_vmcnt(int n) {
+    switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+        case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
+        case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
+        default: __builtin_amdgcn_s_waitcnt(0x0F7C); break;   // 12
+    }
 }
 
 typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, a),
-                                           __builtin_bit_cast(bf16x2_v, b), c, false);
-}
-__device__ __forceinline__ float chunk_dot(const uint32_t *qp, const uint4 &kv, float acc, bf16_t) {
-    acc = dot2_bf16(qp[0], kv.x, acc);
-    acc = dot2_bf16(qp[1], kv.y, acc);
-    acc = dot2_bf16(qp[2], kv.z, acc);
-    acc = dot2_bf16(qp[3], kv.w, acc);
-    return acc;
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, a), __builtin_bit_cast(bf16x2_v, b), c,
+                                           false);
 }
 
-template <typename T> struct QReg;
-template <> struct QReg<float> { typedef float type; static constexpr int PER_CHUNK = 4; };
-template <> struct QReg<bf16_t> { typedef uint32_t type; static constexpr int PER_CHUNK = 4; };
+// Max over aligned groups of N consecutive lanes (all lanes must be active).
+template <int N> __device__ __forceinline__ float group_max(float v) {
+    if constexpr (N >= 2) v = fmaxf(v, xor_lane<1>(v));
+    if constexpr (N >= 4) v = fmaxf(v, xor_lane<2>(v));
+    if constexpr (N >= 8) v = fmaxf(v, xor_lane<4>(v));
+    if constexpr (N >= 16) v = fmaxf(v, xor_lane<8>(v));
+    if constexpr (N >= 32) v = fmaxf(v, xor_lane<16>(v));
+    if constexpr (N >= 64) v = fmaxf(v, xor_lane<32>(v));
+    return v;
+}
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kNT) void decode_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(kNT, 2) void decode_kernel(const DecodeArgs a) {
     using C = DecodeCfg<T, D, G>;
-    using QT = typename QReg<T>::type;
-    __shared__ __align__(16) unsigned char smem[C::SMEM];
-    // fixed head of LDS: per-wave reductions and per-head totals
-    float *sRedM = reinterpret_cast<float *>(smem);                  // [NW][G]
-    float *sRedL = sRedM + C::NW * G;                                 // [NW][G]
-    float *sFin = sRedL + C::NW * G;                                  // [G][2] (max, sum)
-    unsigned char *uni = smem + C::SZ_HEAD;                           // union region
-    uint4 *sK = reinterpret_cast<uint4 *>(uni);                       // [TILE][CPR] swizzled
-    uint4 *sV = reinterpret_cast<uint4 *>(uni + C::SZ_K);             // [TILE][CPR]
-    float *sP = reinterpret_cast<float *>(uni + 2 * C::SZ_K);         // [TILE][G]
-    float *sO = reinterpret_cast<float *>(uni);                       // [KS][G][D] after the tiles
-    float2 *sML = reinterpret_cast<float2 *>(uni);                    // [n_splits][G] in the merge
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char *sStage = smem;
+    float *sAlpha = reinterpret_cast<float *>(smem + C::OFF_ALPHA);   // [G]
+    float *sFin = reinterpret_cast<float *>(smem + C::OFF_FIN);       // [G][2]: max, sum
+    float *sO = reinterpret_cast<float *>(smem + C::OFF_O);           // [KS][G][D]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -128,168 +125,189 @@ __global__ __launch_bounds__(kNT) void decode_kernel(const DecodeArgs a) {
     const T *nk = has_new ? reinterpret_cast<const T *>(a.kn) + nrow : nullptr;
     const T *nv = has_new ? reinterpret_cast<const T *>(a.vn) + nrow : nullptr;
 
-    // the workgroup whose range holds the new token appends it to the window ring
-    if (has_new && k0 <= n - 1 && n - 1 < k1 && tid < 2 * C::CPR) {
-        int r = wst + wlen;
-        if (r >= w_cap) r -= w_cap;
-        const int ch = tid % C::CPR;
-        if (tid < C::CPR)
-            reinterpret_cast<uint4 *>(wk + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nk)[ch];
-        else
-            reinterpret_cast<uint4 *>(wv + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nv)[ch];
-    }
-
-    // ---- query of this thread's head (fixed per thread: kNT % G == 0) ----
-    const int g_me = tid % G;
-    QT qreg[C::CPR * 4];
-    {
-        const uint4 *qsrc = reinterpret_cast<const uint4 *>(
-            reinterpret_cast<const T *>(a.q) + ((size_t)b * a.Hq + (size_t)c * G + g_me) * D);
-        #pragma unroll
-        for (int ch = 0; ch < C::CPR; ++ch) {
-            uint4 v = qsrc[ch];
-            qreg[ch * 4 + 0] = __builtin_bit_cast(QT, v.x);
-            qreg[ch * 4 + 1] = __builtin_bit_cast(QT, v.y);
-            qreg[ch * 4 + 2] = __builtin_bit_cast(QT, v.z);
-            qreg[ch * 4 + 3] = __builtin_bit_cast(QT, v.w);
+    // ---- queries of this thread's score pairs (head g = pair / TILE) ----
+    // With 64-key tiles a wave's score pairs share one head, so its query row is
+    // wave-uniform and comes through the scalar cache (no vector-memory wait);
+    // otherwise each lane loads its own row.
+    constexpr int QW = D * C::ESZ / 4;   // 32-bit words of one query row
+    uint32_t qreg[C::PPT][QW];
+    #pragma unroll
+    for (int pp = 0; pp < C::PPT; ++pp) {
+        const int pr = tid + pp * kNT;
+        const int g = (pr < C::PAIRS ? pr : 0) / C::TILE;
+        const T *qrow = reinterpret_cast<const T *>(a.q) + ((size_t)b * a.Hq + (size_t)c * G + g) * D;
+        if constexpr (C::TILE == 64) {
+            load_uniform_dwords<QW>(qrow, qreg[pp]);
+        } else {
+            const uint4 *qs = reinterpret_cast<const uint4 *>(qrow);
+            #pragma unroll
+            for (int ch = 0; ch < C::CPR; ++ch) {
+                const uint4 v = qs[ch];
+                qreg[pp][4 * ch + 0] = v.x; qreg[pp][4 * ch + 1] = v.y;
+                qreg[pp][4 * ch + 2] = v.z; qreg[pp][4 * ch + 3] = v.w;
+            }
         }
     }
 
-    // ---- running softmax state (identical in every thread) and accumulators ----
-    float m_run[G];
-    float l_acc = 0.f;           // partial sum for head g_me over this thread's pairs
-    float o_acc[G][2];
-    #pragma unroll
-    for (int g = 0; g < G; ++g) { m_run[g] = -INFINITY; o_acc[g][0] = o_acc[g][1] = 0.f; }
+    // ---- append the new token to the window ring (the workgroup holding it) ----
+    if (has_new && k0 <= n - 1 && n - 1 < k1) {
+        if (tid < 2 * C::CPR) {
+            int r = wst + wlen;
+            if (r >= w_cap) r -= w_cap;
+            const int ch = tid % C::CPR;
+            if (tid < C::CPR)
+                reinterpret_cast<uint4 *>(wk + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nk)[ch];
+            else
+                reinterpret_cast<uint4 *>(wv + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nv)[ch];
+        }
+    }
+    // Vector-memory operations issued above are older than every tile load, so
+    // the per-tile vmcnt waits below also cover them.
 
-    const int ld_row = tid / C::CPR, ld_ch = tid % C::CPR;
-    const int pv_dp = tid % C::DP, pv_ks = tid / C::DP;
-
-    // address of logical key row kidx (K or V) of this unit
-    auto row_ptr = [&](int kidx, const T *mb, const T *wb, const T *nb) -> const T * {
-        if (kidx < mlen) return mb + (size_t)kidx * D;
-        int i = kidx - mlen;
+    // ---- tile loader: direct HBM -> LDS, 2 K + 2 V instructions per thread ----
+    auto row_src = [&](int kidx, bool is_v) -> const T * {
+        if (kidx >= k1) kidx = k1 - 1;   // rows past the range load a valid row (weight 0)
+        if (kidx < mlen) return (is_v ? mv : mk) + (size_t)kidx * D;
+        const int i = kidx - mlen;
         if (i < wlen) {
             int r = wst + i;
             if (r >= w_cap) r -= w_cap;
-            return wb + (size_t)r * D;
+            return (is_v ? wv : wk) + (size_t)r * D;
         }
-        return nb;
+        return is_v ? nv : nk;
+    };
+    auto issue_tile = [&](int tile_base, int stage) {
+        unsigned char *st = sStage + stage * kStageBytes;
+        #pragma unroll
+        for (int l = 0; l < C::LPT; ++l) {
+            const int inst = l * 4 + wave;                 // 1 KB block of the 8 KB tensor tile
+            const int row = inst * C::RPI + lane / C::CPR;
+            const int slot = lane % C::CPR;
+            const int kidx = tile_base + row;
+            const T *kp = row_src(kidx, false);
+            const T *vp = row_src(kidx, true);
+            // K: LDS slot `slot` of row `row` holds global chunk slot ^ (row & SW)
+            lds_stream16(reinterpret_cast<const uint4 *>(kp) + (slot ^ (row & C::SW)), st + inst * 1024);
+            lds_stream16(reinterpret_cast<const uint4 *>(vp) + slot, st + 8192 + inst * 1024);
+        }
     };
 
-    uint4 kreg[C::NLD], vreg[C::NLD];
-    auto load_tile = [&](int base) {
-        #pragma unroll
-        for (int l = 0; l < C::NLD; ++l) {
-            int kidx = base + l * C::RPL + ld_row;
-            if (kidx < k1) {
-                kreg[l] = reinterpret_cast<const uint4 *>(row_ptr(kidx, mk, wk, nk))[ld_ch];
-                vreg[l] = reinterpret_cast<const uint4 *>(row_ptr(kidx, mv, wv, nv))[ld_ch];
-            } else {
-                kreg[l] = make_uint4(0, 0, 0, 0);
-                vreg[l] = make_uint4(0, 0, 0, 0);
-            }
+    // ---- running state ----
+    float m_run[C::PPT], l_lane[C::PPT];
+    #pragma unroll
+    for (int pp = 0; pp < C::PPT; ++pp) { m_run[pp] = -INFINITY; l_lane[pp] = 0.f; }
+    float o_acc[G][2];
+    #pragma unroll
+    for (int g = 0; g < G; ++g) o_acc[g][0] = o_acc[g][1] = 0.f;
+    const int pv_dp = tid % C::DP, pv_ks = tid / C::DP;
+
+    const int ntiles = (k1 > k0) ? (k1 - k0 + C::TILE - 1) / C::TILE : 0;
+    int issued = 0;
+    for (; issued < ntiles && issued < kStages - 1; ++issued) issue_tile(k0 + issued * C::TILE, issued);
+
+    for (int t = 0; t < ntiles; ++t) {
+        wait_vmcnt(4 * (issued - t - 1));
+        __syncthreads();   // tile t is in LDS for every wave; stage (t-1) % kStages is free
+        if (issued < ntiles) {
+            issue_tile(k0 + issued * C::TILE, issued % kStages);
+            ++issued;
         }
-    };
+        const unsigned char *st = sStage + (t % kStages) * kStageBytes;
+        const int base = k0 + t * C::TILE;
 
-    if (k0 < k1) load_tile(k0);
-
-    for (int base = k0; base < k1; base += C::TILE) {
-        __syncthreads();  // the previous tile is fully consumed
-        #pragma unroll
-        for (int l = 0; l < C::NLD; ++l) {
-            int row = l * C::RPL + ld_row;
-            sK[row * C::CPR + (ld_ch ^ (row & C::SW))] = kreg[l];
-            sV[row * C::CPR + ld_ch] = vreg[l];
-        }
-        if (base + C::TILE < k1) load_tile(base + C::TILE);   // prefetch the next tile
-        __syncthreads();
-
-        // ---- QK: scores of (key j, head g) pairs, j = pr / G, g = pr % G ----
-        float sc[C::PPT];
-        float tmax = -INFINITY;
+        // ---- QK and softmax statistics: pair (g = pr / TILE, j = pr % TILE) ----
         #pragma unroll
         for (int pp = 0; pp < C::PPT; ++pp) {
-            int pr = tid + pp * kNT;
-            sc[pp] = -INFINITY;
-            if (pr < C::PAIRS) {
-                int j = pr / G;
-                float acc = 0.f;
-                #pragma unroll
-                for (int ch = 0; ch < C::CPR; ++ch) {
-                    uint4 kv = sK[j * C::CPR + (ch ^ (j & C::SW))];
-                    acc = chunk_dot(&qreg[ch * 4], kv, acc, T{});
+            const int pr = tid + pp * kNT;
+            const bool act = pr < C::PAIRS;
+            const int j = pr % C::TILE, g = (act ? pr : 0) / C::TILE;
+            float acc = 0.f;
+            const uint4 *krow = reinterpret_cast<const uint4 *>(st + j * C::RB);
+            #pragma unroll
+            for (int ch = 0; ch < C::CPR; ++ch) {
+                const uint4 kv = krow[ch ^ (j & C::SW)];
+                if constexpr (C::BF) {
+                    acc = dot2_bf16(qreg[pp][4 * ch + 0], kv.x, acc);
+                    acc = dot2_bf16(qreg[pp][4 * ch + 1], kv.y, acc);
+                    acc = dot2_bf16(qreg[pp][4 * ch + 2], kv.z, acc);
+                    acc = dot2_bf16(qreg[pp][4 * ch + 3], kv.w, acc);
+                } else {
+                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 0]), __uint_as_float(kv.x), acc);
+                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 1]), __uint_as_float(kv.y), acc);
+                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 2]), __uint_as_float(kv.z), acc);
+                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 3]), __uint_as_float(kv.w), acc);
                 }
-                if (base + j < k1) sc[pp] = acc * a.scale_log2;
             }
-            tmax = fmaxf(tmax, sc[pp]);
-        }
-        // per-head tile max: lanes sharing lane % G hold the same head
-        tmax = strided_max<G>(tmax);
-        if (lane < G) sRedM[wave * G + lane] = tmax;
-        __syncthreads();
-        float alpha[G];
-        float m_me = 0.f, alpha_me = 0.f;
-        #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            float mt = sRedM[g];
-            #pragma unroll
-            for (int w = 1; w < C::NW; ++w) mt = fmaxf(mt, sRedM[w * G + g]);
-            float mn = fmaxf(m_run[g], mt);
-            alpha[g] = exp2f(m_run[g] - mn);   // 0 while m_run is -inf
-            m_run[g] = mn;
-            if (g == g_me) { m_me = mn; alpha_me = alpha[g]; }
-        }
-        float lsum = 0.f;
-        #pragma unroll
-        for (int pp = 0; pp < C::PPT; ++pp) {
-            int pr = tid + pp * kNT;
-            if (pr < C::PAIRS) {
-                float p = exp2f(sc[pp] - m_me);
-                sP[pr] = p;
-                lsum += p;
-            }
-        }
-        l_acc = l_acc * alpha_me + lsum;
-        __syncthreads();
-
-        // ---- PV: o[g][2dp..2dp+1] += sum over this subset's keys of p[j][g] * V[j] ----
-        #pragma unroll
-        for (int g = 0; g < G; ++g) { o_acc[g][0] *= alpha[g]; o_acc[g][1] *= alpha[g]; }
-        #pragma unroll 4
-        for (int kk = 0; kk < C::KPS; ++kk) {
-            int j = pv_ks * C::KPS + kk;
-            float v0, v1;
-            if constexpr (sizeof(T) == 2) {
-                uint32_t w = reinterpret_cast<const uint32_t *>(sV)[j * (D / 2) + pv_dp];
-                v0 = bf16_lo(w); v1 = bf16_hi(w);
+            const float sc = (base + j < k1) ? acc * a.scale_log2 : -INFINITY;
+            const float tmax = group_max<C::TILE>(sc);
+            const float mn = fmaxf(m_run[pp], tmax);      // finite: every tile holds a valid key
+            const float alpha = exp2f(m_run[pp] - mn);
+            m_run[pp] = mn;
+            const float p = exp2f(sc - mn);
+            if constexpr (C::BF) {
+                // PV consumes the probabilities rounded to bf16 and packed by key
+                // pairs; the normaliser below sums the fp32 values
+                const uint32_t pb = (uint32_t)f32_to_bf16(p);
+                const uint32_t pn = (uint32_t)__float_as_int(xor_lane<1>(__int_as_float((int)pb)));
+                if (act && (j & 1) == 0)
+                    reinterpret_cast<uint32_t *>(smem + C::OFF_P)[(j >> 1) * G + g] = pb | (pn << 16);
             } else {
-                float2 w = reinterpret_cast<const float2 *>(sV)[j * (D / 2) + pv_dp];
-                v0 = w.x; v1 = w.y;
+                if (act) reinterpret_cast<float *>(smem + C::OFF_P)[j * G + g] = p;
             }
-            const float *pj = sP + j * G;
-            #pragma unroll
-            for (int g = 0; g < G; ++g) {
-                float p = pj[g];
-                o_acc[g][0] = fmaf(p, v0, o_acc[g][0]);
-                o_acc[g][1] = fmaf(p, v1, o_acc[g][1]);
+            l_lane[pp] = fmaf(l_lane[pp], alpha, p);
+            if (act && j == 0) sAlpha[g] = alpha;
+        }
+        __syncthreads();   // P and alpha ready
+
+        // ---- PV ----
+        float al[G];
+        #pragma unroll
+        for (int g = 0; g < G; ++g) al[g] = sAlpha[g];
+        #pragma unroll
+        for (int g = 0; g < G; ++g) { o_acc[g][0] *= al[g]; o_acc[g][1] *= al[g]; }
+        const unsigned char *sv = st + 8192;
+        #pragma unroll
+        for (int kk = 0; kk < C::KPS; kk += 2) {
+            const int j0 = pv_ks * C::KPS + kk;
+            if constexpr (C::BF) {
+                const uint32_t w0 = reinterpret_cast<const uint32_t *>(sv + j0 * C::RB)[pv_dp];
+                const uint32_t w1 = reinterpret_cast<const uint32_t *>(sv + (j0 + 1) * C::RB)[pv_dp];
+                const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x05040100u);   // feature 2dp, keys j0 | j0+1
+                const uint32_t hi = __builtin_amdgcn_perm(w1, w0, 0x07060302u);   // feature 2dp+1
+                const uint32_t *pj = reinterpret_cast<const uint32_t *>(smem + C::OFF_P) + (j0 >> 1) * G;
+                #pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const uint32_t pg = pj[g];
+                    o_acc[g][0] = dot2_bf16(pg, lo, o_acc[g][0]);
+                    o_acc[g][1] = dot2_bf16(pg, hi, o_acc[g][1]);
+                }
+            } else {
+                #pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const float2 w = reinterpret_cast<const float2 *>(sv + (j0 + e) * C::RB)[pv_dp];
+                    const float *pj = reinterpret_cast<const float *>(smem + C::OFF_P) + (j0 + e) * G;
+                    #pragma unroll
+                    for (int g = 0; g < G; ++g) {
+                        o_acc[g][0] = fmaf(pj[g], w.x, o_acc[g][0]);
+                        o_acc[g][1] = fmaf(pj[g], w.y, o_acc[g][1]);
+                    }
+                }
             }
         }
     }
 
-    // ---- reduce inside the workgroup ----
-    l_acc = strided_sum<G>(l_acc);
-    if (lane < G) sRedL[wave * G + lane] = l_acc;
-    __syncthreads();   // tiles consumed, sRedL complete
-    if (tid < G) {
-        float t = 0.f;
+    // ---- per-head totals: lanes of one pair group share a head ----
+    #pragma unroll
+    for (int pp = 0; pp < C::PPT; ++pp) {
+        const int pr = tid + pp * kNT;
+        float lt = l_lane[pp];
         #pragma unroll
-        for (int w = 0; w < C::NW; ++w) t += sRedL[w * G + tid];
-        float mm = 0.f;
-        #pragma unroll
-        for (int g = 0; g < G; ++g) if (g == tid) mm = m_run[g];
-        sFin[2 * tid] = mm;
-        sFin[2 * tid + 1] = t;
+        for (int k = 1; k < C::TILE; k <<= 1) lt += __shfl_xor(lt, k, 64);
+        if (pr < C::PAIRS && pr % C::TILE == 0) {
+            const int g = pr / C::TILE;
+            sFin[2 * g] = m_run[pp];   // -inf when this split had no keys
+            sFin[2 * g + 1] = lt;
+        }
     }
     #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -303,96 +321,108 @@ __global__ __launch_bounds__(kNT) void decode_kernel(const DecodeArgs a) {
     T *out = reinterpret_cast<T *>(a.out) + head0 * D;
     if (n_splits == 1) {
         for (int idx = tid; idx < G * D; idx += kNT) {
-            int g = idx / D;
+            const int g = idx / D;
             float o = 0.f;
             #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) o += sO[ks * G * D + idx];
-            float mm = sFin[2 * g], l = sFin[2 * g + 1];
+            const float mm = sFin[2 * g], l = sFin[2 * g + 1];
             Elem<T>::store1(out + idx, l > 0.f ? o / l : 0.f);
             if (a.lse && (idx % D) == 0) a.lse[head0 + g] = l > 0.f ? (mm + log2f(l)) * kLn2 : -INFINITY;
         }
         return;
     }
 
-    // ---- write this split's partial (unnormalised o, running max, running sum) ----
-    float *po = a.part_o + ((size_t)u * n_splits + s) * G * D;
+    // ---- partial of this split: unit block = [o: n_splits][G][D] [ml: n_splits][G][2] ----
+    float *blk = a.part + (size_t)u * a.part_stride;
+    float *po = blk + (size_t)s * G * D;
     for (int idx = tid; idx < G * D; idx += kNT) {
         float o = 0.f;
         #pragma unroll
         for (int ks = 0; ks < C::KS; ++ks) o += sO[ks * G * D + idx];
-        po[idx] = o;
+        store_agent(po + idx, o);
     }
-    if (tid < G)
-        reinterpret_cast<float2 *>(a.part_ml)[((size_t)u * n_splits + s) * G + tid] =
-            make_float2(sFin[2 * tid], sFin[2 * tid + 1]);
-    __threadfence();           // release the partials at device scope
+    if (tid < 2 * G) store_agent(blk + (size_t)n_splits * G * D + (size_t)s * 2 * G + tid, sFin[tid]);
+    wait_vm_stores();
     __syncthreads();
     __shared__ int s_last;
     if (tid == 0) {
-        unsigned prev = atomicAdd(&a.counters[u], 1u);
-        s_last = (prev == (unsigned)(n_splits - 1));
+        unsigned *cnt = a.counters + (size_t)u * kCounterStride;
+        const int last = arrive(cnt) == (unsigned)(n_splits - 1);
+        if (last) reset_counter(cnt);
+        s_last = last;
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();           // acquire the other workgroups' partials
 
-    // ---- last workgroup of the unit: log-sum-exp merge of the splits ----
-    const float2 *pml = reinterpret_cast<const float2 *>(a.part_ml) + (size_t)u * n_splits * G;
-    for (int idx = tid; idx < n_splits * G; idx += kNT) sML[idx] = pml[idx];
+    // ---- last workgroup: pull all partials into LDS in one round trip ----
+    const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
+    for (int off = wave * 1024; off < nbytes; off += 4096) {
+        if (off + lane * 16 < nbytes)
+            lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, sStage + off);
+    }
+    wait_vmcnt(0);
     __syncthreads();
-    const float *pob = a.part_o + (size_t)u * n_splits * G * D;
+    const float *lo = reinterpret_cast<const float *>(sStage);
+    const float *lml = lo + (size_t)n_splits * G * D;
     for (int idx = tid; idx < G * D; idx += kNT) {
-        int g = idx / D;
+        const int g = idx / D;
         float M = -INFINITY;
-        for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, sML[sp * G + g].x);
+        for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, lml[sp * 2 * G + 2 * g]);
         float acc = 0.f, L = 0.f;
         if (M != -INFINITY) {
-            #pragma unroll 8
             for (int sp = 0; sp < n_splits; ++sp) {
-                float2 ml = sML[sp * G + g];
-                float wgt = exp2f(ml.x - M);
-                L = fmaf(wgt, ml.y, L);
-                acc = fmaf(wgt, pob[(size_t)sp * G * D + idx], acc);
+                const float wgt = exp2f(lml[sp * 2 * G + 2 * g] - M);
+                L = fmaf(wgt, lml[sp * 2 * G + 2 * g + 1], L);
+                acc = fmaf(wgt, lo[(size_t)sp * G * D + idx], acc);
             }
         }
         Elem<T>::store1(out + idx, L > 0.f ? acc / L : 0.f);
         if (a.lse && (idx % D) == 0) a.lse[head0 + g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
     }
-    if (tid == 0) a.counters[u] = 0u;   // leave the counter ready for the next call
 }
 
 // ------------------------------------------------------------------ host ----
 
-DecodePlan plan_decode(int B, int Hkv, const int *n_keys) {
+int decode_max_splits(int d, int G) {
+    const int cap = kStages * kStageBytes / (G * (d + 2) * 4);   // merge block must fit the stage LDS
+    return cap < kDecodeMaxSplits ? cap : kDecodeMaxSplits;
+}
+
+static int decode_tile(int dtype, int d) { return 8192 / (d * (dtype == MAD_BF16 ? 2 : 4)); }
+
+DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys) {
     DecodePlan p;
     p.units = B * Hkv;
     p.n_max = 0;
     for (int b = 0; b < B; ++b) p.n_max = n_keys[b] > p.n_max ? n_keys[b] : p.n_max;
-    int fill = (kDecodeTargetWGs + p.units - 1) / p.units;
-    if (fill > kDecodeMaxSplits) fill = kDecodeMaxSplits;
-    if (fill < 1) fill = 1;
-    int chunk = (p.n_max + fill - 1) / fill;
-    chunk = ((chunk + kDecodeChunkQuant - 1) / kDecodeChunkQuant) * kDecodeChunkQuant;
-    if (chunk < kDecodeMinChunk) chunk = kDecodeMinChunk;
-    int ns = (p.n_max + chunk - 1) / chunk;
+    const int tile = decode_tile(dtype, d);
+    int ns = (kDecodeTargetWGs + p.units - 1) / p.units;
+    const int cap = decode_max_splits(d, G);
+    if (ns > cap) ns = cap;
     if (ns < 1) ns = 1;
-    p.n_splits = ns;
+    int chunk = (p.n_max + ns - 1) / ns;
+    chunk = ((chunk + tile - 1) / tile) * tile;
+    if (chunk < tile) chunk = tile;
+    ns = (p.n_max + chunk - 1) / chunk;
+    p.n_splits = ns < 1 ? 1 : ns;
     p.chunk = chunk;
     return p;
 }
 
+// floats per unit block, rounded to 256 bytes (the merge loads whole 16-byte pieces)
+size_t decode_part_stride(int d, int G) {
+    return ((size_t)decode_max_splits(d, G) * G * (d + 2) + 63) / 64 * 64;
+}
+
 size_t decode_ws_bytes(int B, int Hq, int Hkv, int d) {
-    size_t units = (size_t)B * Hkv;
-    int G = Hq / Hkv;
-    size_t fill = (kDecodeTargetWGs + units - 1) / units;
-    if (fill > (size_t)kDecodeMaxSplits) fill = kDecodeMaxSplits;
-    return align256(units * 4) + align256(units * fill * G * d * 4) + align256(units * fill * G * 8);
+    return kCounterRegionBytes + (size_t)B * Hkv * decode_part_stride(d, Hq / Hkv) * 4 + 256;
 }
 
 template <typename T, int D, int G>
 static hipError_t launch_t(const DecodeArgs &a, hipStream_t st) {
+    using C = DecodeCfg<T, D, G>;
     dim3 grid((unsigned)(a.units * a.n_splits)), block(kNT);
-    hipLaunchKernelGGL((decode_kernel<T, D, G>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_kernel<T, D, G>), grid, block, C::SMEM, st, a);
     return hipGetLastError();
 }
 

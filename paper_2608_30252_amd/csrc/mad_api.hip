@@ -107,6 +107,8 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     if (mem && (rc = check_view(mem, "mem", B, Hkv, d, dtype, false, false))) return rc;
     if (win && (rc = check_view(win, "win", B, Hkv, d, dtype, true, k_new != nullptr))) return rc;
     const int G = Hq / Hkv;
+    if ((size_t)B * Hkv > (size_t)mad::kCounterLines)
+        return fail(MAD_ENOTSUP, "B*Hkv=%d too large for the counter region", B * Hkv);
 
     mad::DecodeArgs a;
     memset(&a, 0, sizeof(a));
@@ -117,7 +119,7 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
         a.wstart[b] = (win && win->start) ? win->start[b] : 0;
         n_keys[b] = a.mlen[b] + a.wlen[b] + (k_new ? 1 : 0);
     }
-    mad::DecodePlan p = mad::plan_decode(B, Hkv, n_keys);
+    mad::DecodePlan p = mad::plan_decode(B, Hkv, G, d, dtype, n_keys);
     size_t need = p.n_splits > 1 ? mad::decode_ws_bytes(B, Hq, Hkv, d) : 0;
     if (need > 0) {
         if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
@@ -145,13 +147,9 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     a.n_splits = p.n_splits;
     a.chunk = p.chunk;
     if (need > 0) {
-        size_t units = (size_t)p.units;
-        char *base = (char *)ws;
-        a.counters = (unsigned *)base;
-        size_t fill = (mad::kDecodeTargetWGs + units - 1) / units;
-        if (fill > (size_t)mad::kDecodeMaxSplits) fill = mad::kDecodeMaxSplits;
-        a.part_o = (float *)(base + mad::align256(units * 4));
-        a.part_ml = (float *)(base + mad::align256(units * 4) + mad::align256(units * fill * G * d * 4));
+        a.counters = (unsigned *)ws;
+        a.part = (float *)((char *)ws + mad::kCounterRegionBytes);
+        a.part_stride = (int64_t)mad::decode_part_stride(d, G);
     }
     return hip_status(mad::launch_decode(a, dtype, d, G, (hipStream_t)stream), "decode launch");
 }

@@ -109,4 +109,58 @@ template <int STRIDE> __device__ __forceinline__ float strided_sum(float v) {
     return v;
 }
 
+// ---- cross-workgroup hand-off without cache maintenance -------------------
+// Split partials are written with agent-scope atomic stores (write-through to
+// the device-coherent level, past the per-XCD L2), the writer waits for their
+// completion (vmcnt(0)), and only then bumps the arrival counter.  The last
+// arriving workgroup reads the partials with agent-scope atomic loads.  This
+// is the ordering the memory model's own release sequence relies on, without
+// its L2 writeback and -- worse for a streaming kernel -- the whole-L2
+// invalidate that a full __threadfence() performs in every workgroup.
+__device__ __forceinline__ void store_agent(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_agent(const float *p) {
+    return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void wait_vm_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); /* vmcnt(0) */ }
+__device__ __forceinline__ unsigned arrive(unsigned *counter) {
+    return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void reset_counter(unsigned *counter) {
+    __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---- direct HBM -> LDS loads (gfx950 global_load_lds_dwordx4) ------------
+// Lane i of the wave writes its 16 bytes at lds_base + 16 * i; lds_base must be
+// wave-uniform.  The "coherent" form reads at device scope (sc1), for data
+// written by other workgroups of the same launch.
+//
+// The streaming form is issued through inline assembly on purpose: the
+// compiler cannot tell which LDS bytes an in-flight direct load will write, so
+// for the builtin it places a wait for *every* outstanding vector-memory
+// operation before the next LDS read, which serialises a multi-stage ring.
+// Callers of lds_stream16 therefore own the waits: s_waitcnt vmcnt(n) plus a
+// workgroup barrier before the stage is read.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+__device__ __forceinline__ void lds_stream16(const void *src, void *lds_base) {
+    const uint32_t m = __builtin_amdgcn_readfirstlane(lds_addr(lds_base));
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(m) : "memory", "m0");
+}
+// Load N dwords at a wave-uniform address through the scalar cache (s_load).
+template <int N>
+__device__ __forceinline__ void load_uniform_dwords(const void *p, uint32_t (&out)[N]) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uintptr_t)p >> 32));
+    const __attribute__((address_space(4))) uint32_t *c =
+        (const __attribute__((address_space(4))) uint32_t *)(((uint64_t)hi << 32) | lo);
+    #pragma unroll
+    for (int i = 0; i < N; ++i) out[i] = c[i];
+}
+__device__ __forceinline__ void lds_load16_coherent(const void *src, void *lds_base) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0, 16);
+}
+
 }  // namespace mad

@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/mad.h"
+#include "mad.h"
 
 namespace mad {
 
@@ -27,6 +27,17 @@ constexpr int kDecodeTargetWGs = MAD_DECODE_TARGET_WGS;
 constexpr int kDecodeMinChunk = MAD_DECODE_MIN_CHUNK;
 constexpr int kDecodeChunkQuant = MAD_DECODE_CHUNK_QUANT;
 constexpr int kDecodeMaxSplits = 256;
+// Every workspace starts with a fixed counter region that holds nothing but
+// arrival counters (one per 256-byte line) and that every kernel leaves at
+// zero.  Its layout therefore never overlaps the partial results of a call
+// with other shapes.  Split partials follow it.
+constexpr size_t kCounterRegionBytes = (size_t)1 << 20;
+constexpr int kCounterStride = 64;   // unsigned ints per counter line
+constexpr int kCounterLines = (int)(kCounterRegionBytes / (kCounterStride * 4));
+#ifndef MAD_ARRIVE_GROUP
+#define MAD_ARRIVE_GROUP 8
+#endif
+constexpr int kArriveGroup = MAD_ARRIVE_GROUP;   // splits per arrival group
 
 struct DecodeArgs {
     const void *q;
@@ -37,9 +48,9 @@ struct DecodeArgs {
     void *wk, *wv;        // local window: ring
     int64_t w_seq, w_head;
     const void *kn, *vn;  // current token K/V [B][Hkv][D] or null
-    float *part_o;        // [units][n_splits][G][D]
-    float *part_ml;       // [units][n_splits][G][2]
-    unsigned *counters;   // [units]
+    float *part;          // split partials, one block of part_stride floats per unit
+    int64_t part_stride;
+    unsigned *counters;   // counter region: unit u on line u
     float scale_log2;     // softmax scale * log2(e)
     int Hq, Hkv, units, n_splits, chunk, w_cap;
     int mlen[kMaxB], wstart[kMaxB], wlen[kMaxB];
@@ -49,7 +60,9 @@ struct DecodePlan {
     int units, n_splits, chunk, n_max;
 };
 
-DecodePlan plan_decode(int B, int Hkv, const int *n_keys);
+DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys);
+int decode_max_splits(int d, int G);
+size_t decode_part_stride(int d, int G);
 size_t decode_ws_bytes(int B, int Hq, int Hkv, int d);
 hipError_t launch_decode(const DecodeArgs &a, int dtype, int d, int G, hipStream_t st);
 

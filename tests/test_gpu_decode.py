@@ -145,3 +145,29 @@ def test_deterministic():
     b = _case(torch.bfloat16, 1, 32, 8, 64, 2048, 1023, 1056, 3, seed=12)
     assert torch.equal(a[0].view(torch.int16), b[0].view(torch.int16))
     assert torch.equal(a[1], b[1])
+
+
+def test_one_workspace_serves_calls_of_different_shapes():
+    """Calls of different shapes share one workspace: counters must never sit
+    where another shape's call wrote split partials."""
+    import paper_2608_30252_amd as mad
+    shapes = [(2, 16, 1, 64), (8, 64, 8, 128), (2, 16, 1, 64), (4, 16, 2, 128), (1, 32, 8, 64)]
+    nbytes = max(mad.workspace_bytes(mad.MAD_OP_DECODE, *s) for s in shapes)
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    for i, (B, Hq, Hkv, d) in enumerate(shapes * 2):
+        _case_ws(ws, B, Hq, Hkv, d, seed=100 + i)
+
+
+def _case_ws(ws, B, Hq, Hkv, d, seed):
+    import oracle
+    import paper_2608_30252_amd as mad
+    from paper_2608_30252_amd import synth
+    n = 700
+    q = synth.normal((B, Hq, d), seed * 10 + 1)
+    k = synth.normal((B, Hkv, n, d), seed * 10 + 2)
+    v = synth.normal((B, Hkv, n, d), seed * 10 + 3)
+    out, lse = mad.draft_decode_attn(q.cuda(), mad.KV(k.cuda(), v.cuda(), [n] * B), None, ws=ws)
+    o_ref, lse_ref = oracle.attend_batched(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                           np.full(B, n), d ** -0.5)
+    check_out(to_np(out), o_ref, True, f"out B{B} Hq{Hq} Hkv{Hkv} d{d}")
+    check(to_np(lse), lse_ref, F32_ATOL, None, "lse")
