@@ -3,6 +3,7 @@
 // anything is enqueued; no exception leaves this file.
 #include <stdarg.h>
 #include <stdio.h>
+#include <math.h>
 #include <string.h>
 
 #include "mad_internal.h"
@@ -86,6 +87,9 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
         case MAD_OP_DECODE:
             if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128)) return 0;
             return mad::decode_ws_bytes(B, Hq, Hkv, d);
+        case MAD_OP_UPDATE:   // B = rows (B * n_new), Hq = D
+            if (B < 1 || B > MAD_MAX_UPDATE_ROWS || Hq < 64 || Hq % 64 || Hkv < 1 || (d != 64 && d != 128)) return 0;
+            return mad::update_ws_bytes(B, Hq, Hkv, d);
         default:
             (void)T;
             return 0;
@@ -154,9 +158,60 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     return hip_status(mad::launch_decode(a, dtype, d, G, (hipStream_t)stream), "decode launch");
 }
 
-int mad_memory_update(const void *, const void *, const int32_t *, const uint8_t *, int, int, int, int,
-                      int, int, double, const mad_kv_view *, void *, size_t, void *) {
-    return fail(MAD_ENOTSUP, "mad_memory_update: not built yet");
+int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const uint8_t *fire, int B, int n_new,
+                      int D, int Hkv, int d, int dtype, double rope_base, const mad_kv_view *mem, void *ws,
+                      size_t ws_bytes, void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (n_new < 1 || B * n_new > MAD_MAX_UPDATE_ROWS)
+        return fail(MAD_EINVAL, "B*n_new=%d outside [1, %d]", B * n_new, MAD_MAX_UPDATE_ROWS);
+    if (dtype != MAD_F32 && dtype != MAD_BF16) return fail(MAD_ENOTSUP, "dtype %d not supported", dtype);
+    if (d != 64 && d != 128) return fail(MAD_ENOTSUP, "head_dim %d not supported (64 or 128)", d);
+    if (Hkv < 1 || 2 * Hkv > mad::kCounterLines) return fail(MAD_EINVAL, "Hkv=%d", Hkv);
+    if (D < 64 || D % 64) return fail(MAD_EINVAL, "D=%d must be a positive multiple of 64", D);
+    if (!x || !w_kv || !pos || !mem) return fail(MAD_EINVAL, "null x, w_kv, pos or mem");
+    if (!aligned16(x) || !aligned16(w_kv)) return fail(MAD_EINVAL, "x/w_kv not 16-byte aligned");
+    if (!(rope_base > 1.0) || rope_base != rope_base || rope_base > 1e300)
+        return fail(MAD_EINVAL, "rope_base must be finite and > 1");
+    int rc = check_view(mem, "mem", B, Hkv, d, dtype, false, false);
+    if (rc) return rc;
+    for (int b = 0; b < B; ++b) {
+        const bool f = fire ? fire[b] != 0 : true;
+        if (f && mem->len[b] + n_new > mem->cap)
+            return fail(MAD_EINVAL, "mem: len[%d]=%d + n_new=%d exceeds cap %d", b, mem->len[b], n_new, mem->cap);
+    }
+    const int R = B * n_new;
+    mad::UpdateArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.w = w_kv;
+    a.mk = mem->k;
+    a.mv = mem->v;
+    a.m_seq = mem->seq_stride;
+    a.m_head = mem->head_stride;
+    a.log2_base = log2(rope_base);
+    a.R = R;
+    a.n_new = n_new;
+    a.D = D;
+    a.Hkv = Hkv;
+    a.d = d;
+    for (int b = 0; b < B; ++b) {
+        a.mlen[b] = mem->len[b];
+        a.fire[b] = (unsigned char)(fire ? (fire[b] != 0) : 1);
+    }
+    for (int r = 0; r < R; ++r) a.pos[r] = pos[r];
+    if (dtype == MAD_BF16) {
+        mad::UpdatePlan p = mad::plan_update(R, D, Hkv, d);
+        const size_t need = mad::update_ws_bytes(R, D, Hkv, d);
+        if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
+        if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
+        if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
+        a.KS = p.KS;
+        a.kc = p.kc;
+        a.counters = (unsigned *)ws;
+        a.part = (float *)((char *)ws + mad::kCounterRegionBytes);
+        a.part_stride = (int64_t)mad::update_part_stride(R, d, p.KS);
+    }
+    return hip_status(mad::launch_update(a, dtype, (hipStream_t)stream), "memory update launch");
 }
 
 int mad_verify_attn(const void *, int, int, int, int, int, int, float, const void *, const void *, int64_t,

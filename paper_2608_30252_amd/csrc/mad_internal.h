@@ -66,6 +66,32 @@ size_t decode_part_stride(int d, int G);
 size_t decode_ws_bytes(int B, int Hq, int Hkv, int d);
 hipError_t launch_decode(const DecodeArgs &a, int dtype, int d, int G, hipStream_t st);
 
+// ---------------------------------------------------------------- update ----
+constexpr size_t kUpdateMergeBytes = 65536;   // LDS for the split merge
+
+struct UpdateArgs {
+    const void *x, *w;    // [R][D] slot rows, [2*Hkv*d][D] mirrored projections
+    void *mk, *mv;        // memory segment to append to
+    int64_t m_seq, m_head;
+    float *part;          // split partials: one block of part_stride floats per head block
+    int64_t part_stride;
+    unsigned *counters;   // counter region: head block hb on line hb
+    double log2_base;     // log2 of the RoPE base
+    int R, n_new, D, Hkv, d, KS, kc;
+    int mlen[kMaxB];
+    int pos[MAD_MAX_UPDATE_ROWS];
+    unsigned char fire[kMaxB];
+};
+
+struct UpdatePlan {
+    int KS, kc;   // k-splits and the input-width chunk of each
+};
+
+UpdatePlan plan_update(int R, int D, int Hkv, int d);
+size_t update_part_stride(int R, int d, int KS);
+size_t update_ws_bytes(int R, int D, int Hkv, int d);
+hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st);
+
 // ws layout helpers: counters first (256-byte aligned), then partials.
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
