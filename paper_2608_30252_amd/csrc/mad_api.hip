@@ -90,8 +90,10 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
         case MAD_OP_UPDATE:   // B = rows (B * n_new), Hq = D
             if (B < 1 || B > MAD_MAX_UPDATE_ROWS || Hq < 64 || Hq % 64 || Hkv < 1 || (d != 64 && d != 128)) return 0;
             return mad::update_ws_bytes(B, Hq, Hkv, d);
+        case MAD_OP_VERIFY:
+            if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128) || T < 1) return 0;
+            return mad::verify_ws_bytes(B, Hq, Hkv, d, T);
         default:
-            (void)T;
             return 0;
     }
 }
@@ -214,9 +216,58 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
     return hip_status(mad::launch_update(a, dtype, (hipStream_t)stream), "memory update launch");
 }
 
-int mad_verify_attn(const void *, int, int, int, int, int, int, float, const void *, const void *, int64_t,
-                    int64_t, int32_t, const int32_t *, void *, float *, void *, size_t, void *) {
-    return fail(MAD_ENOTSUP, "mad_verify_attn: not built yet");
+int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale, const void *k,
+                    const void *vt, int64_t seq_stride, int64_t head_stride, int32_t cap, const int32_t *len,
+                    void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    int rc = check_heads(B, Hq, Hkv, d, dtype);
+    if (rc) return rc;
+    if (dtype != MAD_BF16) return fail(MAD_ENOTSUP, "verify attention runs in bf16 only");
+    const int G = Hq / Hkv;
+    if (T < 1 || T * G > MAD_MAX_VERIFY_ROWS)
+        return fail(MAD_EINVAL, "T=%d: T*G=%d must be in [1, %d]", T, T * G, MAD_MAX_VERIFY_ROWS);
+    if (!q || !k || !vt || !out || !len) return fail(MAD_EINVAL, "null q, k, vt, out or len");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(vt) || !aligned16(out))
+        return fail(MAD_EINVAL, "q/k/vt/out not 16-byte aligned");
+    if (!(scale > 0.f) || scale != scale) return fail(MAD_EINVAL, "scale must be positive");
+    if (cap < 8 || cap % 8) return fail(MAD_EINVAL, "cap=%d must be a positive multiple of 8", cap);
+    if (head_stride < (int64_t)cap * d || head_stride % 8 || seq_stride < 0 || seq_stride % 8)
+        return fail(MAD_EINVAL, "bad strides (seq %lld, head %lld) for cap %d, d %d", (long long)seq_stride,
+                    (long long)head_stride, cap, d);
+    if (B > 1 && seq_stride != 0 && seq_stride < (int64_t)Hkv * head_stride)
+        return fail(MAD_EINVAL, "seq_stride %lld overlaps heads", (long long)seq_stride);
+    for (int b = 0; b < B; ++b)
+        if (len[b] < T || len[b] > cap) return fail(MAD_EINVAL, "len[%d]=%d outside [T=%d, cap=%d]", b, len[b], T, cap);
+    const size_t need = mad::verify_ws_bytes(B, Hq, Hkv, d, T);
+    if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
+    if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
+    if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
+    mad::VerifyPlan p = mad::plan_verify(B, Hkv, len);
+    mad::VerifyArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.vt = vt;
+    a.out = out;
+    a.lse = lse;
+    a.seq = seq_stride;
+    a.head = head_stride;
+    size_t off_o, off_ml;
+    mad::verify_ws_layout(B, Hq, Hkv, d, T, &off_o, &off_ml);
+    a.part = (float *)((char *)ws + off_o);
+    a.part_ml = (float *)((char *)ws + off_ml);
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.cap = cap;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = G;
+    a.T = T;
+    a.d = d;
+    a.units = p.units;
+    a.n_splits = p.n_splits;
+    a.chunk = p.chunk;
+    a.part_rows = T * G;
+    for (int b = 0; b < B; ++b) a.len[b] = len[b];
+    return hip_status(mad::launch_verify(a, (hipStream_t)stream), "verify launch");
 }
 
 int mad_accept_greedy(const void *, int, const int32_t *, int, int, int, int32_t *, int32_t *, void *, size_t,

@@ -92,6 +92,34 @@ size_t update_part_stride(int R, int d, int KS);
 size_t update_ws_bytes(int R, int D, int Hkv, int d);
 hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st);
 
+// ---------------------------------------------------------------- verify ----
+#ifndef MAD_VERIFY_TARGET_WGS
+#define MAD_VERIFY_TARGET_WGS 512
+#endif
+constexpr int kVerifyTargetWGs = MAD_VERIFY_TARGET_WGS;
+constexpr int kVerifyMaxSplits = 128;
+
+struct VerifyArgs {
+    const void *q, *k, *vt;
+    void *out;
+    float *lse;
+    int64_t seq, head;    // element strides of sequences and KV heads (K and V^T alike)
+    float *part;          // [units][n_splits][part_rows][d] split partials (unnormalised o)
+    float *part_ml;       // [units][n_splits][part_rows][2] (max, sum)
+    float scale_log2;
+    int cap, Hq, Hkv, G, T, d, units, n_splits, chunk, part_rows;
+    int len[kMaxB];
+};
+
+struct VerifyPlan {
+    int units, n_splits, chunk;
+};
+
+VerifyPlan plan_verify(int B, int Hkv, const int *len);
+size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T);
+void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml);
+hipError_t launch_verify(const VerifyArgs &a, hipStream_t st);
+
 // ws layout helpers: counters first (256-byte aligned), then partials.
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 

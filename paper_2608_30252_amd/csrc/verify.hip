@@ -1,0 +1,303 @@
+// verify.hip -- the target's (gamma+1)-query verify attention over its full KV
+// cache (Sec. 2.1 draft-verify paradigm; Sec. 3.3: the verifier keeps the full
+// KV).  The T = gamma+1 new tokens' K/V sit at rows len-T .. len-1; query t
+// sees rows 0 .. len-T+t.
+//
+// Both products of attention run on the matrix cores
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation), fed straight from HBM:
+//   * the query tile of one (sequence, KV head) unit is the T*G rows
+//     (t, g) -> row t*G + g, padded to 16-row blocks;
+//   * S^T = K Q^T takes K rows as the A operand.  Key rows are assigned to the
+//     A rows with a fixed permutation so that the S^T accumulator already holds,
+//     in every lane, the 8 consecutive keys that the next product needs;
+//   * O^T = V^T P^T takes the values from the verifier's key-contiguous V cache
+//     (one run of cap keys per feature), 8 keys = 16 bytes a lane, and the
+//     probabilities from the lane's own scores (rounded to bf16);
+//   * online softmax per query row: the row's 8 scores sit in one lane, the
+//     row max needs two cross-lane exchanges.
+// Each wave of a workgroup streams its own 32-key slabs; the four waves' (max,
+// sum, o) are merged in LDS into one split partial.  A second small kernel
+// merges the splits of every query row with the log-sum-exp rule.
+#include "mad_device.h"
+#include "mad_internal.h"
+
+namespace mad {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
+typedef __attribute__((ext_vector_type(4))) float f32x4_v;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
+
+__device__ __forceinline__ float max_over_row_lanes(float v) {
+    // lanes l, l^16, l^32, l^48 hold the same query row
+    v = fmaxf(v, xor_lane<16>(v));
+    v = fmaxf(v, xor_lane<32>(v));
+    return v;
+}
+__device__ __forceinline__ float sum_over_row_lanes(float v) {
+    v += xor_lane<16>(v);
+    v += xor_lane<32>(v);
+    return v;
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
+    constexpr int KST = D / 32;   // 32-feature k steps of the QK product
+    constexpr int DB = D / 16;    // 16-feature output blocks of the PV product
+    constexpr int RP = NB * 16;   // padded query rows
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *sML = reinterpret_cast<float *>(smem);          // [4 waves][RP][2]
+    float *sO = sML + 4 * RP * 2;                          // [4 waves][RP][D]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int u = blockIdx.x % a.units, s = blockIdx.x / a.units;
+    const int b = u / a.Hkv, c = u - b * a.Hkv;
+    const int len = a.len[b], T = a.T, G = a.G, R = T * G;
+    const int k0 = s * a.chunk;
+    const int k1 = min(len, k0 + a.chunk);
+    const int cap = a.cap;
+    const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
+    const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
+    const int lr = lane & 15, lg = lane >> 4;   // row within a 16-block, lane group
+
+    // ---- query fragments (B operand of S^T = K Q^T) and causal limits ----
+    bf16x8_v qf[NB][KST];
+    int lim[NB];
+    #pragma unroll
+    for (int rb = 0; rb < NB; ++rb) {
+        const int row = rb * 16 + lr;
+        if (row < R) {
+            const int t = row / G, g = row - t * G;
+            const bf16_t *qrow = reinterpret_cast<const bf16_t *>(a.q) + (((size_t)b * T + t) * a.Hq + c * G + g) * D;
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) qf[rb][ks] = *reinterpret_cast<const bf16x8_v *>(qrow + ks * 32 + 8 * lg);
+            lim[rb] = len - T + t;
+        } else {
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) qf[rb][ks] = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
+            lim[rb] = 0x7fffffff;
+        }
+    }
+
+    f32x4_v o[DB][NB];
+    float m_run[NB], l_run[NB];
+    #pragma unroll
+    for (int rb = 0; rb < NB; ++rb) {
+        m_run[rb] = -INFINITY;
+        l_run[rb] = 0.f;
+        #pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][rb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+    }
+
+    for (int kb = k0 + wave * 32; kb < k1; kb += 128) {
+        // K rows for the two 16-key blocks: A row m of block blk holds key
+        // kb + 8*(m/4) + 4*blk + m%4, so accumulator element i of lane group lg
+        // is key kb + 8*lg + 4*blk + i.
+        bf16x8_v kf[2][KST];
+        #pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+            int key = kb + 8 * (lr >> 2) + 4 * blk + (lr & 3);
+            key = min(key, len - 1);
+            const bf16_t *krow = K + (size_t)key * D + 8 * lg;
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) kf[blk][ks] = *reinterpret_cast<const bf16x8_v *>(krow + ks * 32);
+        }
+        // V^T: feature db*16 + lr, keys kb + 8*lg .. +7 (cap is a multiple of 8)
+        const int kg = kb + 8 * lg;
+        bf16x8_v vf[DB];
+        #pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            if (kg < len) {
+                u32x4_v w = *reinterpret_cast<const u32x4_v *>(VT + (size_t)(db * 16 + lr) * cap + kg);
+                if (kg + 8 > len) {   // zero the values of keys past len (they may be stale)
+                    #pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kk = kg + 2 * e;
+                        if (kk >= len) w[e] = 0u;
+                        else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
+                    }
+                }
+                vf[db] = __builtin_bit_cast(bf16x8_v, w);
+            } else {
+                vf[db] = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
+            }
+        }
+        // S^T
+        f32x4_v sacc[2][NB];
+        #pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+            #pragma unroll
+            for (int rb = 0; rb < NB; ++rb) {
+                sacc[blk][rb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+                #pragma unroll
+                for (int ks = 0; ks < KST; ++ks)
+                    sacc[blk][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[blk][ks], qf[rb][ks], sacc[blk][rb], 0, 0, 0);
+            }
+        // online softmax and PV, per 16-row block
+        #pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            float sv[8];
+            float mt = -INFINITY;
+            #pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int key = kg + j;
+                const bool ok = key < k1 && key <= lim[rb];
+                sv[j] = ok ? sacc[j >> 2][rb][j & 3] * a.scale_log2 : -INFINITY;
+                mt = fmaxf(mt, sv[j]);
+            }
+            mt = max_over_row_lanes(mt);
+            const float mn = fmaxf(m_run[rb], mt);
+            const float ms = (mn == -INFINITY) ? 0.f : mn;
+            const float alpha = exp2f(m_run[rb] - ms);
+            m_run[rb] = mn;
+            float ps = 0.f;
+            uint32_t pk[4];
+            #pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float p0 = exp2f(sv[2 * e] - ms), p1 = exp2f(sv[2 * e + 1] - ms);
+                ps += p0 + p1;
+                pk[e] = pack_bf16x2(p0, p1);
+            }
+            l_run[rb] = fmaf(l_run[rb], alpha, ps);
+            const bf16x8_v pf = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                o[db][rb] *= alpha;
+                o[db][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pf, o[db][rb], 0, 0, 0);
+            }
+        }
+    }
+
+    // ---- merge the four waves in LDS ----
+    #pragma unroll
+    for (int rb = 0; rb < NB; ++rb) {
+        const float lt = sum_over_row_lanes(l_run[rb]);
+        if (lg == 0) {
+            sML[(wave * RP + rb * 16 + lr) * 2] = m_run[rb];
+            sML[(wave * RP + rb * 16 + lr) * 2 + 1] = lt;
+        }
+        #pragma unroll
+        for (int db = 0; db < DB; ++db)
+            #pragma unroll
+            for (int i = 0; i < 4; ++i) sO[((size_t)wave * RP + rb * 16 + lr) * D + db * 16 + 4 * lg + i] = o[db][rb][i];
+    }
+    __syncthreads();
+    float *po = a.part + ((size_t)u * a.n_splits + s) * a.part_rows * D;
+    float *pml = a.part_ml + ((size_t)u * a.n_splits + s) * a.part_rows * 2;
+    for (int idx = tid; idx < R * D; idx += 256) {
+        const int r = idx / D, col = idx - r * D;
+        float M = -INFINITY;
+        #pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, sML[(w * RP + r) * 2]);
+        const float Ms = (M == -INFINITY) ? 0.f : M;
+        float acc = 0.f, L = 0.f;
+        #pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float wt = exp2f(sML[(w * RP + r) * 2] - Ms);
+            acc = fmaf(wt, sO[((size_t)w * RP + r) * D + col], acc);
+            L = fmaf(wt, sML[(w * RP + r) * 2 + 1], L);
+        }
+        po[idx] = acc;
+        if (col == 0) {
+            pml[2 * r] = M;
+            pml[2 * r + 1] = L;
+        }
+    }
+}
+
+// One workgroup per (unit, query row): log-sum-exp merge of the splits.
+template <int D>
+__global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
+    const int R = a.T * a.G;
+    const int u = blockIdx.x / R, r = blockIdx.x - u * R;
+    const int b = u / a.Hkv, c = u - b * a.Hkv;
+    const int t = r / a.G, g = r - t * a.G;
+    const int col = threadIdx.x;
+    const float *po = a.part + (size_t)u * a.n_splits * a.part_rows * D + (size_t)r * D + col;
+    const float *pml = a.part_ml + (size_t)u * a.n_splits * a.part_rows * 2 + 2 * r;
+    const size_t sstride_o = (size_t)a.part_rows * D, sstride_ml = (size_t)a.part_rows * 2;
+    float M = -INFINITY;
+    for (int s = 0; s < a.n_splits; ++s) M = fmaxf(M, pml[s * sstride_ml]);
+    float acc = 0.f, L = 0.f;
+    if (M != -INFINITY) {
+        #pragma unroll 8
+        for (int s = 0; s < a.n_splits; ++s) {
+            const float wt = exp2f(pml[s * sstride_ml] - M);
+            L = fmaf(wt, pml[s * sstride_ml + 1], L);
+            acc = fmaf(wt, po[s * sstride_o], acc);
+        }
+    }
+    const size_t head = ((size_t)b * a.T + t) * a.Hq + (size_t)c * a.G + g;
+    reinterpret_cast<bf16_t *>(a.out)[head * D + col].bits = f32_to_bf16(L > 0.f ? acc / L : 0.f);
+    if (a.lse && col == 0) a.lse[head] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+}
+
+// ------------------------------------------------------------------ host ----
+
+VerifyPlan plan_verify(int B, int Hkv, const int *len) {
+    VerifyPlan p;
+    p.units = B * Hkv;
+    int n_max = 0;
+    for (int b = 0; b < B; ++b) n_max = len[b] > n_max ? len[b] : n_max;
+    int ns = (kVerifyTargetWGs + p.units - 1) / p.units;
+    if (ns > kVerifyMaxSplits) ns = kVerifyMaxSplits;
+    if (ns < 1) ns = 1;
+    int chunk = (n_max + ns - 1) / ns;
+    chunk = (chunk + 127) / 128 * 128;   // whole 32-key slabs for the four waves
+    if (chunk < 128) chunk = 128;
+    p.chunk = chunk;
+    p.n_splits = (n_max + chunk - 1) / chunk;
+    if (p.n_splits < 1) p.n_splits = 1;
+    return p;
+}
+
+static int verify_max_splits(int units) {
+    int ns = (kVerifyTargetWGs + units - 1) / units;
+    return ns > kVerifyMaxSplits ? kVerifyMaxSplits : (ns < 1 ? 1 : ns);
+}
+
+size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T) {
+    const size_t units = (size_t)B * Hkv;
+    const size_t rows = (size_t)T * (Hq / Hkv);
+    const size_t ns = (size_t)verify_max_splits((int)units);
+    return kCounterRegionBytes + align256(units * ns * rows * d * 4) + align256(units * ns * rows * 2 * 4);
+}
+
+void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml) {
+    const size_t units = (size_t)B * Hkv;
+    const size_t rows = (size_t)T * (Hq / Hkv);
+    const size_t ns = (size_t)verify_max_splits((int)units);
+    *off_o = kCounterRegionBytes;
+    *off_ml = kCounterRegionBytes + align256(units * ns * rows * d * 4);
+}
+
+template <int D, int NB>
+static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
+    constexpr int RP = NB * 16;
+    const size_t lds = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
+    hipLaunchKernelGGL((verify_split_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256), lds, st, a);
+    return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_d(const VerifyArgs &a, hipStream_t st) {
+    const int NB = (a.T * a.G + 15) / 16;
+    hipError_t e;
+    switch (NB) {
+        case 1: e = launch_split<D, 1>(a, st); break;
+        case 2: e = launch_split<D, 2>(a, st); break;
+        case 3: e = launch_split<D, 3>(a, st); break;
+        case 4: e = launch_split<D, 4>(a, st); break;
+        default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((verify_merge_kernel<D>), dim3((unsigned)(a.units * a.T * a.G)), dim3(D), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_verify(const VerifyArgs &a, hipStream_t st) {
+    if (a.d == 64) return launch_d<64>(a, st);
+    if (a.d == 128) return launch_d<128>(a, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace mad
