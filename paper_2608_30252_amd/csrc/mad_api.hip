@@ -93,6 +93,9 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
         case MAD_OP_VERIFY:
             if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128) || T < 1) return 0;
             return mad::verify_ws_bytes(B, Hq, Hkv, d, T);
+        case MAD_OP_ACCEPT:   // B, T, max_keys = V
+            if (B < 1 || T < 1 || max_keys < 1) return 0;
+            return mad::accept_ws_bytes(B, T, max_keys);
         default:
             return 0;
     }
@@ -270,9 +273,34 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
     return hip_status(mad::launch_verify(a, (hipStream_t)stream), "verify launch");
 }
 
-int mad_accept_greedy(const void *, int, const int32_t *, int, int, int, int32_t *, int32_t *, void *, size_t,
-                      void *) {
-    return fail(MAD_ENOTSUP, "mad_accept_greedy: not built yet");
+int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, int B, int T, int V,
+                      int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (T < 1 || (size_t)B * T + 1 > (size_t)mad::kCounterLines) return fail(MAD_EINVAL, "T=%d", T);
+    if (V < 1) return fail(MAD_EINVAL, "V=%d", V);
+    if (dtype != MAD_F32 && dtype != MAD_BF16) return fail(MAD_ENOTSUP, "dtype %d not supported", dtype);
+    if (!logits || !n_accept || !next_tok) return fail(MAD_EINVAL, "null logits, n_accept or next_tok");
+    if (T > 1 && !draft_tok) return fail(MAD_EINVAL, "draft_tok required when T > 1");
+    const size_t need = mad::accept_ws_bytes(B, T, V);
+    if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
+    if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
+    if (((uintptr_t)ws & 255u) != 0) return fail(MAD_EINVAL, "workspace not 256-byte aligned");
+    mad::AcceptArgs a;
+    memset(&a, 0, sizeof(a));
+    a.logits = logits;
+    a.draft = draft_tok;
+    a.n_accept = n_accept;
+    a.next_tok = next_tok;
+    size_t off_part, off_rows;
+    mad::accept_ws_layout(B, T, V, &off_part, &off_rows);
+    a.part = (uint64_t *)((char *)ws + off_part);
+    a.row_best = (uint64_t *)((char *)ws + off_rows);
+    a.counters = (unsigned *)ws;
+    a.B = B;
+    a.T = T;
+    a.V = V;
+    a.n_chunks = (V + mad::kAcceptChunk - 1) / mad::kAcceptChunk;
+    return hip_status(mad::launch_accept(a, dtype, (hipStream_t)stream), "accept launch");
 }
 
 }  // extern "C"

@@ -120,6 +120,23 @@ size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T);
 void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml);
 hipError_t launch_verify(const VerifyArgs &a, hipStream_t st);
 
+// ---------------------------------------------------------------- accept ----
+constexpr int kAcceptChunk = 8192;   // vocabulary entries per workgroup
+
+struct AcceptArgs {
+    const void *logits;
+    const int32_t *draft;      // [B][T-1] device
+    int32_t *n_accept, *next_tok;
+    uint64_t *part;            // [rows][n_chunks] chunk argmax keys
+    uint64_t *row_best;        // [rows] row argmax keys
+    unsigned *counters;        // lines 0..rows-1: per row; line rows: all rows
+    int B, T, V, n_chunks;
+};
+
+size_t accept_ws_bytes(int B, int T, int V);
+void accept_ws_layout(int B, int T, int V, size_t *off_part, size_t *off_rows);
+hipError_t launch_accept(const AcceptArgs &a, int dtype, hipStream_t st);
+
 // ws layout helpers: counters first (256-byte aligned), then partials.
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
