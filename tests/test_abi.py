@@ -1,0 +1,140 @@
+"""The C ABI on the CPU: the library loads, exports every function that
+include/mad.h declares, sizes workspaces, and rejects bad arguments with the
+documented status codes before anything is launched (no GPU is touched: all
+of these calls fail validation)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mad.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mad_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def mad():
+    import paper_2608_30252_amd as m
+    m._load_library()
+    return m
+
+
+def test_every_declared_symbol_is_exported(mad):
+    names = _declared_functions()
+    assert {"mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
+            "mad_workspace_bytes", "mad_last_error", "mad_version"} <= set(names)
+    lib = ctypes.CDLL(mad.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_empty_error(mad):
+    assert "gfx950" in mad.version()
+
+
+def test_workspace_sizes(mad):
+    ws = mad.workspace_bytes
+    assert ws(mad.MAD_OP_DECODE, 1, 32, 8, 64) > (1 << 20)          # counter region + partials
+    assert ws(mad.MAD_OP_DECODE, 16, 32, 8, 64) >= ws(mad.MAD_OP_DECODE, 1, 32, 8, 64)
+    assert ws(mad.MAD_OP_UPDATE, 4, 2048, 8, 64) > (1 << 20)
+    assert ws(mad.MAD_OP_VERIFY, 4, 32, 8, 128, 5) >= ws(mad.MAD_OP_VERIFY, 1, 32, 8, 128, 5) > (1 << 20)
+    assert ws(mad.MAD_OP_ACCEPT, 4, 1, 1, 64, 5, 128256) > (1 << 20)
+    # invalid sizes give 0
+    assert ws(mad.MAD_OP_DECODE, 0, 32, 8, 64) == 0
+    assert ws(mad.MAD_OP_DECODE, 1, 30, 8, 64) == 0
+    assert ws(mad.MAD_OP_UPDATE, 65, 2048, 8, 64) == 0
+    assert ws(99, 1, 1, 1, 64) == 0
+
+
+def _last_error(mad):
+    return mad._load_library().mad_last_error().decode()
+
+
+def _decode(mad, **kw):
+    args = dict(q=1 << 20, B=1, Hq=32, Hkv=8, d=64, dtype=mad.MAD_BF16, scale=0.125, mem=None, win=None,
+                kn=None, vn=None, out=1 << 21, lse=None, ws=None, ws_bytes=0)
+    args.update(kw)
+    lib = mad._load_library()
+    return lib.mad_draft_decode_attn(ctypes.c_void_p(args["q"]), args["B"], args["Hq"], args["Hkv"], args["d"],
+                                     args["dtype"], args["scale"], args["mem"], args["win"],
+                                     ctypes.c_void_p(args["kn"]) if args["kn"] else None,
+                                     ctypes.c_void_p(args["vn"]) if args["vn"] else None,
+                                     ctypes.c_void_p(args["out"]), None, None, 0, None)
+
+
+def test_decode_validation(mad):
+    assert _decode(mad, B=0) == mad.MAD_EINVAL
+    assert _decode(mad, B=65) == mad.MAD_EINVAL
+    assert _decode(mad, Hq=30) == mad.MAD_EINVAL
+    assert _decode(mad, d=96) == mad.MAD_ENOTSUP and "head_dim" in _last_error(mad)
+    assert _decode(mad, Hq=96, Hkv=3) == mad.MAD_ENOTSUP            # group 32
+    assert _decode(mad, dtype=7) == mad.MAD_ENOTSUP
+    assert _decode(mad, q=0) == mad.MAD_EINVAL
+    assert _decode(mad, q=(1 << 20) + 4) == mad.MAD_EINVAL            # unaligned
+    assert _decode(mad, kn=1 << 22) == mad.MAD_EINVAL                 # k_new without v_new
+    assert _decode(mad, kn=1 << 22, vn=1 << 23) == mad.MAD_EINVAL     # k_new without a window
+    assert _decode(mad, scale=-1.0) == mad.MAD_EINVAL
+    # a window whose len would overflow its capacity once the new token is appended
+    ln = (ctypes.c_int32 * 1)(16)
+    win = mad._KVView(1 << 24, 1 << 25, 0, 16 * 64, 16, None, ln)
+    assert _decode(mad, win=ctypes.byref(win), kn=1 << 22, vn=1 << 23) == mad.MAD_EINVAL
+    assert "exceeds cap" in _last_error(mad)
+    st = (ctypes.c_int32 * 1)(16)
+    ln2 = (ctypes.c_int32 * 1)(3)
+    win2 = mad._KVView(1 << 24, 1 << 25, 0, 16 * 64, 16, st, ln2)
+    assert _decode(mad, win=ctypes.byref(win2)) == mad.MAD_EINVAL        # start outside [0, cap)
+    win3 = mad._KVView(1 << 24, 1 << 25, 0, 8 * 64, 16, None, ln2)
+    assert _decode(mad, win=ctypes.byref(win3)) == mad.MAD_EINVAL        # head stride < cap*d
+    # missing workspace when the call needs split partials
+    ln4 = (ctypes.c_int32 * 1)(30000)
+    win4 = mad._KVView(1 << 24, 1 << 25, 0, 32768 * 64, 32768, None, ln4)
+    assert _decode(mad, win=ctypes.byref(win4)) == mad.MAD_EWS
+
+
+def test_update_validation(mad):
+    lib = mad._load_library()
+    pos = (ctypes.c_int32 * 4)(16, 32, 48, 64)
+    ln = (ctypes.c_int32 * 1)(10)
+    mem = mad._KVView(1 << 24, 1 << 25, 0, 16 * 64, 16, None, ln)
+    def call(B=1, n_new=4, D=2048, Hkv=8, d=64, dtype=mad.MAD_BF16, base=500000.0, x=1 << 20, memp=True):
+        return lib.mad_memory_update(ctypes.c_void_p(x), ctypes.c_void_p(1 << 21), pos, None, B, n_new, D, Hkv, d,
+                                     dtype, base, ctypes.byref(mem) if memp else None, None, 0, None)
+    assert call(n_new=8) == mad.MAD_EINVAL and "exceeds cap" in _last_error(mad)   # 10 + 8 > 16
+    assert call(n_new=4) == mad.MAD_EWS                                             # valid, but no workspace
+    assert call(n_new=0) == mad.MAD_EINVAL
+    assert call(B=65) == mad.MAD_EINVAL
+    assert call(D=100) == mad.MAD_EINVAL
+    assert call(d=32) == mad.MAD_ENOTSUP
+    assert call(base=1.0) == mad.MAD_EINVAL
+    assert call(x=0) == mad.MAD_EINVAL
+    assert call(memp=False) == mad.MAD_EINVAL
+
+
+def test_verify_and_accept_validation(mad):
+    lib = mad._load_library()
+    ln = (ctypes.c_int32 * 1)(100)
+    def ver(T=5, Hq=32, Hkv=8, d=128, dtype=mad.MAD_BF16, cap=128, head=128 * 128, ln_=ln):
+        return lib.mad_verify_attn(ctypes.c_void_p(1 << 20), 1, T, Hq, Hkv, d, dtype, 0.088, ctypes.c_void_p(1 << 21),
+                                   ctypes.c_void_p(1 << 22), 0, head, cap, ln_, ctypes.c_void_p(1 << 23), None,
+                                   None, 0, None)
+    assert ver(dtype=mad.MAD_F32) == mad.MAD_ENOTSUP
+    assert ver(T=0) == mad.MAD_EINVAL
+    assert ver(T=5, Hq=128, Hkv=8) == mad.MAD_EINVAL                 # T*G = 80 > 64
+    assert ver(cap=100) == mad.MAD_EINVAL                            # not a multiple of 8
+    assert ver(head=64) == mad.MAD_EINVAL
+    assert ver(ln_=(ctypes.c_int32 * 1)(3)) == mad.MAD_EINVAL        # len < T
+    assert ver(ln_=(ctypes.c_int32 * 1)(200)) == mad.MAD_EINVAL      # len > cap
+    assert ver() == mad.MAD_EWS                                      # workspace missing
+    acc = lambda B=1, T=5, V=128256, dtype=mad.MAD_F32, draft=1 << 21: lib.mad_accept_greedy(
+        ctypes.c_void_p(1 << 20), dtype, ctypes.c_void_p(draft) if draft else None, B, T, V,
+        ctypes.c_void_p(1 << 22), ctypes.c_void_p(1 << 23), None, 0, None)
+    assert acc(V=0) == mad.MAD_EINVAL
+    assert acc(T=0) == mad.MAD_EINVAL
+    assert acc(draft=0) == mad.MAD_EINVAL
+    assert acc(dtype=5) == mad.MAD_ENOTSUP
+    assert acc() == mad.MAD_EWS
