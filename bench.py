@@ -1,0 +1,444 @@
+#!/usr/bin/env python3
+"""Benchmark of the MASW hot path on one MI355X (gfx950).
+
+    python bench.py [--gpus 1] [--steps 64] [--warmup 8] [--no-cpu-baseline]
+
+Headline workload: draft decode at a 32K prefix -- batch 1, 16 layers, 32
+query / 8 KV heads, head_dim 64, bf16, a compact memory of 2048 slots (slot
+interval 16, no sinks) plus a 1024-token exact window.  One step is one draft
+token through all 16 layers:
+  * per layer, the fused draft decode attention over [memory | window ring]
+    with the current token's K/V appended to the ring in the same launch;
+  * when a sequence crosses a 64-token boundary, per layer the memory update
+    (mirrored projection of 4 slot rows + RoPE + append) and the four new
+    slots' write-scope attention (one launch, the four queries alias one
+    sequence's buffers).
+Six independent sequences are decoded round-robin so that each layer's data
+(6.3 MB, 100 MB per sequence) has left the 256 MB Infinity Cache before it is
+read again: the timed reads come from HBM.  The timed steps are captured in
+one HIP graph and replayed, so the clock measures GPU work, not Python.
+
+Reported in the same run (sub-objects of the JSON line):
+  full_kv        the same draft step over the uncompressed 32768-token KV
+  memory_update  the adaptor alone at 4 rows (32K) and 64 rows (16 sequences)
+  verify         the target's 5-query verify attention, 8B- and 70B-shaped
+                 layers at a 32768-token prefix
+  accept         greedy accept on [B, 5, 128256] fp32 logits
+  roofline       the dominant kernel (draft decode attention): algorithmic
+                 bytes per launch / mean launch duration from HIP events
+  cpu_baseline   the fp64 oracle on the host cores (a bounded sample)
+Inputs are synthetic N(0, 1) activations and N(0, 0.02^2) adaptor weights.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "draft-step attn latency (µs/layer) + achieved HBM TB/s at 32K prefix, 1 GPU"
+PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15         # dense MFMA bf16 FLOP/s
+GAMMA, ROLLBACK = 4, 16
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--sets", type=int, default=6, help="sequences decoded round-robin (cold HBM reads)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def kv_bytes(keys, hkv, d, esz=2):
+    return keys * hkv * d * 2 * esz
+
+
+class FullKVLayout:
+    """The uncompressed draft: raw position x at row x, all earlier tokens attended."""
+
+    def __init__(self, ring_cap):
+        self.ring_cap = ring_cap
+
+    def decode_view(self, p):
+        from paper_2608_30252_amd.state import DecodeView
+        if p + 1 > self.ring_cap:
+            raise ValueError("full-KV capacity exceeded")
+        return DecodeView(0, 0, p)
+
+
+class DraftModel:
+    """Buffers and host bookkeeping of the 16-layer compact draft memory for
+    `n_sets` independent batch-1 sequences at a 32K prefix."""
+
+    def __init__(self, torch, mad, n_sets, layers=16, Hq=32, Hkv=8, d=64, W=1024, r=16, u=4,
+                 prefix=32768, full_kv=False, dev="cuda"):
+        from paper_2608_30252_amd.state import MemoryLayout
+        self.torch, self.mad = torch, mad
+        self.layers, self.Hq, self.Hkv, self.d = layers, Hq, Hkv, d
+        self.D = Hq * d
+        self.full_kv = full_kv
+        self.n_sets = n_sets
+        self.prefix = prefix
+        ring_extra = r * u + GAMMA + ROLLBACK
+        if full_kv:
+            # the uncompressed draft: no memory, every earlier token in the window
+            self.lay = FullKVLayout(ring_cap=prefix + 256)
+        else:
+            ring_cap = (W + ring_extra + 7) // 8 * 8
+            n_mem = (prefix // (r * u)) * u
+            self.lay = MemoryLayout(0, W, r, ring_cap=ring_cap, mem_cap=n_mem + 64, slots_per_update=u)
+        bf = torch.bfloat16
+        L = layers
+        mk = lambda *s: torch.randn(*s, device=dev, dtype=torch.float32).to(bf)
+        if not full_kv:
+            self.mem_k = [[mk(1, Hkv, self.lay.mem_cap, d) for _ in range(L)] for _ in range(n_sets)]
+            self.mem_v = [[mk(1, Hkv, self.lay.mem_cap, d) for _ in range(L)] for _ in range(n_sets)]
+        self.ring_k = [[mk(1, Hkv, self.lay.ring_cap, d) for _ in range(L)] for _ in range(n_sets)]
+        self.ring_v = [[mk(1, Hkv, self.lay.ring_cap, d) for _ in range(L)] for _ in range(n_sets)]
+        self.q = [mk(1, Hq, d) for _ in range(L)]
+        self.kn = [mk(1, Hkv, d) for _ in range(L)]
+        self.vn = [mk(1, Hkv, d) for _ in range(L)]
+        self.out = [torch.empty(1, Hq, d, device=dev, dtype=bf) for _ in range(L)]
+        self.lse = [torch.empty(1, Hq, device=dev, dtype=torch.float32) for _ in range(L)]
+        if not full_kv:
+            self.u = u
+            self.x = [mk(1, u, self.D) for _ in range(L)]
+            self.w_g = [(torch.randn(2 * Hkv * d, self.D, device=dev) * 0.02).to(bf) for _ in range(L)]
+            self.qg = [mk(u, Hq, d) for _ in range(L)]
+            self.outg = [torch.empty(u, Hq, d, device=dev, dtype=bf) for _ in range(L)]
+        self.ws = torch.zeros(max(mad.workspace_bytes(mad.MAD_OP_DECODE, u if not full_kv else 1, Hq, Hkv, d),
+                                  mad.workspace_bytes(mad.MAD_OP_UPDATE, u if not full_kv else 1, self.D, Hkv, d)),
+                              dtype=torch.uint8, device=dev)
+        self.decode_calls = []   # (keys attended) per decode launch, for the roofline
+        self.n_updates = 0
+
+    def step(self, set_idx, p, decode_hook=None):
+        """One draft step of sequence `set_idx` at raw position p through all layers."""
+        mad, lay = self.mad, self.lay
+        view = lay.decode_view(p)
+        upd = None if self.full_kv else lay.update_in_pass_of(p)
+        for l in range(self.layers):
+            rk, rv = self.ring_k[set_idx][l], self.ring_v[set_idx][l]
+            mem = None if self.full_kv else mad.KV(self.mem_k[set_idx][l], self.mem_v[set_idx][l], [view.mem_len])
+            win = mad.KV(rk, rv, [view.win_len], [view.win_start])
+            if decode_hook:
+                decode_hook(True)
+            mad.draft_decode_attn(self.q[l], mem, win, self.kn[l], self.vn[l], self.out[l], self.lse[l], ws=self.ws)
+            if decode_hook:
+                decode_hook(False)
+            self.decode_calls.append(view.mem_len + view.win_len + 1)
+            if upd is not None:
+                mk, mv = self.mem_k[set_idx][l], self.mem_v[set_idx][l]
+                mad.memory_update(self.x[l], self.w_g[l], [upd.positions], mad.KV(mk, mv, [upd.mem_row]),
+                                  ws=self.ws)
+                # the new slots' write scopes: u queries over one sequence's buffers
+                views = [lay.slot_scope_view(upd.first_slot + i) for i in range(self.u)]
+                mad.draft_decode_attn(self.qg[l], mad.KV(mk, mv, [v.mem_len for v in views]),
+                                      mad.KV(rk, rv, [v.win_len for v in views], [v.win_start for v in views]),
+                                      out=self.outg[l], ws=self.ws)
+        if upd is not None:
+            self.n_updates += 1
+
+
+def graph_of(torch, fn):
+    """Capture fn() into a HIP graph on a side stream; return the graph."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph(torch, g, reps=1):
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / reps   # seconds per replay
+
+
+def mean_launch_seconds(torch, launches):
+    """Mean device duration of individual launches, each bracketed by HIP
+    events on the launching stream; a spin kernel keeps the stream busy while
+    the host enqueues the event/launch/event triple, so host latency stays out."""
+    evs = []
+    for fn in launches:
+        torch.cuda._sleep(200000)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in evs) * 1e-3 / len(evs)
+
+
+def source_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_30252_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_from_profile(kernel_file, bytes_default=None):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "decode_32k_compressed_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256") != source_digest(kernel_file):
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_30252_amd as mad
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(3)
+    torch.manual_seed(0)
+    K, Wm = max(args.steps, 1), max(args.warmup, 0)
+    n_sets = max(args.sets, 1)
+    log(f"device {torch.cuda.get_device_name(0)}; {mad.version()}")
+
+    # ------------------------------------------------------------ headline ----
+    model = DraftModel(torch, mad, n_sets)
+    # positions: every sequence starts at the 32K prefix; sequence 0 starts a few
+    # tokens before a 64-token boundary so that one memory update falls in the
+    # timed steps (one per 64 tokens of one sequence)
+    uses_before = -(-(Wm + 1) // n_sets)
+    pos = [model.prefix] * n_sets
+    pos[0] = model.prefix + 64 - 1 - uses_before
+    schedule = []
+    for s in range(Wm + K):
+        i = s % n_sets
+        schedule.append((i, pos[i]))
+        pos[i] += 1
+    warm, timed = schedule[:Wm], schedule[Wm:]
+    log(f"headline: {K} timed steps x {model.layers} layers, {n_sets} sequences round-robin")
+    g_warm = graph_of(torch, lambda: [model.step(i, p) for i, p in warm]) if warm else None
+    model.decode_calls.clear()
+    model.n_updates = 0
+    g_timed = graph_of(torch, lambda: [model.step(i, p) for i, p in timed])
+    keys_per_call = list(model.decode_calls)
+    n_updates = model.n_updates
+    if g_warm is not None:
+        g_warm.replay()
+    torch.cuda.synchronize()
+    t_step_total = time_graph(torch, g_timed)
+    ms_per_step = t_step_total * 1e3 / K
+    us_per_layer = ms_per_step * 1e3 / model.layers
+    decode_bytes = [kv_bytes(k, model.Hkv, model.d) for k in keys_per_call]
+    step_tbps = sum(decode_bytes) / t_step_total / 1e12
+    log(f"headline: {ms_per_step:.4f} ms/step, {us_per_layer:.2f} us/layer, {n_updates} boundary step(s)")
+
+    # dominant kernel: mean duration of the draft decode launches of the timed steps
+    launches = []
+    for i, p in timed[: min(len(timed), 8)]:
+        view = model.lay.decode_view(p)
+        for l in range(model.layers):
+            def fn(i=i, l=l, view=view):
+                mad.draft_decode_attn(model.q[l], mad.KV(model.mem_k[i][l], model.mem_v[i][l], [view.mem_len]),
+                                      mad.KV(model.ring_k[i][l], model.ring_v[i][l], [view.win_len],
+                                             [view.win_start]),
+                                      model.kn[l], model.vn[l], model.out[l], model.lse[l], ws=model.ws)
+            launches.append((fn, view.mem_len + view.win_len + 1))
+    t_launch = mean_launch_seconds(torch, [f for f, _ in launches])
+    bytes_launch = sum(kv_bytes(k, model.Hkv, model.d) for _, k in launches) / len(launches)
+    achieved = bytes_launch / t_launch
+    log(f"decode launch: {t_launch * 1e6:.2f} us mean over {len(launches)}, {bytes_launch:,.0f} B -> "
+        f"{achieved / 1e12:.2f} TB/s")
+    roofline = {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM, 4), "traffic": traffic_from_profile("decode.hip"),
+                "kernel": "mad::decode_kernel<bf16_t, 64, 4>", "bytes_per_launch": int(bytes_launch),
+                "mean_launch_us": round(t_launch * 1e6, 3)}
+    del model
+    torch.cuda.empty_cache()
+
+    # ------------------------------------------------------- full-KV draft ----
+    K2 = min(K, 16)
+    full = DraftModel(torch, mad, 1, full_kv=True)
+    sched = [(0, full.prefix + s) for s in range(K2 + 2)]
+    g_full_w = graph_of(torch, lambda: [full.step(i, p) for i, p in sched[:2]])
+    full.decode_calls.clear()
+    g_full = graph_of(torch, lambda: [full.step(i, p) for i, p in sched[2:]])
+    g_full_w.replay()
+    t_full = time_graph(torch, g_full)
+    full_bytes = sum(kv_bytes(k, full.Hkv, full.d) for k in full.decode_calls)
+    full_us_layer = t_full * 1e6 / (K2 * full.layers)
+    f_launch = []
+    for i, p in sched[2:4]:
+        view = full.lay.decode_view(p)
+        for l in range(full.layers):
+            f_launch.append(lambda l=l, view=view: mad.draft_decode_attn(
+                full.q[l], None, mad.KV(full.ring_k[0][l], full.ring_v[0][l], [view.win_len], [view.win_start]),
+                full.kn[l], full.vn[l], full.out[l], full.lse[l], ws=full.ws))
+    t_full_launch = mean_launch_seconds(torch, f_launch)
+    full_launch_bytes = kv_bytes(full.prefix + 1, full.Hkv, full.d)
+    full_kv = {"workload": "draft decode over the full 32768-token KV: B1, 16 layers, 32/8 heads, d64, bf16",
+               "us_per_layer": round(full_us_layer, 3), "ms_per_step": round(t_full * 1e3 / K2, 4),
+               "tbps": round(full_bytes / t_full / 1e12, 3),
+               "mean_launch_us": round(t_full_launch * 1e6, 3),
+               "launch_frac_of_hbm_peak": round(full_launch_bytes / t_full_launch / PEAK_HBM, 4),
+               "bytes_per_launch": full_launch_bytes, "steps": K2}
+    log(f"full KV: {full_us_layer:.2f} us/layer, launch {t_full_launch * 1e6:.2f} us "
+        f"({full_launch_bytes / t_full_launch / 1e12:.2f} TB/s)")
+    del full
+    torch.cuda.empty_cache()
+
+    # ------------------------------------------------------- memory update ----
+    upd_res = {}
+    for name, B, n_new, sets in (("32k_4_rows", 1, 4, 8), ("batched_64_rows", 16, 4, 8)):
+        Hkv, d, D = 8, 64, 2048
+        xs = [torch.randn(B, n_new, D, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        ws_ = [(torch.randn(2 * Hkv * d, D, device="cuda") * 0.02).to(torch.bfloat16) for _ in range(sets)]
+        mks = [torch.randn(B, Hkv, 1088, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        mvs = [torch.randn(B, Hkv, 1088, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        wsb = torch.zeros(mad.workspace_bytes(mad.MAD_OP_UPDATE, B * n_new, D, Hkv, d), dtype=torch.uint8,
+                          device="cuda")
+        posl = [[16 * (2048 + 4 * b + i) for i in range(n_new)] for b in range(B)]
+        fns = [lambda j=j: mad.memory_update(xs[j], ws_[j], posl, mad.KV(mks[j], mvs[j], [1024] * B), ws=wsb)
+               for j in range(sets)]
+        g = graph_of(torch, lambda: [f() for f in fns])
+        g.replay()
+        t = time_graph(torch, g, reps=4) / sets
+        nbytes = 2 * Hkv * d * D * 2 + B * n_new * D * 2 + B * n_new * 2 * Hkv * d * 2
+        flops = 2.0 * B * n_new * D * 2 * Hkv * d
+        upd_res[name] = {"rows": B * n_new, "us": round(t * 1e6, 3), "tbps": round(nbytes / t / 1e12, 3),
+                         "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "tflops": round(flops / t / 1e12, 3),
+                         "mfma_frac_of_bf16_peak": round(flops / t / PEAK_BF16, 6), "bytes": nbytes}
+        log(f"memory update {name}: {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
+        del xs, ws_, mks, mvs, wsb, fns, g
+    torch.cuda.empty_cache()
+
+    # -------------------------------------------------------------- verify ----
+    ver_res = {}
+    for name, B, Hq, sets in (("8b_layer_b4", 4, 32, 1), ("70b_layer_b1", 1, 64, 3)):
+        Hkv, d, T, cap = 8, 128, 5, 32776
+        L = 32768 + T
+        ks = [torch.randn(B, Hkv, cap, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        vts = [torch.randn(B, Hkv, d, cap, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        qv = torch.randn(B, T, Hq, d, device="cuda").to(torch.bfloat16)
+        ov = torch.empty_like(qv)
+        lv = torch.empty(B, T, Hq, device="cuda")
+        wsv = torch.zeros(mad.workspace_bytes(mad.MAD_OP_VERIFY, B, Hq, Hkv, d, T), dtype=torch.uint8,
+                          device="cuda")
+        reps = max(3, 6 // sets) * sets
+        fns = [lambda j=j: mad.verify_attn(qv, ks[j % sets], vts[j % sets], [L] * B, ov, lv, ws=wsv)
+               for j in range(reps)]
+        g = graph_of(torch, lambda: [f() for f in fns])
+        g.replay()
+        t = time_graph(torch, g, reps=2) / reps
+        nbytes = kv_bytes(L, Hkv, d) * B
+        flops = 4.0 * B * Hq * T * L * d
+        ver_res[name] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3),
+                         "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "bytes": nbytes,
+                         "mfma_tflops": round(flops / t / 1e12, 2)}
+        log(f"verify {name}: {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
+        del ks, vts, fns, g
+    torch.cuda.empty_cache()
+
+    # -------------------------------------------------------------- accept ----
+    acc_res = {}
+    for name, B in (("8b_b4", 4), ("70b_b1", 1)):
+        T, V = 5, 128256
+        lg = [torch.randn(B, T, V, device="cuda") for _ in range(4)]
+        dr = torch.randint(0, V, (B, T - 1), device="cuda", dtype=torch.int32)
+        na = torch.empty(B, dtype=torch.int32, device="cuda")
+        nx = torch.empty(B, dtype=torch.int32, device="cuda")
+        wsa = torch.zeros(mad.workspace_bytes(mad.MAD_OP_ACCEPT, B, 1, 1, 64, T, V), dtype=torch.uint8,
+                          device="cuda")
+        fns = [lambda j=j: mad.accept_greedy(lg[j], dr, na, nx, ws=wsa) for j in range(4)]
+        g = graph_of(torch, lambda: [f() for f in fns])
+        g.replay()
+        t = time_graph(torch, g, reps=4) / 4
+        nbytes = B * T * V * 4
+        acc_res[name] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3), "bytes": nbytes}
+        log(f"accept {name}: {t * 1e6:.2f} us")
+        del lg, fns, g
+
+    # --------------------------------------------------------- CPU baseline ----
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(args.cpu_seconds)
+        log(f"cpu baseline: {cpu['value']:.1f} us/layer on {cpu['cores']} threads")
+
+    result = {
+        "metric": METRIC, "value": round(us_per_layer, 3), "unit": "us/layer", "n_gpus": 1, "steps": K,
+        "warmup": Wm, "ms_per_step": round(ms_per_step, 5), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "draft decode at a 32K prefix: batch 1, 16 layers, 32 query / 8 KV heads, "
+                               "head_dim 64, 2048 memory slots + 1024-token window, bf16",
+                   "batch": 1, "prefix": 32768, "layers": 16, "memory_slots": 2048, "window": 1024,
+                   "slot_interval": 16, "slots_per_update": 4, "sequences_round_robin": n_sets,
+                   "parallelism": "none"},
+        "step_tbps": round(step_tbps, 3),
+        "tokens_per_s": round(1.0 / (ms_per_step * 1e-3), 1),
+        "boundary_steps_timed": n_updates,
+        "roofline": roofline,
+        "full_kv": full_kv,
+        "speedup_vs_full_kv": round(full_us_layer / us_per_layer, 3),
+        "memory_update": upd_res,
+        "verify": ver_res,
+        "accept": acc_res,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(seconds):
+    """The fp64 oracle on the host: the 32K compact-memory layer attention
+    (8 KV heads x 3072 keys x 4 query heads, head_dim 64), repeated for about
+    `seconds` of wall time."""
+    import numpy as np
+    import oracle
+    from paper_2608_30252_amd import synth
+    Hq, Hkv, d, n = 32, 8, 64, 3072
+    q = synth.normal((1, Hq, d), 1).double().numpy()
+    k = synth.normal((1, Hkv, n, d), 2).double().numpy()
+    v = synth.normal((1, Hkv, n, d), 3).double().numpy()
+    nn = np.array([n])
+    oracle.attend_batched(q, k, v, nn, d ** -0.5)
+    t0 = time.perf_counter()
+    calls = 0
+    while True:
+        oracle.attend_batched(q, k, v, nn, d ** -0.5)
+        calls += 1
+        if time.perf_counter() - t0 > seconds:
+            break
+    t = (time.perf_counter() - t0) / calls
+    return {"value": round(t * 1e6, 1), "unit": "us/layer", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{calls} calls of one 32K compact-memory layer attention (8 KV heads x 3072 keys x 4 "
+                      f"query heads, d 64, fp64)"}
+
+
+if __name__ == "__main__":
+    main()

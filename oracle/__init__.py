@@ -49,6 +49,8 @@ def _load():
     lib.oracle_rope.argtypes = [i, i, i, _dp, _ip, d]
     lib.oracle_argmax.argtypes = [i, i, _fp, _ip]
     lib.oracle_accept_greedy.argtypes = [i, i, i, _fp, _ip, _ip, _ip]
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     for f in ("oracle_attend", "oracle_attend_batched", "oracle_verify", "oracle_project",
               "oracle_rope", "oracle_argmax", "oracle_accept_greedy"):
         getattr(lib, f).restype = None
@@ -66,6 +68,11 @@ def _i32(a):
 
 def _ptr(a, t):
     return a.ctypes.data_as(t)
+
+
+def num_threads():
+    """OpenMP threads the batched oracle routines run on."""
+    return int(_load().oracle_num_threads())
 
 
 def attend(q, k, v, scale, with_wsum=False):

@@ -219,3 +219,11 @@ void oracle_accept_greedy(int B, int T, int V, const float *logits, const int *d
     }
     free(am);
 }
+
+/* Number of OpenMP threads the batched routines use (1 without OpenMP). */
+#ifdef _OPENMP
+#include <omp.h>
+int oracle_num_threads(void) { return omp_get_max_threads(); }
+#else
+int oracle_num_threads(void) { return 1; }
+#endif
