@@ -278,7 +278,7 @@ def main():
         f"{achieved / 1e12:.2f} TB/s")
     roofline = {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM, 4), "traffic": traffic_from_profile("decode.hip"),
-                "kernel": "mad::decode_kernel<bf16_t, 64, 4>", "bytes_per_launch": int(bytes_launch),
+                "kernel": "mad::decode_kernel<bf16_t, 64, 4, 1>", "bytes_per_launch": int(bytes_launch),
                 "mean_launch_us": round(t_launch * 1e6, 3)}
     del model
     torch.cuda.empty_cache()

@@ -7,28 +7,33 @@
 // window ring in the same pass (Sec. 3.2).
 //
 // Work decomposition (split-K / flash-decoding), grid = n_splits * units
-// workgroups of 256 threads, units = B * Hkv; workgroup w handles unit
-// u = w % units and the s = w / units-th range of `chunk` keys.
+// workgroups, units = B * Hkv; workgroup w handles unit u = w % units and key
+// range s = n_splits - 1 - w / units (the short last range, which holds the
+// new token, is dispatched first).  With units a multiple of 8 every split of
+// a unit runs on one XCD (workgroups are dealt to the 8 XCDs round-robin).
 //
-// Inside a workgroup keys stream through LDS in tiles of 8 KB of K + 8 KB of V
-// (64 keys for bf16, head_dim 64):
-//   * loads go straight from HBM into LDS (global_load_lds_dwordx4, 16 bytes a
-//     lane, no VGPR round trip) through a 4-stage ring, so up to three tiles
-//     are in flight while one is consumed; K rows are XOR-swizzled by 16-byte
-//     chunk on the way in so the QK reads are bank-conflict free;
-//   * QK: one wave per query head of the GQA group, one lane per key; the
-//     full head_dim dot product comes from LDS (K is read once from HBM and
-//     shared by the G heads);
-//   * online softmax on exp2 of pre-scaled scores; the per-head tile max is a
-//     single in-wave DPP/swizzle reduction; for the PV product the
-//     probabilities are rounded to bf16 and packed in key pairs (the softmax
-//     normaliser keeps the fp32 values);
-//   * PV: thread <-> (feature pair, key subset) for all G heads at once, two
-//     keys per v_dot2_f32_bf16 (fp32 accumulation);
+// A workgroup is NSUB groups of four waves.  Keys stream through LDS in
+// super-tiles of NSUB tiles, a tile being 8 KB of K + 8 KB of V (64 keys for
+// bf16 with head_dim 64); group j owns tile j of every super-tile:
+//   * all waves load each super-tile together straight from HBM into LDS
+//     (global_load_lds_dwordx4, 16 bytes a lane, no VGPR round trip) through a
+//     ring of stages; K rows are XOR-swizzled by 16-byte chunk on the way in so
+//     the QK reads are bank-conflict free; a super-tile inside one segment
+//     (memory, or the ring without a wrap) takes a uniform address path;
+//   * everything after the load is wave-local: wave w of a group owns query
+//     heads w, w+4, ... of the GQA group.  QK puts one key on each lane (query
+//     rows in SGPRs or VGPRs, K chunks read from LDS in one burst), the tile
+//     maximum of a head is a DPP row reduction plus row broadcasts and a
+//     readlane, and PV runs over (feature pair, key subset) lanes, two keys per
+//     v_dot2_f32_bf16 on bf16-rounded probabilities that the wave passes to
+//     itself through a private LDS slice (the softmax normaliser keeps the
+//     fp32 values).  One barrier per super-tile: the one that says it landed;
+//   * the groups' running (max, sum, o) are merged in LDS into one partial per
+//     workgroup;
 //   * the last workgroup of a unit (one arrival counter per unit, on its own
-//     256-byte line) pulls every split's partial (o, max, sum) into LDS with
-//     device-coherent direct loads in a single round trip and merges them with
-//     the log-sum-exp rule.
+//     256-byte line) pulls every split's partial into LDS with device-coherent
+//     direct loads in a single round trip and merges them with the
+//     log-sum-exp rule, all splits of a head in parallel lanes.
 #include <type_traits>
 
 #include "mad_device.h"
@@ -36,40 +41,51 @@
 
 namespace mad {
 
-constexpr int kNT = 256;
-constexpr int kStages = 4;
-constexpr int kStageBytes = 16384;   // 8 KB of K + 8 KB of V
+constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
+constexpr int kMergeLds = 65536;    // LDS that holds a unit's split partials in the merge
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, int NSUB>
 struct DecodeCfg {
+    static constexpr bool BF = std::is_same<T, bf16_t>::value;
+    static constexpr int NT = 256 * NSUB;              // threads per workgroup
+    static constexpr int NW = 4 * NSUB;                // waves
     static constexpr int ESZ = (int)sizeof(T);
     static constexpr int RB = D * ESZ;                 // bytes per K/V row
-    static constexpr int TILE = 8192 / RB;             // keys per tile
-    static constexpr int CPR = RB / 16;                // 16-byte chunks per row
-    static constexpr int SW = (CPR < 8 ? CPR : 8) - 1; // K swizzle mask
+    static constexpr int TILE = 8192 / RB;             // keys per tile: 64, 32 or 16
+    static constexpr int SUPER = NSUB * TILE;          // keys per super-tile
+    static constexpr int STAGES = NSUB == 1 ? 4 : 2;   // super-tiles in the LDS ring
+    static constexpr int SB = NSUB * kTileBytes;       // bytes per stage: [K: NSUB x 8 KB][V: NSUB x 8 KB]
+    static constexpr int CPR = RB / 16;                // 16-byte chunks per row (>= 8)
+    static constexpr int SW = 7;                       // K swizzle: chunk ^ (row & 7)
     static constexpr int RPI = 1024 / RB;              // rows per wave load (64 lanes x 16 B)
-    static constexpr int LPT = 2;                      // K (and V) loads per thread per tile
-    static constexpr int PAIRS = TILE * G;             // (head, key) score pairs per tile
-    static constexpr int PPT = (PAIRS + kNT - 1) / kNT;
-    static constexpr int DP = D / 2;                   // feature pairs
-    static constexpr int KS = kNT / DP;                // key subsets in PV
-    static constexpr int KPS = TILE / KS;              // keys per subset per tile
-    static constexpr bool BF = std::is_same<T, bf16_t>::value;
-    // LDS layout: [stages | P | alpha | fin | O]; the merge reuses [stages]
-    static constexpr int OFF_P = kStages * kStageBytes;
-    static constexpr int SZ_P = TILE * G * 4;
-    static constexpr int OFF_ALPHA = OFF_P + SZ_P;
-    static constexpr int OFF_FIN = OFF_ALPHA + G * 4;
-    static constexpr int OFF_O = OFF_FIN + G * 8;
-    static constexpr int SZ_O = KS * G * D * 4;
-    static constexpr int SMEM = OFF_O + SZ_O;
-    static_assert(TILE * RB == 8192 && kNT / 64 * LPT * 1024 == 8192, "tile = 8 KB per tensor");
-    static_assert(KPS % 2 == 0 && kNT % DP == 0 && TILE % KS == 0, "pv shape");
-    static_assert(PAIRS % TILE == 0 && (kNT % TILE == 0), "score pair groups");
+    static constexpr int LPT = 2;                      // K (and V) loads per thread per super-tile
+    static constexpr int HPP = 64 / TILE;              // heads per QK pass of a wave
+    static constexpr int HW = (G + 3) / 4;             // heads per wave
+    static constexpr int NPASS = (HW + HPP - 1) / HPP; // QK passes per tile
+    static constexpr int QW = RB / 4;                  // 32-bit words of one query row
+    static constexpr int KB = 8;                       // K chunks read per batch
+    static constexpr int DW = D / 2;                   // PV: each lane owns two features
+    static constexpr int KSW = 64 / DW;                // PV key subsets per wave
+    static constexpr int KPL = TILE / KSW;             // PV keys per lane per tile
+    // a 64-key tile gives every wave one head per pass: its query rows (at most
+    // two) come through the scalar cache, loaded at kernel start
+    static constexpr bool QS = TILE == 64 && HW <= 2;
+    // LDS: [stages | Q: the unit's query rows | P: per-wave probabilities | WN: merge weights]
+    static constexpr int SZ_ST = STAGES * SB;
+    static constexpr int OFF_Q = SZ_ST > kMergeLds ? SZ_ST : kMergeLds;
+    static constexpr int SZ_Q = (G * RB + 1023) / 1024 * 1024;
+    static constexpr int OFF_P = OFF_Q + SZ_Q;
+    static constexpr int SZ_P = NW * TILE * HW * 4;
+    static constexpr int OFF_WN = OFF_P + SZ_P;
+    static constexpr int SZ_WN = 1024;
+    static constexpr int SMEM = OFF_WN + SZ_WN;
+    static_assert(TILE * RB == 8192 && 4 * LPT * 1024 == 8192, "tile = 8 KB per tensor");
+    static_assert(CPR % KB == 0 && KPL % 2 == 0 && 64 % DW == 0, "shape");
+    static_assert(NSUB * G * (D + 2) * 4 <= SZ_ST, "group merge buffer fits the stages");
 };
 
 // vmcnt(n) for n in {0, 4, 8, 12} (the tile loads are the only vector memory
-// operations in flight inside the pipeline; 4 per tile and thread).
+// operations in flight inside the pipeline; 4 per super-tile and thread).
 __device__ __forceinline__ void wait_vmcnt(int n) {
     switch (n) {
         case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
@@ -85,30 +101,152 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
                                            false);
 }
 
-// Max over aligned groups of N consecutive lanes (all lanes must be active).
-template <int N> __device__ __forceinline__ float group_max(float v) {
-    if constexpr (N >= 2) v = fmaxf(v, xor_lane<1>(v));
-    if constexpr (N >= 4) v = fmaxf(v, xor_lane<2>(v));
-    if constexpr (N >= 8) v = fmaxf(v, xor_lane<4>(v));
-    if constexpr (N >= 16) v = fmaxf(v, xor_lane<8>(v));
-    if constexpr (N >= 32) v = fmaxf(v, xor_lane<16>(v));
-    if constexpr (N >= 64) v = fmaxf(v, xor_lane<32>(v));
-    return v;
+// Max over aligned groups of N in {16, 32, 64} lanes, returned to every lane
+// of the group.  A 16-lane row is reduced with DPP; rows are then folded with
+// the row broadcasts (row 1 <- lane 15, row 3 <- lane 47 under row mask 0xa;
+// rows 2 and 3 <- lane 31 under mask 0xc) and the group's last lane is read
+// back as a wave-uniform value.
+__device__ __forceinline__ float row_bcast15(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x142, 0xA, 0xF, false));
+}
+__device__ __forceinline__ float row_bcast31(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x143, 0xC, 0xF, false));
+}
+__device__ __forceinline__ float read_lane(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+template <int N> __device__ __forceinline__ float group_max_b(float v, int lane) {
+    v = fmaxf(v, xor_lane<1>(v));
+    v = fmaxf(v, xor_lane<2>(v));
+    v = fmaxf(v, xor_lane<4>(v));
+    v = fmaxf(v, xor_lane<8>(v));
+    if constexpr (N == 16) {
+        return v;
+    } else if constexpr (N == 32) {
+        v = fmaxf(v, row_bcast15(v));
+        const float a = read_lane(v, 31), b = read_lane(v, 63);
+        return lane < 32 ? a : b;
+    } else {
+        v = fmaxf(v, row_bcast15(v));
+        v = fmaxf(v, row_bcast31(v));
+        return read_lane(v, 63);
+    }
+}
+// Sum over all 64 lanes, returned as a wave-uniform value (same scheme as
+// group_max_b; rows outside a broadcast's mask add zero).
+__device__ __forceinline__ float wave_sum_b(float v) {
+    v += xor_lane<1>(v);
+    v += xor_lane<2>(v);
+    v += xor_lane<4>(v);
+    v += xor_lane<8>(v);
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+    return read_lane(v, 63);
 }
 
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kNT, 2) void decode_kernel(const DecodeArgs a) {
-    using C = DecodeCfg<T, D, G>;
+// Merge of a unit's split partials by its last-arriving workgroup (NT threads).
+//   blk   unit block in the workspace: [o: n_splits][G][D] [ml: n_splits][G][2]
+//   lds   >= n_splits * G * (D + 2) * 4 bytes of LDS (16-byte aligned); wn: n_splits * G floats
+template <typename T, int D, int G, int NT>
+__device__ __forceinline__ void merge_splits(const float *blk, int n_splits, unsigned char *lds, float *wn, T *out,
+                                             float *lse) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // ---- pull all partials into LDS in one round trip (1 KB per wave instruction) ----
+    const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
+    for (int off = wave * 1024; off < nbytes; off += NT * 16) {
+        if (off + lane * 16 < nbytes)
+            lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, lds + off);
+    }
+    wait_vmcnt(0);
+    __syncthreads();
+    const float *lo = reinterpret_cast<const float *>(lds);   // [n_splits][G][D]
+    const float *lml = lo + (size_t)n_splits * G * D;          // [n_splits][G][2]: max, sum
+
+    // phase 1, one wave per head: M = max_s m_s, L = sum_s 2^(m_s - M) l_s and the
+    // split weights 2^(m_s - M) / L (all splits of a head in parallel lanes, at
+    // most kDecodeMaxSplits / 64 per lane)
+    constexpr int SPL = kDecodeMaxSplits / 64;
+    for (int g = wave; g < G; g += NT / 64) {
+        float2 ml[SPL];
+        float mloc = -INFINITY;
+        #pragma unroll
+        for (int i = 0; i < SPL; ++i) {
+            const int sp = lane + 64 * i;
+            ml[i] = sp < n_splits ? reinterpret_cast<const float2 *>(lml)[sp * G + g] : make_float2(-INFINITY, 0.f);
+            mloc = fmaxf(mloc, ml[i].x);
+        }
+        const float M = group_max_b<64>(mloc, lane);
+        float w[SPL], lsum = 0.f;
+        #pragma unroll
+        for (int i = 0; i < SPL; ++i) {
+            w[i] = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml[i].x - M);
+            lsum = fmaf(w[i], ml[i].y, lsum);
+        }
+        const float L = wave_sum_b(lsum);
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        #pragma unroll
+        for (int i = 0; i < SPL; ++i)
+            if (lane + 64 * i < n_splits) wn[g * n_splits + lane + 64 * i] = w[i] * inv;
+        if (lse && lane == 0) lse[g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+    }
+    __syncthreads();
+
+    // phase 2: o = sum_s weight_s o_s, one 16-byte group of outputs per NQ
+    // neighbouring lanes, each lane summing every NQ-th split; the reads of a
+    // batch of MB splits are issued together (indices past the last split read
+    // the last one with weight 0)
+    constexpr int NG4 = G * D / 4;
+    constexpr int NQ = NG4 >= NT ? 1 : (NT / NG4 > 64 ? 64 : NT / NG4);
+    constexpr int MB = 16;
+    for (int grp = tid / NQ; grp < NG4; grp += NT / NQ) {
+        const int qq = tid % NQ;
+        const float *wg = wn + (grp * 4 / D) * n_splits;
+        const float4 *lo4 = reinterpret_cast<const float4 *>(lo) + grp;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int sb = qq; sb < n_splits; sb += MB * NQ) {
+            float4 o4[MB];
+            float wt[MB];
+            #pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                const int sp = sb + i * NQ;
+                const int spc = sp < n_splits ? sp : n_splits - 1;
+                o4[i] = lo4[(size_t)spc * NG4];
+                wt[i] = wg[spc];
+                if (sp >= n_splits) wt[i] = 0.f;
+            }
+            #pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                acc.x = fmaf(wt[i], o4[i].x, acc.x);
+                acc.y = fmaf(wt[i], o4[i].y, acc.y);
+                acc.z = fmaf(wt[i], o4[i].z, acc.z);
+                acc.w = fmaf(wt[i], o4[i].w, acc.w);
+            }
+        }
+        acc.x = group_sum<NQ>(acc.x);
+        acc.y = group_sum<NQ>(acc.y);
+        acc.z = group_sum<NQ>(acc.z);
+        acc.w = group_sum<NQ>(acc.w);
+        if (qq == 0) {
+            if constexpr (std::is_same<T, bf16_t>::value) {
+                reinterpret_cast<uint2 *>(out)[grp] = make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
+            } else {
+                reinterpret_cast<float4 *>(out)[grp] = acc;
+            }
+        }
+    }
+}
+
+template <typename T, int D, int G, int NSUB>
+__global__ __launch_bounds__(256 * NSUB, NSUB == 1 ? 2 : 1) void decode_kernel(const DecodeArgs a) {
+    using C = DecodeCfg<T, D, G, NSUB>;
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *sStage = smem;
-    float *sAlpha = reinterpret_cast<float *>(smem + C::OFF_ALPHA);   // [G]
-    float *sFin = reinterpret_cast<float *>(smem + C::OFF_FIN);       // [G][2]: max, sum
-    float *sO = reinterpret_cast<float *>(smem + C::OFF_O);           // [KS][G][D]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
+    const int grp = wave >> 2, wq = wave & 3;   // wave group (tile of the super-tile), wave in group
     const int units = a.units;
-    const int u = blockIdx.x % units, s = blockIdx.x / units;
+    const int u = blockIdx.x % units, s = a.n_splits - 1 - (int)(blockIdx.x / units);
     const int b = u / a.Hkv, c = u - b * a.Hkv;
     const int mlen = a.mlen[b], wlen = a.wlen[b], wst = a.wstart[b];
     const bool has_new = a.kn != nullptr;
@@ -124,47 +262,31 @@ __global__ __launch_bounds__(kNT, 2) void decode_kernel(const DecodeArgs a) {
     const size_t nrow = ((size_t)b * a.Hkv + c) * D;
     const T *nk = has_new ? reinterpret_cast<const T *>(a.kn) + nrow : nullptr;
     const T *nv = has_new ? reinterpret_cast<const T *>(a.vn) + nrow : nullptr;
+    const size_t head0 = (size_t)b * a.Hq + (size_t)c * G;
 
-    // ---- queries of this thread's score pairs (head g = pair / TILE) ----
-    // With 64-key tiles a wave's score pairs share one head, so its query row is
-    // wave-uniform and comes through the scalar cache (no vector-memory wait);
-    // otherwise each lane loads its own row.
-    constexpr int QW = D * C::ESZ / 4;   // 32-bit words of one query row
-    uint32_t qreg[C::PPT][QW];
-    #pragma unroll
-    for (int pp = 0; pp < C::PPT; ++pp) {
-        const int pr = tid + pp * kNT;
-        const int g = (pr < C::PAIRS ? pr : 0) / C::TILE;
-        const T *qrow = reinterpret_cast<const T *>(a.q) + ((size_t)b * a.Hq + (size_t)c * G + g) * D;
-        if constexpr (C::TILE == 64) {
-            load_uniform_dwords<QW>(qrow, qreg[pp]);
-        } else {
-            const uint4 *qs = reinterpret_cast<const uint4 *>(qrow);
-            #pragma unroll
-            for (int ch = 0; ch < C::CPR; ++ch) {
-                const uint4 v = qs[ch];
-                qreg[pp][4 * ch + 0] = v.x; qreg[pp][4 * ch + 1] = v.y;
-                qreg[pp][4 * ch + 2] = v.z; qreg[pp][4 * ch + 3] = v.w;
-            }
+    // ---- query rows ----
+    // QS: each wave's rows in SGPRs.  Otherwise the unit's G rows go to LDS by
+    // the same direct loads as the tiles (older than every tile load, so the
+    // first tile's wait covers them; lanes past the rows fetch the last chunk
+    // again into the padding of the region) and each lane copies its row out.
+    uint32_t qsr[C::QS ? C::HW : 1][C::QW];
+    if constexpr (C::QS) {
+        #pragma unroll
+        for (int hi = 0; hi < C::HW; ++hi) {
+            const int g = wq + 4 * hi;
+            load_uniform_dwords<C::QW>(reinterpret_cast<const T *>(a.q) + (head0 + (g < G ? g : 0)) * D, qsr[hi]);
+        }
+    } else {
+        const unsigned char *qsrc = reinterpret_cast<const unsigned char *>(a.q) + head0 * C::RB;
+        for (int off = wave * 1024; off < G * C::RB; off += C::NT * 16) {
+            const int o = min(off + lane * 16, G * C::RB - 16);
+            lds_stream16(qsrc + o, smem + C::OFF_Q + off);
         }
     }
+    const int qj = lane % C::TILE, qhs = lane / C::TILE;
+    uint32_t qv[C::QS ? 1 : C::NPASS][C::QW];
 
-    // ---- append the new token to the window ring (the workgroup holding it) ----
-    if (has_new && k0 <= n - 1 && n - 1 < k1) {
-        if (tid < 2 * C::CPR) {
-            int r = wst + wlen;
-            if (r >= w_cap) r -= w_cap;
-            const int ch = tid % C::CPR;
-            if (tid < C::CPR)
-                reinterpret_cast<uint4 *>(wk + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nk)[ch];
-            else
-                reinterpret_cast<uint4 *>(wv + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nv)[ch];
-        }
-    }
-    // Vector-memory operations issued above are older than every tile load, so
-    // the per-tile vmcnt waits below also cover them.
-
-    // ---- tile loader: direct HBM -> LDS, 2 K + 2 V instructions per thread ----
+    // ---- super-tile loader: direct HBM -> LDS, 2 K + 2 V instructions per thread ----
     auto row_src = [&](int kidx, bool is_v) -> const T * {
         if (kidx >= k1) kidx = k1 - 1;   // rows past the range load a valid row (weight 0)
         if (kidx < mlen) return (is_v ? mv : mk) + (size_t)kidx * D;
@@ -176,172 +298,266 @@ __global__ __launch_bounds__(kNT, 2) void decode_kernel(const DecodeArgs a) {
         }
         return is_v ? nv : nk;
     };
-    auto issue_tile = [&](int tile_base, int stage) {
-        unsigned char *st = sStage + stage * kStageBytes;
+    auto issue = [&](int tb, int stage) {
+        unsigned char *st = sStage + stage * C::SB;
+        // a full super-tile inside one segment (memory, or the ring without a
+        // wrap) has one base address for all its rows: a wave-uniform test
+        const T *kb = nullptr, *vb = nullptr;
+        if (tb + C::SUPER <= k1) {
+            if (tb + C::SUPER <= mlen) {
+                kb = mk + (size_t)tb * D;
+                vb = mv + (size_t)tb * D;
+            } else if (tb >= mlen && tb + C::SUPER <= mlen + wlen) {
+                int r0 = wst + (tb - mlen);
+                if (r0 >= w_cap) r0 -= w_cap;
+                if (r0 + C::SUPER <= w_cap) {
+                    kb = wk + (size_t)r0 * D;
+                    vb = wv + (size_t)r0 * D;
+                }
+            }
+        }
         #pragma unroll
         for (int l = 0; l < C::LPT; ++l) {
-            const int inst = l * 4 + wave;                 // 1 KB block of the 8 KB tensor tile
+            const int inst = l * C::NW + wave;             // 1 KB block of the NSUB x 8 KB tensor super-tile
             const int row = inst * C::RPI + lane / C::CPR;
             const int slot = lane % C::CPR;
-            const int kidx = tile_base + row;
-            const T *kp = row_src(kidx, false);
-            const T *vp = row_src(kidx, true);
+            const T *kp, *vp;
+            if (kb != nullptr) {
+                kp = kb + (size_t)row * D;
+                vp = vb + (size_t)row * D;
+            } else {
+                kp = row_src(tb + row, false);
+                vp = row_src(tb + row, true);
+            }
             // K: LDS slot `slot` of row `row` holds global chunk slot ^ (row & SW)
             lds_stream16(reinterpret_cast<const uint4 *>(kp) + (slot ^ (row & C::SW)), st + inst * 1024);
-            lds_stream16(reinterpret_cast<const uint4 *>(vp) + slot, st + 8192 + inst * 1024);
+            lds_stream16(reinterpret_cast<const uint4 *>(vp) + slot, st + NSUB * 8192 + inst * 1024);
         }
     };
 
-    // ---- running state ----
-    float m_run[C::PPT], l_lane[C::PPT];
+    // ---- running state of this wave (heads wq + 4 hi, keys of tile `grp`) ----
+    float m_run[C::NPASS], l_lane[C::NPASS];
     #pragma unroll
-    for (int pp = 0; pp < C::PPT; ++pp) { m_run[pp] = -INFINITY; l_lane[pp] = 0.f; }
-    float o_acc[G][2];
+    for (int p = 0; p < C::NPASS; ++p) { m_run[p] = -INFINITY; l_lane[p] = 0.f; }
+    float o_acc[C::HW][2];
     #pragma unroll
-    for (int g = 0; g < G; ++g) o_acc[g][0] = o_acc[g][1] = 0.f;
-    const int pv_dp = tid % C::DP, pv_ks = tid / C::DP;
+    for (int hi = 0; hi < C::HW; ++hi) o_acc[hi][0] = o_acc[hi][1] = 0.f;
+    const int pv_dp = lane % C::DW, pv_ks = lane / C::DW;
+    unsigned char *sP = smem + C::OFF_P + wave * (C::TILE * C::HW * 4);   // this wave's slice
+    const bool wave_active = wq < G;
 
-    const int ntiles = (k1 > k0) ? (k1 - k0 + C::TILE - 1) / C::TILE : 0;
+    const int nst = (k1 > k0) ? (k1 - k0 + C::SUPER - 1) / C::SUPER : 0;
     int issued = 0;
-    for (; issued < ntiles && issued < kStages - 1; ++issued) issue_tile(k0 + issued * C::TILE, issued);
+    for (; issued < nst && issued < C::STAGES - 1; ++issued) issue(k0 + issued * C::SUPER, issued);
 
-    for (int t = 0; t < ntiles; ++t) {
+    for (int t = 0; t < nst; ++t) {
         wait_vmcnt(4 * (issued - t - 1));
-        __syncthreads();   // tile t is in LDS for every wave; stage (t-1) % kStages is free
-        if (issued < ntiles) {
-            issue_tile(k0 + issued * C::TILE, issued % kStages);
+        __syncthreads();   // super-tile t is in LDS for every wave; stage (t-1) % STAGES is free
+        if (issued < nst) {
+            issue(k0 + issued * C::SUPER, issued % C::STAGES);
             ++issued;
         }
-        const unsigned char *st = sStage + (t % kStages) * kStageBytes;
-        const int base = k0 + t * C::TILE;
-
-        // ---- QK and softmax statistics: pair (g = pr / TILE, j = pr % TILE) ----
-        #pragma unroll
-        for (int pp = 0; pp < C::PPT; ++pp) {
-            const int pr = tid + pp * kNT;
-            const bool act = pr < C::PAIRS;
-            const int j = pr % C::TILE, g = (act ? pr : 0) / C::TILE;
-            float acc = 0.f;
-            const uint4 *krow = reinterpret_cast<const uint4 *>(st + j * C::RB);
+        const int base = k0 + t * C::SUPER + grp * C::TILE;   // first key of this group's tile
+        if (!wave_active || base >= k1) continue;
+        if (!C::QS && t == 0) {
+            // this lane's query row in each QK pass: head wq + 4 (pass * HPP + lane / TILE)
             #pragma unroll
-            for (int ch = 0; ch < C::CPR; ++ch) {
-                const uint4 kv = krow[ch ^ (j & C::SW)];
-                if constexpr (C::BF) {
-                    acc = dot2_bf16(qreg[pp][4 * ch + 0], kv.x, acc);
-                    acc = dot2_bf16(qreg[pp][4 * ch + 1], kv.y, acc);
-                    acc = dot2_bf16(qreg[pp][4 * ch + 2], kv.z, acc);
-                    acc = dot2_bf16(qreg[pp][4 * ch + 3], kv.w, acc);
-                } else {
-                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 0]), __uint_as_float(kv.x), acc);
-                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 1]), __uint_as_float(kv.y), acc);
-                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 2]), __uint_as_float(kv.z), acc);
-                    acc = fmaf(__uint_as_float(qreg[pp][4 * ch + 3]), __uint_as_float(kv.w), acc);
+            for (int p = 0; p < C::NPASS; ++p) {
+                const int hi = p * C::HPP + qhs, g = wq + 4 * hi;
+                const uint4 *qs = reinterpret_cast<const uint4 *>(smem + C::OFF_Q + ((hi < C::HW && g < G) ? g : 0) * C::RB);
+                #pragma unroll
+                for (int ch = 0; ch < C::QW / 4; ++ch) {
+                    const uint4 v = qs[ch];
+                    qv[p][4 * ch + 0] = v.x; qv[p][4 * ch + 1] = v.y; qv[p][4 * ch + 2] = v.z; qv[p][4 * ch + 3] = v.w;
                 }
             }
-            const float sc = (base + j < k1) ? acc * a.scale_log2 : -INFINITY;
-            const float tmax = group_max<C::TILE>(sc);
-            const float mn = fmaxf(m_run[pp], tmax);      // finite: every tile holds a valid key
-            const float alpha = exp2f(m_run[pp] - mn);
-            m_run[pp] = mn;
-            const float p = exp2f(sc - mn);
-            if constexpr (C::BF) {
-                // PV consumes the probabilities rounded to bf16 and packed by key
-                // pairs; the normaliser below sums the fp32 values
-                const uint32_t pb = (uint32_t)f32_to_bf16(p);
-                const uint32_t pn = (uint32_t)__float_as_int(xor_lane<1>(__int_as_float((int)pb)));
-                if (act && (j & 1) == 0)
-                    reinterpret_cast<uint32_t *>(smem + C::OFF_P)[(j >> 1) * G + g] = pb | (pn << 16);
-            } else {
-                if (act) reinterpret_cast<float *>(smem + C::OFF_P)[j * G + g] = p;
-            }
-            l_lane[pp] = fmaf(l_lane[pp], alpha, p);
-            if (act && j == 0) sAlpha[g] = alpha;
         }
-        __syncthreads();   // P and alpha ready
+        const unsigned char *st = sStage + (t % C::STAGES) * C::SB;
+        const unsigned char *sk = st + grp * 8192;
+        const unsigned char *sv = st + NSUB * 8192 + grp * 8192;
 
-        // ---- PV ----
-        float al[G];
+        // ---- QK, softmax statistics and the probabilities, pass by pass ----
+        float al[C::HW];
         #pragma unroll
-        for (int g = 0; g < G; ++g) al[g] = sAlpha[g];
-        #pragma unroll
-        for (int g = 0; g < G; ++g) { o_acc[g][0] *= al[g]; o_acc[g][1] *= al[g]; }
-        const unsigned char *sv = st + 8192;
-        #pragma unroll
-        for (int kk = 0; kk < C::KPS; kk += 2) {
-            const int j0 = pv_ks * C::KPS + kk;
-            if constexpr (C::BF) {
-                const uint32_t w0 = reinterpret_cast<const uint32_t *>(sv + j0 * C::RB)[pv_dp];
-                const uint32_t w1 = reinterpret_cast<const uint32_t *>(sv + (j0 + 1) * C::RB)[pv_dp];
-                const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x05040100u);   // feature 2dp, keys j0 | j0+1
-                const uint32_t hi = __builtin_amdgcn_perm(w1, w0, 0x07060302u);   // feature 2dp+1
-                const uint32_t *pj = reinterpret_cast<const uint32_t *>(smem + C::OFF_P) + (j0 >> 1) * G;
+        for (int p = 0; p < C::NPASS; ++p) {
+            const int hi = p * C::HPP + qhs;
+            const bool act = hi < C::HW && wq + 4 * hi < G;
+            const uint4 *krow = reinterpret_cast<const uint4 *>(sk + qj * C::RB);
+            float acc0 = 0.f, acc1 = 0.f;
+            #pragma unroll
+            for (int cb = 0; cb < C::CPR; cb += C::KB) {
+                uint4 kc[C::KB];
                 #pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const uint32_t pg = pj[g];
-                    o_acc[g][0] = dot2_bf16(pg, lo, o_acc[g][0]);
-                    o_acc[g][1] = dot2_bf16(pg, hi, o_acc[g][1]);
-                }
-            } else {
+                for (int i = 0; i < C::KB; ++i) kc[i] = krow[(cb + i) ^ (qj & C::SW)];
                 #pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const float2 w = reinterpret_cast<const float2 *>(sv + (j0 + e) * C::RB)[pv_dp];
-                    const float *pj = reinterpret_cast<const float *>(smem + C::OFF_P) + (j0 + e) * G;
-                    #pragma unroll
-                    for (int g = 0; g < G; ++g) {
-                        o_acc[g][0] = fmaf(pj[g], w.x, o_acc[g][0]);
-                        o_acc[g][1] = fmaf(pj[g], w.y, o_acc[g][1]);
+                for (int i = 0; i < C::KB; ++i) {
+                    const uint32_t *qq = C::QS ? &qsr[p][4 * (cb + i)] : &qv[p][4 * (cb + i)];
+                    float &acc = (i & 1) ? acc1 : acc0;
+                    if constexpr (C::BF) {
+                        acc = dot2_bf16(qq[0], kc[i].x, acc);
+                        acc = dot2_bf16(qq[1], kc[i].y, acc);
+                        acc = dot2_bf16(qq[2], kc[i].z, acc);
+                        acc = dot2_bf16(qq[3], kc[i].w, acc);
+                    } else {
+                        acc = fmaf(__uint_as_float(qq[0]), __uint_as_float(kc[i].x), acc);
+                        acc = fmaf(__uint_as_float(qq[1]), __uint_as_float(kc[i].y), acc);
+                        acc = fmaf(__uint_as_float(qq[2]), __uint_as_float(kc[i].z), acc);
+                        acc = fmaf(__uint_as_float(qq[3]), __uint_as_float(kc[i].w), acc);
                     }
                 }
             }
-        }
-    }
-
-    // ---- per-head totals: lanes of one pair group share a head ----
-    #pragma unroll
-    for (int pp = 0; pp < C::PPT; ++pp) {
-        const int pr = tid + pp * kNT;
-        float lt = l_lane[pp];
-        #pragma unroll
-        for (int k = 1; k < C::TILE; k <<= 1) lt += __shfl_xor(lt, k, 64);
-        if (pr < C::PAIRS && pr % C::TILE == 0) {
-            const int g = pr / C::TILE;
-            sFin[2 * g] = m_run[pp];   // -inf when this split had no keys
-            sFin[2 * g + 1] = lt;
-        }
-    }
-    #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        sO[(pv_ks * G + g) * D + 2 * pv_dp] = o_acc[g][0];
-        sO[(pv_ks * G + g) * D + 2 * pv_dp + 1] = o_acc[g][1];
-    }
-    __syncthreads();
-
-    const int n_splits = a.n_splits;
-    const size_t head0 = (size_t)b * a.Hq + (size_t)c * G;
-    T *out = reinterpret_cast<T *>(a.out) + head0 * D;
-    if (n_splits == 1) {
-        for (int idx = tid; idx < G * D; idx += kNT) {
-            const int g = idx / D;
-            float o = 0.f;
+            const float sc = (act && base + qj < k1) ? (acc0 + acc1) * a.scale_log2 : -INFINITY;
+            const float tmax = group_max_b<C::TILE>(sc, lane);
+            const float mn = fmaxf(m_run[p], tmax);
+            const bool live = mn != -INFINITY;   // false only for heads this lane does not own
+            const float alpha = live ? __builtin_amdgcn_exp2f(m_run[p] - mn) : 1.f;
+            const float pr = live ? __builtin_amdgcn_exp2f(sc - mn) : 0.f;
+            m_run[p] = mn;
+            l_lane[p] = fmaf(l_lane[p], alpha, pr);
+            if constexpr (C::BF) {
+                // PV consumes the probabilities rounded to bf16 and packed by key pairs
+                const uint32_t pb = (uint32_t)f32_to_bf16(pr);
+                const uint32_t pn = (uint32_t)__float_as_int(xor_lane<1>(__int_as_float((int)pb)));
+                if (act && (qj & 1) == 0)
+                    reinterpret_cast<uint32_t *>(sP)[(qj >> 1) * C::HW + hi] = pb | (pn << 16);
+            } else {
+                if (act) reinterpret_cast<float *>(sP)[qj * C::HW + hi] = pr;
+            }
             #pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) o += sO[ks * G * D + idx];
-            const float mm = sFin[2 * g], l = sFin[2 * g + 1];
-            Elem<T>::store1(out + idx, l > 0.f ? o / l : 0.f);
-            if (a.lse && (idx % D) == 0) a.lse[head0 + g] = l > 0.f ? (mm + log2f(l)) * kLn2 : -INFINITY;
+            for (int hs = 0; hs < C::HPP; ++hs)
+                if (p * C::HPP + hs < C::HW) al[p * C::HPP + hs] = read_lane(alpha, hs * C::TILE);
         }
-        return;
+
+        // ---- PV over this wave's heads ----
+        #pragma unroll
+        for (int hi = 0; hi < C::HW; ++hi) { o_acc[hi][0] *= al[hi]; o_acc[hi][1] *= al[hi]; }
+        if constexpr (C::BF) {
+            // all V words and probabilities of the tile first, then the products
+            // (one LDS round trip instead of one per key pair)
+            uint32_t vw[C::KPL], pw[C::KPL / 2][C::HW];
+            #pragma unroll
+            for (int k = 0; k < C::KPL; ++k)
+                vw[k] = reinterpret_cast<const uint32_t *>(sv + (pv_ks * C::KPL + k) * C::RB)[pv_dp];
+            #pragma unroll
+            for (int k = 0; k < C::KPL / 2; ++k)
+                #pragma unroll
+                for (int hi = 0; hi < C::HW; ++hi)
+                    pw[k][hi] = reinterpret_cast<const uint32_t *>(sP)[((pv_ks * C::KPL >> 1) + k) * C::HW + hi];
+            #pragma unroll
+            for (int k = 0; k < C::KPL / 2; ++k) {
+                const uint32_t lo = __builtin_amdgcn_perm(vw[2 * k + 1], vw[2 * k], 0x05040100u);   // feature 2dp
+                const uint32_t hi2 = __builtin_amdgcn_perm(vw[2 * k + 1], vw[2 * k], 0x07060302u);  // feature 2dp+1
+                #pragma unroll
+                for (int hi = 0; hi < C::HW; ++hi) {
+                    o_acc[hi][0] = dot2_bf16(pw[k][hi], lo, o_acc[hi][0]);
+                    o_acc[hi][1] = dot2_bf16(pw[k][hi], hi2, o_acc[hi][1]);
+                }
+            }
+        } else {
+            float2 vf[C::KPL];
+            #pragma unroll
+            for (int k = 0; k < C::KPL; ++k)
+                vf[k] = reinterpret_cast<const float2 *>(sv + (pv_ks * C::KPL + k) * C::RB)[pv_dp];
+            #pragma unroll
+            for (int k = 0; k < C::KPL; ++k) {
+                const float *pj = reinterpret_cast<const float *>(sP) + (pv_ks * C::KPL + k) * C::HW;
+                #pragma unroll
+                for (int hi = 0; hi < C::HW; ++hi) {
+                    const float pf = pj[hi];
+                    o_acc[hi][0] = fmaf(pf, vf[k].x, o_acc[hi][0]);
+                    o_acc[hi][1] = fmaf(pf, vf[k].y, o_acc[hi][1]);
+                }
+            }
+        }
     }
 
-    // ---- partial of this split: unit block = [o: n_splits][G][D] [ml: n_splits][G][2] ----
-    float *blk = a.part + (size_t)u * a.part_stride;
-    float *po = blk + (size_t)s * G * D;
-    for (int idx = tid; idx < G * D; idx += kNT) {
-        float o = 0.f;
-        #pragma unroll
-        for (int ks = 0; ks < C::KS; ++ks) o += sO[ks * G * D + idx];
-        store_agent(po + idx, o);
+    // ---- append the new token to the window ring (the workgroup holding it) ----
+    // Its row is outside every window of this launch (the window ends just
+    // before it), and attention above read the token from k_new / v_new.
+    if (has_new && k0 <= n - 1 && n - 1 < k1) {
+        if (tid < 2 * C::CPR) {
+            int r = wst + wlen;
+            if (r >= w_cap) r -= w_cap;
+            const int ch = tid % C::CPR;
+            if (tid < C::CPR)
+                reinterpret_cast<uint4 *>(wk + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nk)[ch];
+            else
+                reinterpret_cast<uint4 *>(wv + (size_t)r * D)[ch] = reinterpret_cast<const uint4 *>(nv)[ch];
+        }
     }
-    if (tid < 2 * G) store_agent(blk + (size_t)n_splits * G * D + (size_t)s * 2 * G + tid, sFin[tid]);
+
+    // ---- this wave's per-head (max, sum, o) ----
+    const int n_splits = a.n_splits;
+    T *out = reinterpret_cast<T *>(a.out) + head0 * D;
+    float *blk = a.part + (size_t)u * a.part_stride;
+    // group results go to LDS ([group][G][D] o, then [group][G] (max, sum)) and
+    // are merged there; one group writes them straight out
+    float *go = reinterpret_cast<float *>(sStage);
+    float2 *gml = reinterpret_cast<float2 *>(go + NSUB * G * D);
+    if constexpr (NSUB > 1) __syncthreads();   // every wave is done with the stages
+    if (wave_active) {
+        float l_tot[C::NPASS];
+        #pragma unroll
+        for (int p = 0; p < C::NPASS; ++p) l_tot[p] = group_sum<C::TILE>(l_lane[p]);
+        #pragma unroll
+        for (int hi = 0; hi < C::HW; ++hi) {
+            if constexpr (C::KSW == 2) {
+                o_acc[hi][0] += __shfl_xor(o_acc[hi][0], 32, 64);
+                o_acc[hi][1] += __shfl_xor(o_acc[hi][1], 32, 64);
+            }
+        }
+        #pragma unroll
+        for (int hi = 0; hi < C::HW; ++hi) {
+            const int g = wq + 4 * hi;
+            if (g >= G) continue;
+            const int p = hi / C::HPP, hs = hi % C::HPP;
+            const float mm = read_lane(m_run[p], hs * C::TILE);   // -inf when the group had no keys
+            const float l = read_lane(l_tot[p], hs * C::TILE);
+            if constexpr (NSUB > 1) {
+                if (pv_ks == 0)
+                    reinterpret_cast<float2 *>(go + ((size_t)grp * G + g) * D)[pv_dp] = make_float2(o_acc[hi][0], o_acc[hi][1]);
+                if (lane == 0) gml[grp * G + g] = make_float2(mm, l);
+            } else if (n_splits == 1) {
+                if (pv_ks == 0) {
+                    const float inv = l > 0.f ? 1.f / l : 0.f;
+                    Elem<T>::store1(out + g * D + 2 * pv_dp, o_acc[hi][0] * inv);
+                    Elem<T>::store1(out + g * D + 2 * pv_dp + 1, o_acc[hi][1] * inv);
+                }
+                if (a.lse && lane == 0) a.lse[head0 + g] = l > 0.f ? (mm + log2f(l)) * kLn2 : -INFINITY;
+            } else {
+                // partial of this split: unit block = [o: n_splits][G][D] [ml: n_splits][G][2]
+                float *po = blk + ((size_t)s * G + g) * D;
+                if (pv_ks == 0) store_agent2(po + 2 * pv_dp, o_acc[hi][0], o_acc[hi][1]);
+                if (lane == 0) store_agent2(blk + (size_t)n_splits * G * D + ((size_t)s * G + g) * 2, mm, l);
+            }
+        }
+    }
+    if constexpr (NSUB > 1) {
+        __syncthreads();
+        // merge the groups: per (head g, feature d), weights 2^(m_j - M)
+        for (int idx = tid; idx < G * D; idx += C::NT) {
+            const int g = idx / D;
+            float mj[NSUB], M = -INFINITY;
+            #pragma unroll
+            for (int j = 0; j < NSUB; ++j) { mj[j] = gml[j * G + g].x; M = fmaxf(M, mj[j]); }
+            float L = 0.f, O = 0.f;
+            #pragma unroll
+            for (int j = 0; j < NSUB; ++j) {
+                const float w = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mj[j] - M);
+                L = fmaf(w, gml[j * G + g].y, L);
+                O = fmaf(w, go[(size_t)j * G * D + idx], O);
+            }
+            if (n_splits == 1) {
+                Elem<T>::store1(out + idx, L > 0.f ? O / L : 0.f);
+                if (a.lse && idx % D == 0) a.lse[head0 + g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+            } else {
+                store_agent(blk + (size_t)s * G * D + idx, O);
+                if (idx % D == 0) store_agent2(blk + (size_t)n_splits * G * D + ((size_t)s * G + g) * 2, M, L);
+            }
+        }
+    }
+    if (n_splits == 1) return;
+    // every head g < G belongs to exactly one active wave: the block is complete
     wait_vm_stores();
     __syncthreads();
     __shared__ int s_last;
@@ -353,57 +569,53 @@ __global__ __launch_bounds__(kNT, 2) void decode_kernel(const DecodeArgs a) {
     }
     __syncthreads();
     if (!s_last) return;
-
-    // ---- last workgroup: pull all partials into LDS in one round trip ----
-    const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
-    for (int off = wave * 1024; off < nbytes; off += 4096) {
-        if (off + lane * 16 < nbytes)
-            lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, sStage + off);
-    }
-    wait_vmcnt(0);
-    __syncthreads();
-    const float *lo = reinterpret_cast<const float *>(sStage);
-    const float *lml = lo + (size_t)n_splits * G * D;
-    for (int idx = tid; idx < G * D; idx += kNT) {
-        const int g = idx / D;
-        float M = -INFINITY;
-        for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, lml[sp * 2 * G + 2 * g]);
-        float acc = 0.f, L = 0.f;
-        if (M != -INFINITY) {
-            for (int sp = 0; sp < n_splits; ++sp) {
-                const float wgt = exp2f(lml[sp * 2 * G + 2 * g] - M);
-                L = fmaf(wgt, lml[sp * 2 * G + 2 * g + 1], L);
-                acc = fmaf(wgt, lo[(size_t)sp * G * D + idx], acc);
-            }
-        }
-        Elem<T>::store1(out + idx, L > 0.f ? acc / L : 0.f);
-        if (a.lse && (idx % D) == 0) a.lse[head0 + g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
-    }
+    merge_splits<T, D, G, C::NT>(blk, n_splits, sStage, reinterpret_cast<float *>(smem + C::OFF_WN), out,
+                                 a.lse ? a.lse + head0 : nullptr);
 }
 
 // ------------------------------------------------------------------ host ----
 
 int decode_max_splits(int d, int G) {
-    const int cap = kStages * kStageBytes / (G * (d + 2) * 4);   // merge block must fit the stage LDS
+    const int cap = kMergeLds / (G * (d + 2) * 4);   // merge block must fit its LDS
     return cap < kDecodeMaxSplits ? cap : kDecodeMaxSplits;
 }
 
 static int decode_tile(int dtype, int d) { return 8192 / (d * (dtype == MAD_BF16 ? 2 : 4)); }
+
+// Four-group workgroups (16 waves, one per CU) for bf16 with head_dim 64 and
+// at most 4 query heads per KV head when few units hold many keys (a long
+// stream per CU, where fewer, larger merges pay); single-group workgroups (4
+// waves, two per CU) elsewhere, where the first loads spread over more CUs.
+static int decode_nsub(int units, int n_max, int G, int d, int dtype) {
+    const bool wide = units <= kDecodeWideUnits && (int64_t)units * n_max >= kDecodeWideKeys;
+    return (dtype == MAD_BF16 && d == 64 && G <= 4 && wide) ? 4 : 1;
+}
 
 DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys) {
     DecodePlan p;
     p.units = B * Hkv;
     p.n_max = 0;
     for (int b = 0; b < B; ++b) p.n_max = n_keys[b] > p.n_max ? n_keys[b] : p.n_max;
-    const int tile = decode_tile(dtype, d);
-    int ns = (kDecodeTargetWGs + p.units - 1) / p.units;
+    p.nsub = decode_nsub(p.units, p.n_max, G, d, dtype);
+    const int super = p.nsub * decode_tile(dtype, d);
+    // workgroups to fill the machine: one per CU with 16 waves, two with 4
+    const int target = p.nsub > 1 ? kDecodeCUs : 2 * kDecodeCUs;
+    int ns = (target + p.units - 1) / p.units;
     const int cap = decode_max_splits(d, G);
     if (ns > cap) ns = cap;
     if (ns < 1) ns = 1;
-    int chunk = (p.n_max + ns - 1) / ns;
-    chunk = ((chunk + tile - 1) / tile) * tile;
-    if (chunk < tile) chunk = tile;
+    // whole super-tiles per split; the count is planned on n - 1 keys so that a
+    // lone new token (n = k * chunk + 1) becomes a short extra split, which the
+    // grid dispatches first, rather than one more super-tile for every split
+    const int base = p.n_max > 1 ? p.n_max - 1 : 1;
+    int chunk = (base + ns - 1) / ns;
+    chunk = (chunk + super - 1) / super * super;
     ns = (p.n_max + chunk - 1) / chunk;
+    if (ns > cap) {   // the extra split would not fit the merge: one more super-tile each
+        chunk = (p.n_max + cap - 1) / cap;
+        chunk = (chunk + super - 1) / super * super;
+        ns = (p.n_max + chunk - 1) / chunk;
+    }
     p.n_splits = ns < 1 ? 1 : ns;
     p.chunk = chunk;
     return p;
@@ -418,22 +630,33 @@ size_t decode_ws_bytes(int B, int Hq, int Hkv, int d) {
     return kCounterRegionBytes + (size_t)B * Hkv * decode_part_stride(d, Hq / Hkv) * 4 + 256;
 }
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, int NSUB>
 static hipError_t launch_t(const DecodeArgs &a, hipStream_t st) {
-    using C = DecodeCfg<T, D, G>;
-    dim3 grid((unsigned)(a.units * a.n_splits)), block(kNT);
-    hipLaunchKernelGGL((decode_kernel<T, D, G>), grid, block, C::SMEM, st, a);
+    using C = DecodeCfg<T, D, G, NSUB>;
+    dim3 grid((unsigned)(a.units * a.n_splits)), block(C::NT);
+    hipLaunchKernelGGL((decode_kernel<T, D, G, NSUB>), grid, block, C::SMEM, st, a);
     return hipGetLastError();
 }
 
 template <typename T, int D>
 static hipError_t launch_g(const DecodeArgs &a, int G, hipStream_t st) {
+    if constexpr (std::is_same<T, bf16_t>::value && D == 64) {
+        if (a.nsub == 4) {
+            switch (G) {
+                case 1: return launch_t<T, D, 1, 4>(a, st);
+                case 2: return launch_t<T, D, 2, 4>(a, st);
+                case 4: return launch_t<T, D, 4, 4>(a, st);
+            }
+            return hipErrorInvalidValue;
+        }
+    }
+    if (a.nsub != 1) return hipErrorInvalidValue;
     switch (G) {
-        case 1: return launch_t<T, D, 1>(a, st);
-        case 2: return launch_t<T, D, 2>(a, st);
-        case 4: return launch_t<T, D, 4>(a, st);
-        case 8: return launch_t<T, D, 8>(a, st);
-        case 16: return launch_t<T, D, 16>(a, st);
+        case 1: return launch_t<T, D, 1, 1>(a, st);
+        case 2: return launch_t<T, D, 2, 1>(a, st);
+        case 4: return launch_t<T, D, 4, 1>(a, st);
+        case 8: return launch_t<T, D, 8, 1>(a, st);
+        case 16: return launch_t<T, D, 16, 1>(a, st);
     }
     return hipErrorInvalidValue;
 }

@@ -154,6 +154,7 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     a.Hkv = Hkv;
     a.units = p.units;
     a.n_splits = p.n_splits;
+    a.nsub = p.nsub;
     a.chunk = p.chunk;
     if (need > 0) {
         a.counters = (unsigned *)ws;

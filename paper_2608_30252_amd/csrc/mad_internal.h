@@ -12,20 +12,11 @@ namespace mad {
 constexpr int kMaxB = MAD_MAX_BATCH;
 
 // ---------------------------------------------------------------- decode ----
-// Keys per split are a multiple of kDecodeChunkQuant and at least
-// kDecodeMinChunk; the split count aims at kDecodeTargetWGs workgroups.
-#ifndef MAD_DECODE_TARGET_WGS
-#define MAD_DECODE_TARGET_WGS 1024
-#endif
-#ifndef MAD_DECODE_MIN_CHUNK
-#define MAD_DECODE_MIN_CHUNK 32
-#endif
-#ifndef MAD_DECODE_CHUNK_QUANT
-#define MAD_DECODE_CHUNK_QUANT 16
-#endif
-constexpr int kDecodeTargetWGs = MAD_DECODE_TARGET_WGS;
-constexpr int kDecodeMinChunk = MAD_DECODE_MIN_CHUNK;
-constexpr int kDecodeChunkQuant = MAD_DECODE_CHUNK_QUANT;
+// The split count aims at one 16-wave or two 4-wave workgroups per CU; splits
+// are whole super-tiles (see plan_decode).
+constexpr int kDecodeCUs = 256;        // compute units of the device the split plan is sized for
+constexpr int kDecodeWideUnits = 32;        // 16-wave workgroups: at most this many units
+constexpr int kDecodeWideKeys = 65536;      //   holding at least this many keys in all
 constexpr int kDecodeMaxSplits = 256;
 // Every workspace starts with a fixed counter region that holds nothing but
 // arrival counters (one per 256-byte line) and that every kernel leaves at
@@ -53,11 +44,12 @@ struct DecodeArgs {
     unsigned *counters;   // counter region: unit u on line u
     float scale_log2;     // softmax scale * log2(e)
     int Hq, Hkv, units, n_splits, chunk, w_cap;
+    int nsub;             // wave groups per workgroup (1 or 4)
     int mlen[kMaxB], wstart[kMaxB], wlen[kMaxB];
 };
 
 struct DecodePlan {
-    int units, n_splits, chunk, n_max;
+    int units, n_splits, chunk, n_max, nsub;
 };
 
 DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys);
