@@ -57,7 +57,30 @@ def parse():
     ap.add_argument("--sets", type=int, default=6, help="sequences decoded round-robin (cold HBM reads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--summarize-trace", metavar="CSV",
+                    help="print per-(kernel, grid) durations of a rocprofv3 kernel_trace.csv and exit")
     return ap.parse_args()
+
+
+def summarize_trace(path):
+    """Durations of the library's kernels in a rocprofv3 --kernel-trace CSV,
+    grouped by kernel and launch shape (grid and workgroup size)."""
+    import csv
+    import statistics
+    groups = {}
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            name = row["Kernel_Name"]
+            if "mad::" not in name:
+                continue
+            short = name.split("(")[0].replace("void ", "")
+            key = (short, int(row["Grid_Size_X"]), int(row["Workgroup_Size_X"]))
+            groups.setdefault(key, []).append((int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3)
+    print(f"{'kernel':48s} {'grid':>8s} {'wg':>5s} {'calls':>6s} {'mean_us':>8s} {'p10':>8s} {'median':>8s} {'p90':>8s}")
+    for (short, grid, wg), d in sorted(groups.items()):
+        d.sort()
+        print(f"{short:48s} {grid // wg:8d} {wg:5d} {len(d):6d} {sum(d) / len(d):8.2f} {d[len(d) // 10]:8.2f} "
+              f"{statistics.median(d):8.2f} {d[9 * len(d) // 10]:8.2f}")
 
 
 def kv_bytes(keys, hkv, d, esz=2):
@@ -214,6 +237,9 @@ def traffic_from_profile(kernel_file, bytes_default=None):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)

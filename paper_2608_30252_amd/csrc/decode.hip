@@ -237,7 +237,7 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
 }
 
 template <typename T, int D, int G, int NSUB>
-__global__ __launch_bounds__(256 * NSUB, NSUB == 1 ? 2 : 1) void decode_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(const DecodeArgs a) {
     using C = DecodeCfg<T, D, G, NSUB>;
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *sStage = smem;
@@ -582,13 +582,18 @@ int decode_max_splits(int d, int G) {
 
 static int decode_tile(int dtype, int d) { return 8192 / (d * (dtype == MAD_BF16 ? 2 : 4)); }
 
-// Four-group workgroups (16 waves, one per CU) for bf16 with head_dim 64 and
-// at most 4 query heads per KV head when few units hold many keys (a long
-// stream per CU, where fewer, larger merges pay); single-group workgroups (4
-// waves, two per CU) elsewhere, where the first loads spread over more CUs.
+// Two-group workgroups (8 waves, two per CU) for bf16 with head_dim 64 and at
+// most 4 query heads per KV head when few units hold many keys (long streams,
+// where two tiles in flight per workgroup and fewer partials pay); one-group
+// workgroups (4 waves, one per CU, about two tiles per split) elsewhere, where
+// the first loads are spread over as many CUs as possible.
 static int decode_nsub(int units, int n_max, int G, int d, int dtype) {
+    if (!(dtype == MAD_BF16 && d == 64 && G <= 4)) return 1;
+#ifdef MAD_DECODE_FORCE_NSUB
+    return MAD_DECODE_FORCE_NSUB;
+#endif
     const bool wide = units <= kDecodeWideUnits && (int64_t)units * n_max >= kDecodeWideKeys;
-    return (dtype == MAD_BF16 && d == 64 && G <= 4 && wide) ? 4 : 1;
+    return wide ? 2 : 1;
 }
 
 DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys) {
@@ -598,22 +603,28 @@ DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_key
     for (int b = 0; b < B; ++b) p.n_max = n_keys[b] > p.n_max ? n_keys[b] : p.n_max;
     p.nsub = decode_nsub(p.units, p.n_max, G, d, dtype);
     const int super = p.nsub * decode_tile(dtype, d);
-    // workgroups to fill the machine: one per CU with 16 waves, two with 4
-    const int target = p.nsub > 1 ? kDecodeCUs : 2 * kDecodeCUs;
+    // workgroups to aim for: two per CU with 8 waves, one with 4
+    const int target = (p.nsub == 2 ? 2 * kDecodeCUs : kDecodeCUs) / kDecodeTargetDiv;
     int ns = (target + p.units - 1) / p.units;
     const int cap = decode_max_splits(d, G);
     if (ns > cap) ns = cap;
     if (ns < 1) ns = 1;
-    // whole super-tiles per split; the count is planned on n - 1 keys so that a
-    // lone new token (n = k * chunk + 1) becomes a short extra split, which the
-    // grid dispatches first, rather than one more super-tile for every split
-    const int base = p.n_max > 1 ? p.n_max - 1 : 1;
-    int chunk = (base + ns - 1) / ns;
-    chunk = (chunk + super - 1) / super * super;
+    // Whole super-tiles per split.  Rounding the even share down leaves a few
+    // keys (e.g. the new token) for one short extra split per unit, which the
+    // grid dispatches first; when the leftover is more than a sliver the share
+    // is rounded up instead (one split fewer, the last one short).
+    const int share = p.n_max / ns;
+    const int down = share / super * super;
+    int chunk;
+    if (down >= super && p.n_max - ns * down <= down / 8) {
+        chunk = down;
+    } else {
+        chunk = ((p.n_max + ns - 1) / ns + super - 1) / super * super;
+    }
+    if (chunk < super) chunk = super;
     ns = (p.n_max + chunk - 1) / chunk;
-    if (ns > cap) {   // the extra split would not fit the merge: one more super-tile each
-        chunk = (p.n_max + cap - 1) / cap;
-        chunk = (chunk + super - 1) / super * super;
+    if (ns > cap) {   // the extra split would not fit the merge
+        chunk = ((p.n_max + cap - 1) / cap + super - 1) / super * super;
         ns = (p.n_max + chunk - 1) / chunk;
     }
     p.n_splits = ns < 1 ? 1 : ns;
@@ -641,11 +652,11 @@ static hipError_t launch_t(const DecodeArgs &a, hipStream_t st) {
 template <typename T, int D>
 static hipError_t launch_g(const DecodeArgs &a, int G, hipStream_t st) {
     if constexpr (std::is_same<T, bf16_t>::value && D == 64) {
-        if (a.nsub == 4) {
+        if (a.nsub == 2) {
             switch (G) {
-                case 1: return launch_t<T, D, 1, 4>(a, st);
-                case 2: return launch_t<T, D, 2, 4>(a, st);
-                case 4: return launch_t<T, D, 4, 4>(a, st);
+                case 1: return launch_t<T, D, 1, 2>(a, st);
+                case 2: return launch_t<T, D, 2, 2>(a, st);
+                case 4: return launch_t<T, D, 4, 2>(a, st);
             }
             return hipErrorInvalidValue;
         }

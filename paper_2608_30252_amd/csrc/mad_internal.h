@@ -12,11 +12,15 @@ namespace mad {
 constexpr int kMaxB = MAD_MAX_BATCH;
 
 // ---------------------------------------------------------------- decode ----
-// The split count aims at one 16-wave or two 4-wave workgroups per CU; splits
+// The split count aims at one 4-wave or two 8-wave workgroups per CU; splits
 // are whole super-tiles (see plan_decode).
 constexpr int kDecodeCUs = 256;        // compute units of the device the split plan is sized for
-constexpr int kDecodeWideUnits = 32;        // 16-wave workgroups: at most this many units
+constexpr int kDecodeWideUnits = 32;        // 8-wave workgroups: at most this many units
 constexpr int kDecodeWideKeys = 65536;      //   holding at least this many keys in all
+#ifndef MAD_DECODE_TARGET_DIV
+#define MAD_DECODE_TARGET_DIV 1
+#endif
+constexpr int kDecodeTargetDiv = MAD_DECODE_TARGET_DIV;   // fewer, longer splits (tuning)
 constexpr int kDecodeMaxSplits = 256;
 // Every workspace starts with a fixed counter region that holds nothing but
 // arrival counters (one per 256-byte line) and that every kernel leaves at
@@ -44,7 +48,7 @@ struct DecodeArgs {
     unsigned *counters;   // counter region: unit u on line u
     float scale_log2;     // softmax scale * log2(e)
     int Hq, Hkv, units, n_splits, chunk, w_cap;
-    int nsub;             // wave groups per workgroup (1 or 4)
+    int nsub;             // wave groups per workgroup (1 or 2)
     int mlen[kMaxB], wstart[kMaxB], wlen[kMaxB];
 };
 
