@@ -59,7 +59,58 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--summarize-trace", metavar="CSV",
                     help="print per-(kernel, grid) durations of a rocprofv3 kernel_trace.csv and exit")
+    ap.add_argument("--pmc-workload", choices=("decode", "copy"),
+                    help="run only a counter workload (under rocprofv3 --pmc): 'decode' = the headline's "
+                         "compact-memory decode launches, 'copy' = a streaming copy of known size")
+    ap.add_argument("--summarize-counters", metavar="CSV",
+                    help="print per-(kernel, grid) mean counter values of a rocprofv3 counter_collection.csv")
     return ap.parse_args()
+
+
+COPY_FLOATS = 64 << 20   # the calibration copy: 256 MiB read + 256 MiB written
+
+
+def pmc_workload(kind):
+    """Kernels whose hardware counters calibrate or measure HBM traffic."""
+    import torch
+    import paper_2608_30252_amd as mad
+    if kind == "copy":
+        src = torch.ones(COPY_FLOATS, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(4):
+            torch.mul(src, 1.0, out=dst)   # one elementwise kernel: 4 B read + 4 B written per element
+        torch.cuda.synchronize()
+        print(f"copy: 4 launches of {COPY_FLOATS * 4} B read + {COPY_FLOATS * 4} B written", flush=True)
+        return
+    model = DraftModel(torch, mad, 6)
+    n = 0
+    for k in range(4):
+        for i in range(model.n_sets):
+            view = model.lay.decode_view(model.prefix + k)
+            for l in range(model.layers):
+                mad.draft_decode_attn(model.q[l], mad.KV(model.mem_k[i][l], model.mem_v[i][l], [view.mem_len]),
+                                      mad.KV(model.ring_k[i][l], model.ring_v[i][l], [view.win_len],
+                                             [view.win_start]),
+                                      model.kn[l], model.vn[l], model.out[l], model.lse[l], ws=model.ws)
+                n += 1
+    torch.cuda.synchronize()
+    print(f"decode: {n} compact-memory launches, {kv_bytes(3073, model.Hkv, model.d)} B of K/V each", flush=True)
+
+
+def summarize_counters(path):
+    """Mean value per dispatch of each counter in a rocprofv3 --pmc counter_collection.csv,
+    grouped by the library's kernel (or any kernel for the copy) and grid."""
+    import csv
+    groups = {}
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            name = row["Kernel_Name"].replace("void ", "").split("(")[0]
+            grid = row.get("Grid_Size") or row.get("Grid_Size_X") or "?"
+            key = (name[:60], grid, row["Counter_Name"])
+            groups.setdefault(key, []).append(float(row["Counter_Value"]))
+    for (name, grid, ctr), v in sorted(groups.items()):
+        print(f"{name:60s} grid {grid:>8s} {ctr:12s} n {len(v):4d} mean {sum(v) / len(v):14.1f}")
 
 
 def summarize_trace(path):
@@ -239,6 +290,12 @@ def main():
     args = parse()
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
+    if args.pmc_workload:
+        pmc_workload(args.pmc_workload)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
