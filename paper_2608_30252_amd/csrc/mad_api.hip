@@ -213,6 +213,7 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
         if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
         a.KS = p.KS;
         a.kc = p.kc;
+        a.stages = p.stages;
         a.counters = (unsigned *)ws;
         a.part = (float *)((char *)ws + mad::kCounterRegionBytes);
         a.part_stride = (int64_t)mad::update_part_stride(R, d, p.KS);

@@ -63,7 +63,11 @@ size_t decode_ws_bytes(int B, int Hq, int Hkv, int d);
 hipError_t launch_decode(const DecodeArgs &a, int dtype, int d, int G, hipStream_t st);
 
 // ---------------------------------------------------------------- update ----
-constexpr size_t kUpdateMergeBytes = 65536;   // LDS for the split merge
+constexpr size_t kUpdateMaxLds = 160 * 1024 - 512;   // LDS a workgroup may use (staging ring or split merge)
+#ifndef MAD_UPDATE_TARGET_WGS
+#define MAD_UPDATE_TARGET_WGS 256
+#endif
+constexpr int kUpdateTargetWGs = MAD_UPDATE_TARGET_WGS;   // the k-split aims at this many workgroups
 
 struct UpdateArgs {
     const void *x, *w;    // [R][D] slot rows, [2*Hkv*d][D] mirrored projections
@@ -73,14 +77,14 @@ struct UpdateArgs {
     int64_t part_stride;
     unsigned *counters;   // counter region: head block hb on line hb
     double log2_base;     // log2 of the RoPE base
-    int R, n_new, D, Hkv, d, KS, kc;
+    int R, n_new, D, Hkv, d, KS, kc, stages;
     int mlen[kMaxB];
     int pos[MAD_MAX_UPDATE_ROWS];
     unsigned char fire[kMaxB];
 };
 
 struct UpdatePlan {
-    int KS, kc;   // k-splits and the input-width chunk of each
+    int KS, kc, stages;   // k-splits, the input-width chunk of each, LDS ring stages
 };
 
 UpdatePlan plan_update(int R, int D, int Hkv, int d);

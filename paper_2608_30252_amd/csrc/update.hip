@@ -10,11 +10,13 @@
 // BF16: the projection Y[R x N] = X[R x D] W^T runs on the matrix cores
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  Workgroup (head block hb,
 // k-split ks) owns the d output features of one K or V head and a slice of the
-// input width; every wave covers d/4 features for all rows.  W is streamed
-// once from HBM straight into the MFMA operand registers (16 bytes a lane).
-// Split partials go to the workspace with device-coherent stores; the last
-// workgroup of a head block (arrival counter) pulls them into LDS in one round
-// trip, sums them, applies RoPE with fp64 angles and writes bf16 rows.
+// input width.  Its X and W slices stream from HBM straight into LDS
+// (global_load_lds_dwordx4) in 64-wide k chunks through a two-stage ring, 16-byte
+// chunks XOR-swizzled by row so the MFMA operand reads are conflict-free; every
+// wave covers d/4 features for all rows.  Split partials go to the workspace
+// with device-coherent stores; the last workgroup of a head block (arrival
+// counter) pulls them into LDS in one round trip, sums them, applies RoPE with
+// fp64 angles and writes bf16 rows.
 // F32: a vector-ALU kernel, one thread per (row, rotation pair).
 #include "mad_device.h"
 #include "mad_internal.h"
@@ -24,20 +26,105 @@ namespace mad {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 
-// Rotate-half RoPE of one feature pair (j, j + d/2) at integer position pos;
-// the angle pos * base^(-2j/d) is formed and reduced in double precision.
-__device__ __forceinline__ void rope_pair(double y0, double y1, int j, int d, int pos, double log2_base,
-                                          double *k0, double *k1) {
-    const double theta = exp2(-2.0 * (double)j / (double)d * log2_base);
-    double s, c;
-    sincos((double)pos * theta, &s, &c);
+// Rotate-half RoPE: theta_j = base^(-2j/d) in double precision (one table per
+// workgroup), the angle pos * theta_j formed and reduced modulo 2 pi in double
+// precision (Cody-Waite with a two-part 2 pi), its sine and cosine taken in
+// single precision on the reduced angle in [-pi, pi].
+__device__ __forceinline__ double rope_theta(int j, int d, double log2_base) {
+    return exp2(-2.0 * (double)j / (double)d * log2_base);
+}
+__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
+    const double a = (double)pos * theta;
+    const double n = rint(a * 0.15915494309189535);            // 1 / (2 pi)
+    const double r = fma(-n, 1.2246467991473532e-16, fma(-n, 6.283185307179586, a));   // 2 pi = hi + lo
+    float s, c;
+    sincosf((float)r, &s, &c);
     *k0 = y0 * c - y1 * s;
     *k1 = y1 * c + y0 * s;
+}
+
+constexpr int kUpdSubK = 64;                 // k elements per ring stage (8 chunks of 16 bytes a row)
+
+// LDS of the merged rows [KS][R][d] fp32, 16-byte aligned; the angle table follows.
+__host__ __device__ __forceinline__ size_t update_merge_bytes(int KS, int R, int d) {
+    return ((size_t)KS * R * d * 4 + 15) / 16 * 16;
+}
+constexpr int kUpdRowBytes = kUpdSubK * 2;   // 128 bytes of X or W row per stage
+
+// s_waitcnt vmcnt(n), n in [0, 63] (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14)
+__device__ __forceinline__ void wait_vm(int n) {
+    switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0x0f70); break;
+        case 1: __builtin_amdgcn_s_waitcnt(0x0f71); break;
+        case 2: __builtin_amdgcn_s_waitcnt(0x0f72); break;
+        case 3: __builtin_amdgcn_s_waitcnt(0x0f73); break;
+        case 4: __builtin_amdgcn_s_waitcnt(0x0f74); break;
+        case 5: __builtin_amdgcn_s_waitcnt(0x0f75); break;
+        case 6: __builtin_amdgcn_s_waitcnt(0x0f76); break;
+        case 7: __builtin_amdgcn_s_waitcnt(0x0f77); break;
+        case 8: __builtin_amdgcn_s_waitcnt(0x0f78); break;
+        case 9: __builtin_amdgcn_s_waitcnt(0x0f79); break;
+        case 10: __builtin_amdgcn_s_waitcnt(0x0f7a); break;
+        case 11: __builtin_amdgcn_s_waitcnt(0x0f7b); break;
+        case 12: __builtin_amdgcn_s_waitcnt(0x0f7c); break;
+        case 13: __builtin_amdgcn_s_waitcnt(0x0f7d); break;
+        case 14: __builtin_amdgcn_s_waitcnt(0x0f7e); break;
+        case 15: __builtin_amdgcn_s_waitcnt(0x0f7f); break;
+        case 16: __builtin_amdgcn_s_waitcnt(0x4f70); break;
+        case 17: __builtin_amdgcn_s_waitcnt(0x4f71); break;
+        case 18: __builtin_amdgcn_s_waitcnt(0x4f72); break;
+        case 19: __builtin_amdgcn_s_waitcnt(0x4f73); break;
+        case 20: __builtin_amdgcn_s_waitcnt(0x4f74); break;
+        case 21: __builtin_amdgcn_s_waitcnt(0x4f75); break;
+        case 22: __builtin_amdgcn_s_waitcnt(0x4f76); break;
+        case 23: __builtin_amdgcn_s_waitcnt(0x4f77); break;
+        case 24: __builtin_amdgcn_s_waitcnt(0x4f78); break;
+        case 25: __builtin_amdgcn_s_waitcnt(0x4f79); break;
+        case 26: __builtin_amdgcn_s_waitcnt(0x4f7a); break;
+        case 27: __builtin_amdgcn_s_waitcnt(0x4f7b); break;
+        case 28: __builtin_amdgcn_s_waitcnt(0x4f7c); break;
+        case 29: __builtin_amdgcn_s_waitcnt(0x4f7d); break;
+        case 30: __builtin_amdgcn_s_waitcnt(0x4f7e); break;
+        case 31: __builtin_amdgcn_s_waitcnt(0x4f7f); break;
+        case 32: __builtin_amdgcn_s_waitcnt(0x8f70); break;
+        case 33: __builtin_amdgcn_s_waitcnt(0x8f71); break;
+        case 34: __builtin_amdgcn_s_waitcnt(0x8f72); break;
+        case 35: __builtin_amdgcn_s_waitcnt(0x8f73); break;
+        case 36: __builtin_amdgcn_s_waitcnt(0x8f74); break;
+        case 37: __builtin_amdgcn_s_waitcnt(0x8f75); break;
+        case 38: __builtin_amdgcn_s_waitcnt(0x8f76); break;
+        case 39: __builtin_amdgcn_s_waitcnt(0x8f77); break;
+        case 40: __builtin_amdgcn_s_waitcnt(0x8f78); break;
+        case 41: __builtin_amdgcn_s_waitcnt(0x8f79); break;
+        case 42: __builtin_amdgcn_s_waitcnt(0x8f7a); break;
+        case 43: __builtin_amdgcn_s_waitcnt(0x8f7b); break;
+        case 44: __builtin_amdgcn_s_waitcnt(0x8f7c); break;
+        case 45: __builtin_amdgcn_s_waitcnt(0x8f7d); break;
+        case 46: __builtin_amdgcn_s_waitcnt(0x8f7e); break;
+        case 47: __builtin_amdgcn_s_waitcnt(0x8f7f); break;
+        case 48: __builtin_amdgcn_s_waitcnt(0xcf70); break;
+        case 49: __builtin_amdgcn_s_waitcnt(0xcf71); break;
+        case 50: __builtin_amdgcn_s_waitcnt(0xcf72); break;
+        case 51: __builtin_amdgcn_s_waitcnt(0xcf73); break;
+        case 52: __builtin_amdgcn_s_waitcnt(0xcf74); break;
+        case 53: __builtin_amdgcn_s_waitcnt(0xcf75); break;
+        case 54: __builtin_amdgcn_s_waitcnt(0xcf76); break;
+        case 55: __builtin_amdgcn_s_waitcnt(0xcf77); break;
+        case 56: __builtin_amdgcn_s_waitcnt(0xcf78); break;
+        case 57: __builtin_amdgcn_s_waitcnt(0xcf79); break;
+        case 58: __builtin_amdgcn_s_waitcnt(0xcf7a); break;
+        case 59: __builtin_amdgcn_s_waitcnt(0xcf7b); break;
+        case 60: __builtin_amdgcn_s_waitcnt(0xcf7c); break;
+        case 61: __builtin_amdgcn_s_waitcnt(0xcf7d); break;
+        case 62: __builtin_amdgcn_s_waitcnt(0xcf7e); break;
+        default: __builtin_amdgcn_s_waitcnt(0xCF7F); break;
+    }
 }
 
 template <int D>
 __global__ __launch_bounds__(256) void update_mfma_kernel(const UpdateArgs a) {
     constexpr int CT = D / 64;   // 16-feature column tiles per wave
+    extern __shared__ __align__(16) unsigned char smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int NH = 2 * a.Hkv;
     const int hb = blockIdx.x % NH, ks = blockIdx.x / NH;
@@ -47,37 +134,75 @@ __global__ __launch_bounds__(256) void update_mfma_kernel(const UpdateArgs a) {
     const bf16_t *x = reinterpret_cast<const bf16_t *>(a.x);
     const bf16_t *w = reinterpret_cast<const bf16_t *>(a.w) + (size_t)hb * D * a.D;
 
+    // ---- stage layout: [X rows 0..R-1 | W rows 0..D-1], 128 bytes each ----
+    const int rows = R + D;
+    const int chunks = rows * (kUpdRowBytes / 16);              // 16-byte pieces per stage
+    const int per_round = 256;                                  // one piece per thread per round
+    const int rounds = (chunks + per_round - 1) / per_round;    // load instructions per thread per stage
+    const int stage_bytes = rounds * per_round * 16;
+    const int nsub = a.kc / kUpdSubK;
+    const int S = a.stages;                                     // ring stages (all slices at once when they fit)
+    auto issue = [&](int sub, int stage) {
+        unsigned char *st = smem + stage * stage_bytes;
+        const int kb = k_lo + sub * kUpdSubK;
+        for (int rd = 0; rd < rounds; ++rd) {
+            const int inst = rd * 4 + wave;                      // 1 KB block of the stage
+            int piece = inst * 64 + lane;
+            if (piece >= chunks) piece = chunks - 1;             // padding lanes fetch a valid piece again
+            const int r = piece >> 3, slot = piece & 7;
+            const int c = slot ^ (r & 7);                        // LDS slot `slot` of row r holds chunk c
+            const bf16_t *src = r < R ? x + (size_t)r * a.D : w + (size_t)(r - R) * a.D;
+            lds_stream16(src + kb + c * 8, st + inst * 1024);
+        }
+    };
+
     f32x4_v acc[4][CT];
     #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
         #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
-    const int kq = 8 * (lane >> 4);   // this lane's 8-element slice of a 32-wide k step
-    for (int k0 = k_lo; k0 < k_lo + a.kc; k0 += 32) {
-        bf16x8_v bop[CT];
+    int issued = 0;
+    for (; issued < nsub && issued < S; ++issued) issue(issued, issued);
+    const int kq = lane >> 4;   // this lane's chunk within a 32-wide k step (8 elements)
+    for (int t = 0; t < nsub; ++t) {
+        wait_vm(rounds * (issued - t - 1));
+        __syncthreads();   // slice t is in LDS
+        const unsigned char *st = smem + (t % S) * stage_bytes;
         #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            const int col = wave * (D / 4) + ct * 16 + (lane & 15);
-            bop[ct] = *reinterpret_cast<const bf16x8_v *>(w + (size_t)col * a.D + k0 + kq);
-        }
-        #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-            if (rt < RT) {
-                const int row = rt * 16 + (lane & 15);
-                bf16x8_v aop;
-                if (row < R) aop = *reinterpret_cast<const bf16x8_v *>(x + (size_t)row * a.D + k0 + kq);
-                else aop = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
-                #pragma unroll
-                for (int ct = 0; ct < CT; ++ct)
-                    acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[ct], acc[rt][ct], 0, 0, 0);
+        for (int kst = 0; kst < kUpdSubK / 32; ++kst) {
+            const int c = kst * 4 + kq;
+            bf16x8_v bop[CT];
+            #pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const int fr = R + wave * (D / 4) + ct * 16 + (lane & 15);   // stage row of the feature
+                bop[ct] = *reinterpret_cast<const bf16x8_v *>(st + (size_t)fr * kUpdRowBytes + ((c ^ (fr & 7)) << 4));
             }
+            #pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                if (rt < RT) {
+                    const int row = rt * 16 + (lane & 15);
+                    bf16x8_v aop = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
+                    if (row < R) aop = *reinterpret_cast<const bf16x8_v *>(st + (size_t)row * kUpdRowBytes + ((c ^ (row & 7)) << 4));
+                    #pragma unroll
+                    for (int ct = 0; ct < CT; ++ct)
+                        acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[ct], acc[rt][ct], 0, 0, 0);
+                }
+            }
+        }
+        if (issued < nsub) {
+            __syncthreads();   // every wave is done with stage t % S
+            issue(issued, issued % S);
+            ++issued;
         }
     }
 
-    // ---- partial [hb][ks][R][D] with device-coherent stores ----
+    __syncthreads();   // every wave is done with the stages
+    // ---- the head block's rows y [R][D]: in LDS directly (one split) or via
+    // device-coherent partials [ks][R][D] and the last-arriving workgroup ----
     float *blk = a.part + (size_t)hb * a.part_stride;
-    float *pp = blk + (size_t)ks * R * D;
+    float *ys = reinterpret_cast<float *>(smem);
+    const bool single = a.KS == 1;
     #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
         if (rt < RT) {
@@ -87,49 +212,75 @@ __global__ __launch_bounds__(256) void update_mfma_kernel(const UpdateArgs a) {
                 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int row = rt * 16 + 4 * (lane >> 4) + i;
-                    if (row < R) store_agent(pp + (size_t)row * D + col, acc[rt][ct][i]);
+                    if (row < R) {
+                        if (single) ys[(size_t)row * D + col] = acc[rt][ct][i];
+                        else store_agent(blk + ((size_t)ks * R + row) * D + col, acc[rt][ct][i]);
+                    }
                 }
             }
         }
     }
-    wait_vm_stores();
-    __syncthreads();
-    __shared__ int s_last;
-    if (tid == 0) {
-        unsigned *cnt = a.counters + (size_t)hb * kCounterStride;
-        const int last = arrive(cnt) == (unsigned)(a.KS - 1);
-        if (last) reset_counter(cnt);
-        s_last = last;
+    if (!single) {
+        wait_vm_stores();
+        __syncthreads();
+        __shared__ int s_last;
+        if (tid == 0) {
+            unsigned *cnt = a.counters + (size_t)hb * kCounterStride;
+            const int last = arrive(cnt) == (unsigned)(a.KS - 1);
+            if (last) reset_counter(cnt);
+            s_last = last;
+        }
+        __syncthreads();
+        if (!s_last) return;
+        // ---- last workgroup of the head block: pull every split into LDS ----
+        const int nbytes = (a.KS * R * D * 4 + 15) & ~15;
+        for (int off = wave * 1024; off < nbytes; off += 4096)
+            if (off + lane * 16 < nbytes)
+                lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, smem + off);
+        __builtin_amdgcn_s_waitcnt(0x0F70);
     }
     __syncthreads();
-    if (!s_last) return;
 
-    // ---- last workgroup of the head block: sum the splits, rotate, append ----
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int nbytes = (a.KS * R * D * 4 + 15) & ~15;
-    for (int off = wave * 1024; off < nbytes; off += 4096)
-        if (off + lane * 16 < nbytes)
-            lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, smem + off);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
+    // ---- sum the splits, rotate the K half at the slot positions, append ----
+    // thread <-> (row r, four consecutive rotation pairs j..j+3); the 2 x KS
+    // 16-byte reads of an item are issued together
     const float *sp = reinterpret_cast<const float *>(smem);
+    double *theta = reinterpret_cast<double *>(smem + update_merge_bytes(a.KS, R, D));
     const bool is_k = hb < a.Hkv;
+    if (is_k && tid < D / 2) theta[tid] = rope_theta(tid, D, a.log2_base);
+    __syncthreads();
     const int h = is_k ? hb : hb - a.Hkv;
     bf16_t *dst_base = reinterpret_cast<bf16_t *>(is_k ? a.mk : a.mv) + (size_t)h * a.m_head;
-    for (int idx = tid; idx < R * (D / 2); idx += 256) {
-        const int r = idx / (D / 2), j = idx % (D / 2);
-        float y0 = 0.f, y1 = 0.f;
-        for (int s = 0; s < a.KS; ++s) {
-            y0 += sp[((size_t)s * R + r) * D + j];
-            y1 += sp[((size_t)s * R + r) * D + j + D / 2];
+    constexpr int Q = D / 8;   // groups of four pairs per row
+    for (int idx = tid; idx < R * Q; idx += 256) {
+        const int r = idx / Q, j = (idx % Q) * 4;
+        float4 y0 = make_float4(0.f, 0.f, 0.f, 0.f), y1 = y0;
+        for (int s0 = 0; s0 < a.KS; s0 += 8) {
+            float4 u[8], v[8];
+            #pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int sidx = s0 + t < a.KS ? s0 + t : a.KS - 1;
+                u[t] = *reinterpret_cast<const float4 *>(sp + ((size_t)sidx * R + r) * D + j);
+                v[t] = *reinterpret_cast<const float4 *>(sp + ((size_t)sidx * R + r) * D + j + D / 2);
+            }
+            #pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                if (s0 + t < a.KS) {
+                    y0.x += u[t].x; y0.y += u[t].y; y0.z += u[t].z; y0.w += u[t].w;
+                    y1.x += v[t].x; y1.y += v[t].y; y1.z += v[t].z; y1.w += v[t].w;
+                }
+            }
         }
         const int b = r / a.n_new, i = r - b * a.n_new;
         if (!a.fire[b]) continue;
-        double o0 = y0, o1 = y1;
-        if (is_k) rope_pair(y0, y1, j, D, a.pos[r], a.log2_base, &o0, &o1);
+        float o0[4] = {y0.x, y0.y, y0.z, y0.w}, o1[4] = {y1.x, y1.y, y1.z, y1.w};
+        if (is_k) {
+            #pragma unroll
+            for (int e = 0; e < 4; ++e) rope_rotate(o0[e], o1[e], a.pos[r], theta[j + e], &o0[e], &o1[e]);
+        }
         bf16_t *dst = dst_base + (size_t)b * a.m_seq + (size_t)(a.mlen[b] + i) * D;
-        dst[j].bits = f32_to_bf16((float)o0);
-        dst[j + D / 2].bits = f32_to_bf16((float)o1);
+        reinterpret_cast<uint2 *>(dst + j)[0] = make_uint2(pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]));
+        reinterpret_cast<uint2 *>(dst + j + D / 2)[0] = make_uint2(pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3]));
     }
 }
 
@@ -156,28 +307,53 @@ __global__ __launch_bounds__(256) void update_f32_kernel(const UpdateArgs a) {
     if (!a.fire[b]) return;
     const bool is_k = hb < a.Hkv;
     const int h = is_k ? hb : hb - a.Hkv;
-    double o0 = y0, o1 = y1;
-    if (is_k) rope_pair(y0, y1, j, d, a.pos[r], a.log2_base, &o0, &o1);
+    float o0 = y0, o1 = y1;
+    if (is_k) rope_rotate(y0, y1, a.pos[r], rope_theta(j, d, a.log2_base), &o0, &o1);
     float *dst = reinterpret_cast<float *>(is_k ? a.mk : a.mv) + (size_t)b * a.m_seq + (size_t)h * a.m_head +
                  (size_t)(a.mlen[b] + i) * d;
-    dst[j] = (float)o0;
-    dst[j + half] = (float)o1;
+    dst[j] = o0;
+    dst[j + half] = o1;
 }
 
 // ------------------------------------------------------------------ host ----
 
+// Bytes of LDS a bf16 update workgroup needs: the two-stage ring, or the
+// merge of all KS partials, whichever is larger.
+static size_t update_stage_bytes(int R, int d) {
+    const size_t pieces = (size_t)(R + d) * (kUpdRowBytes / 16);
+    return (pieces + 255) / 256 * 256 * 16;
+}
+static int update_rounds(int R, int d) { return (int)(update_stage_bytes(R, d) / 4096); }
+// Ring stages: every k slice of the workgroup at once when LDS and the vmcnt
+// range allow it, else as many as fit (at least two).
+static int update_stages(int R, int d, int KS, int D) {
+    const int nsub = D / KS / kUpdSubK;
+    int s = nsub;
+    const int by_lds = (int)((kUpdateMaxLds - (size_t)d / 2 * 8 - 16) / update_stage_bytes(R, d));
+    const int by_cnt = 62 / update_rounds(R, d) + 1;
+    if (s > by_lds) s = by_lds;
+    if (s > by_cnt) s = by_cnt;
+    if (s < 2) s = 2;
+    return s;
+}
+static size_t update_lds_bytes(int R, int d, int KS, int stages) {
+    const size_t ring = (size_t)stages * update_stage_bytes(R, d);
+    const size_t merge = update_merge_bytes(KS, R, d);
+    return (ring > merge ? ring : merge) + (size_t)d / 2 * 8 + 16;   // + the RoPE angle table
+}
+
 UpdatePlan plan_update(int R, int D, int Hkv, int d) {
     UpdatePlan p;
     const int NH = 2 * Hkv;
-    const int ksteps = D / 32;
-    int ks = (256 + NH - 1) / NH;                               // aim at ~256 workgroups
-    const int lds_cap = (int)(kUpdateMergeBytes / ((size_t)R * d * 4));
-    if (ks > lds_cap) ks = lds_cap;
-    if (ks > ksteps) ks = ksteps;
+    const int nk = D / kUpdSubK;                                // 64-wide k chunks
+    int ks = (kUpdateTargetWGs + NH - 1) / NH;
+    while (ks > 1 && update_lds_bytes(R, d, ks, 2) > kUpdateMaxLds) --ks;
+    if (ks > nk) ks = nk;
     if (ks < 1) ks = 1;
-    while (ksteps % ks) --ks;                                   // equal k chunks of whole steps
+    while (nk % ks) --ks;                                       // equal k slices of whole chunks
     p.KS = ks;
     p.kc = D / ks;
+    p.stages = update_stages(R, d, ks, D);
     return p;
 }
 
@@ -191,7 +367,7 @@ size_t update_part_stride(int R, int d, int KS) { return ((size_t)KS * R * d + 6
 hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st) {
     if (dtype == MAD_BF16) {
         dim3 grid((unsigned)(2 * a.Hkv * a.KS)), block(256);
-        const size_t lds = (size_t)a.KS * a.R * a.d * 4 + 16;
+        const size_t lds = update_lds_bytes(a.R, a.d, a.KS, a.stages);
         if (a.d == 64) hipLaunchKernelGGL(update_mfma_kernel<64>, grid, block, lds, st, a);
         else hipLaunchKernelGGL(update_mfma_kernel<128>, grid, block, lds, st, a);
     } else {
