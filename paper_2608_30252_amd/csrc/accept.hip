@@ -59,9 +59,35 @@ __global__ __launch_bounds__(256) void accept_kernel(const AcceptArgs a) {
     const T *x = reinterpret_cast<const T *>(a.logits) + (size_t)row * a.V;
 
     uint64_t best = 0;   // below every real key (index 0xffffffff is never used)
-    for (int i = v0 + tid; i < v1; i += 256) {
-        const uint64_t k = argmax_key(Elem<T>::load1(x + i), i);
-        best = k > best ? k : best;
+    constexpr int VEC = Elem<T>::VEC;                   // elements per 16-byte load
+    constexpr int NV = kAcceptChunk / (256 * VEC);      // 16-byte loads per thread per chunk
+    if (a.vec16) {
+        // rows start on 16-byte boundaries and V is a multiple of VEC: every
+        // load of the chunk is issued before any is used
+        uint4 v[NV];
+        #pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int e = v0 + (tid + 256 * k) * VEC;
+            v[k] = e < v1 ? *reinterpret_cast<const uint4 *>(x + e) : make_uint4(0u, 0u, 0u, 0u);
+        }
+        #pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int e = v0 + (tid + 256 * k) * VEC;
+            if (e < v1) {
+                float f[VEC];
+                unpack16(v[k], f, T());
+                #pragma unroll
+                for (int q = 0; q < VEC; ++q) {
+                    const uint64_t key = argmax_key(f[q], e + q);
+                    best = key > best ? key : best;
+                }
+            }
+        }
+    } else {
+        for (int i = v0 + tid; i < v1; i += 256) {
+            const uint64_t k = argmax_key(Elem<T>::load1(x + i), i);
+            best = k > best ? k : best;
+        }
     }
     best = wave_max_u64(best);
     __shared__ uint64_t s_w[4];

@@ -302,6 +302,8 @@ int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, i
     a.T = T;
     a.V = V;
     a.n_chunks = (V + mad::kAcceptChunk - 1) / mad::kAcceptChunk;
+    const size_t esz = dtype == MAD_BF16 ? 2 : 4;
+    a.vec16 = aligned16(logits) && ((size_t)V * esz) % 16 == 0;
     return hip_status(mad::launch_accept(a, dtype, (hipStream_t)stream), "accept launch");
 }
 

@@ -131,6 +131,7 @@ struct AcceptArgs {
     uint64_t *row_best;        // [rows] row argmax keys
     unsigned *counters;        // lines 0..rows-1: per row; line rows: all rows
     int B, T, V, n_chunks;
+    int vec16;                 // rows 16-byte aligned and V a multiple of 16 / element size
 };
 
 size_t accept_ws_bytes(int B, int T, int V);
