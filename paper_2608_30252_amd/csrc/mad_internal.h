@@ -94,7 +94,7 @@ hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st);
 
 // ---------------------------------------------------------------- verify ----
 #ifndef MAD_VERIFY_TARGET_WGS
-#define MAD_VERIFY_TARGET_WGS 512
+#define MAD_VERIFY_TARGET_WGS 256
 #endif
 constexpr int kVerifyTargetWGs = MAD_VERIFY_TARGET_WGS;
 constexpr int kVerifyMaxSplits = 128;

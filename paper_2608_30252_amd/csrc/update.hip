@@ -51,76 +51,6 @@ __host__ __device__ __forceinline__ size_t update_merge_bytes(int KS, int R, int
 }
 constexpr int kUpdRowBytes = kUpdSubK * 2;   // 128 bytes of X or W row per stage
 
-// s_waitcnt vmcnt(n), n in [0, 63] (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14)
-__device__ __forceinline__ void wait_vm(int n) {
-    switch (n) {
-        case 0: __builtin_amdgcn_s_waitcnt(0x0f70); break;
-        case 1: __builtin_amdgcn_s_waitcnt(0x0f71); break;
-        case 2: __builtin_amdgcn_s_waitcnt(0x0f72); break;
-        case 3: __builtin_amdgcn_s_waitcnt(0x0f73); break;
-        case 4: __builtin_amdgcn_s_waitcnt(0x0f74); break;
-        case 5: __builtin_amdgcn_s_waitcnt(0x0f75); break;
-        case 6: __builtin_amdgcn_s_waitcnt(0x0f76); break;
-        case 7: __builtin_amdgcn_s_waitcnt(0x0f77); break;
-        case 8: __builtin_amdgcn_s_waitcnt(0x0f78); break;
-        case 9: __builtin_amdgcn_s_waitcnt(0x0f79); break;
-        case 10: __builtin_amdgcn_s_waitcnt(0x0f7a); break;
-        case 11: __builtin_amdgcn_s_waitcnt(0x0f7b); break;
-        case 12: __builtin_amdgcn_s_waitcnt(0x0f7c); break;
-        case 13: __builtin_amdgcn_s_waitcnt(0x0f7d); break;
-        case 14: __builtin_amdgcn_s_waitcnt(0x0f7e); break;
-        case 15: __builtin_amdgcn_s_waitcnt(0x0f7f); break;
-        case 16: __builtin_amdgcn_s_waitcnt(0x4f70); break;
-        case 17: __builtin_amdgcn_s_waitcnt(0x4f71); break;
-        case 18: __builtin_amdgcn_s_waitcnt(0x4f72); break;
-        case 19: __builtin_amdgcn_s_waitcnt(0x4f73); break;
-        case 20: __builtin_amdgcn_s_waitcnt(0x4f74); break;
-        case 21: __builtin_amdgcn_s_waitcnt(0x4f75); break;
-        case 22: __builtin_amdgcn_s_waitcnt(0x4f76); break;
-        case 23: __builtin_amdgcn_s_waitcnt(0x4f77); break;
-        case 24: __builtin_amdgcn_s_waitcnt(0x4f78); break;
-        case 25: __builtin_amdgcn_s_waitcnt(0x4f79); break;
-        case 26: __builtin_amdgcn_s_waitcnt(0x4f7a); break;
-        case 27: __builtin_amdgcn_s_waitcnt(0x4f7b); break;
-        case 28: __builtin_amdgcn_s_waitcnt(0x4f7c); break;
-        case 29: __builtin_amdgcn_s_waitcnt(0x4f7d); break;
-        case 30: __builtin_amdgcn_s_waitcnt(0x4f7e); break;
-        case 31: __builtin_amdgcn_s_waitcnt(0x4f7f); break;
-        case 32: __builtin_amdgcn_s_waitcnt(0x8f70); break;
-        case 33: __builtin_amdgcn_s_waitcnt(0x8f71); break;
-        case 34: __builtin_amdgcn_s_waitcnt(0x8f72); break;
-        case 35: __builtin_amdgcn_s_waitcnt(0x8f73); break;
-        case 36: __builtin_amdgcn_s_waitcnt(0x8f74); break;
-        case 37: __builtin_amdgcn_s_waitcnt(0x8f75); break;
-        case 38: __builtin_amdgcn_s_waitcnt(0x8f76); break;
-        case 39: __builtin_amdgcn_s_waitcnt(0x8f77); break;
-        case 40: __builtin_amdgcn_s_waitcnt(0x8f78); break;
-        case 41: __builtin_amdgcn_s_waitcnt(0x8f79); break;
-        case 42: __builtin_amdgcn_s_waitcnt(0x8f7a); break;
-        case 43: __builtin_amdgcn_s_waitcnt(0x8f7b); break;
-        case 44: __builtin_amdgcn_s_waitcnt(0x8f7c); break;
-        case 45: __builtin_amdgcn_s_waitcnt(0x8f7d); break;
-        case 46: __builtin_amdgcn_s_waitcnt(0x8f7e); break;
-        case 47: __builtin_amdgcn_s_waitcnt(0x8f7f); break;
-        case 48: __builtin_amdgcn_s_waitcnt(0xcf70); break;
-        case 49: __builtin_amdgcn_s_waitcnt(0xcf71); break;
-        case 50: __builtin_amdgcn_s_waitcnt(0xcf72); break;
-        case 51: __builtin_amdgcn_s_waitcnt(0xcf73); break;
-        case 52: __builtin_amdgcn_s_waitcnt(0xcf74); break;
-        case 53: __builtin_amdgcn_s_waitcnt(0xcf75); break;
-        case 54: __builtin_amdgcn_s_waitcnt(0xcf76); break;
-        case 55: __builtin_amdgcn_s_waitcnt(0xcf77); break;
-        case 56: __builtin_amdgcn_s_waitcnt(0xcf78); break;
-        case 57: __builtin_amdgcn_s_waitcnt(0xcf79); break;
-        case 58: __builtin_amdgcn_s_waitcnt(0xcf7a); break;
-        case 59: __builtin_amdgcn_s_waitcnt(0xcf7b); break;
-        case 60: __builtin_amdgcn_s_waitcnt(0xcf7c); break;
-        case 61: __builtin_amdgcn_s_waitcnt(0xcf7d); break;
-        case 62: __builtin_amdgcn_s_waitcnt(0xcf7e); break;
-        default: __builtin_amdgcn_s_waitcnt(0xCF7F); break;
-    }
-}
-
 template <int D>
 __global__ __launch_bounds__(256) void update_mfma_kernel(const UpdateArgs a) {
     constexpr int CT = D / 64;   // 16-feature column tiles per wave

@@ -4,7 +4,7 @@
 // sees rows 0 .. len-T+t.
 //
 // Both products of attention run on the matrix cores
-// (v_mfma_f32_16x16x32_bf16, fp32 accumulation), fed straight from HBM:
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation):
 //   * the query tile of one (sequence, KV head) unit is the T*G rows
 //     (t, g) -> row t*G + g, padded to 16-row blocks;
 //   * S^T = K Q^T takes K rows as the A operand.  Key rows are assigned to the
@@ -15,9 +15,12 @@
 //     probabilities from the lane's own scores (rounded to bf16);
 //   * online softmax per query row: the row's 8 scores sit in one lane, the
 //     row max needs two cross-lane exchanges.
-// Each wave of a workgroup streams its own 32-key slabs; the four waves' (max,
-// sum, o) are merged in LDS into one split partial.  A second small kernel
-// merges the splits of every query row with the log-sum-exp rule.
+// Each wave of a workgroup streams its own 32-key slabs (K rows and the V^T
+// columns) from HBM straight into a private LDS ring (global_load_lds_dwordx4,
+// 16-byte chunks XOR-swizzled so the operand reads are conflict-free) and waits
+// only on its own loads: no workgroup barrier inside the key loop.  The four
+// waves' (max, sum, o) are merged in LDS into one split partial; a second small
+// kernel merges the splits of every query row with the log-sum-exp rule.
 #include "mad_device.h"
 #include "mad_internal.h"
 
@@ -39,14 +42,33 @@ __device__ __forceinline__ float sum_over_row_lanes(float v) {
     return v;
 }
 
+// Geometry of one wave's 32-key slab in LDS: [K: 32 rows of D bf16][V^T: D features x 32 keys].
+template <int D> struct VerifySlab {
+    static constexpr int KROW = D * 2;                  // bytes per K row
+    static constexpr int KCH = KROW / 16;               // 16-byte chunks per K row (8 or 16)
+    static constexpr int KBYTES = 32 * KROW;
+    static constexpr int BYTES = KBYTES + D * 64;       // + V^T: 64 bytes (32 keys) per feature
+    static constexpr int KI = KBYTES / 1024;            // load instructions per lane: K
+    static constexpr int VI = D * 64 / 1024;            //                             V^T
+    static constexpr int NI = KI + VI;
+    static constexpr int STAGES = 65536 / 2 / BYTES;    // 2 (d 128) or 4 (d 64): 32 KB per wave
+    static constexpr int WAVE_BYTES = STAGES * BYTES;
+};
+// K chunk swizzle: the 16 rows an A-operand read touches differ in key bits
+// 0, 1, 3 and 4 (key = 8 q + 4 blk + r); those bits pick the slot.
+template <int KCH> __device__ __forceinline__ int kswz(int j) {
+    const int v = (j & 3) | (((j >> 3) & 3) << 2);
+    return v & (KCH - 1);
+}
+__device__ __forceinline__ int vswz(int f) { return (f >> 1) & 3; }
+
 template <int D, int NB>
 __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
+    using SL = VerifySlab<D>;
     constexpr int KST = D / 32;   // 32-feature k steps of the QK product
     constexpr int DB = D / 16;    // 16-feature output blocks of the PV product
     constexpr int RP = NB * 16;   // padded query rows
     extern __shared__ __align__(16) unsigned char smem[];
-    float *sML = reinterpret_cast<float *>(smem);          // [4 waves][RP][2]
-    float *sO = sML + 4 * RP * 2;                          // [4 waves][RP][D]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.x % a.units, s = blockIdx.x / a.units;
@@ -58,8 +80,34 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
     const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
     const int lr = lane & 15, lg = lane >> 4;   // row within a 16-block, lane group
+    unsigned char *ring = smem + wave * SL::WAVE_BYTES;
+
+    // ---- this wave's slabs: keys kb = k0 + 32 wave + 128 i ----
+    const int nsl = (k1 > k0 + wave * 32) ? (k1 - k0 - wave * 32 + 127) / 128 : 0;
+    auto issue = [&](int i, int stage) {
+        const int kb = k0 + wave * 32 + i * 128;
+        unsigned char *st = ring + stage * SL::BYTES;
+        #pragma unroll
+        for (int q = 0; q < SL::KI; ++q) {
+            const int ci = q * 64 + lane;
+            const int j = ci / SL::KCH, sl = ci % SL::KCH;
+            const int key = min(kb + j, len - 1);   // rows past len load a valid row (masked below)
+            lds_stream16(K + (size_t)key * D + 8 * (sl ^ kswz<SL::KCH>(j)), st + q * 1024);
+        }
+        #pragma unroll
+        for (int q = 0; q < SL::VI; ++q) {
+            const int ci = q * 64 + lane;
+            const int f = ci >> 2, sl = ci & 3;
+            int kg = kb + 8 * (sl ^ vswz(f));
+            if (kg >= len) kg = (len - 1) & ~7;     // past len: any valid chunk (zeroed below)
+            lds_stream16(VT + (size_t)f * cap + kg, st + SL::KBYTES + q * 1024);
+        }
+    };
+    int issued = 0;
+    for (; issued < nsl && issued < SL::STAGES; ++issued) issue(issued, issued);
 
     // ---- query fragments (B operand of S^T = K Q^T) and causal limits ----
+    // (issued after the first slabs, so waiting for them also covers those)
     bf16x8_v qf[NB][KST];
     int lim[NB];
     #pragma unroll
@@ -88,38 +136,43 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         for (int db = 0; db < DB; ++db) o[db][rb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
     }
 
-    for (int kb = k0 + wave * 32; kb < k1; kb += 128) {
+    for (int i = 0; i < nsl; ++i) {
+        const int kb = k0 + wave * 32 + i * 128;
+        wait_vm(SL::NI * (issued - i - 1));   // this slab has landed (this wave's own loads)
+        const unsigned char *st = ring + (i % SL::STAGES) * SL::BYTES;
         // K rows for the two 16-key blocks: A row m of block blk holds key
         // kb + 8*(m/4) + 4*blk + m%4, so accumulator element i of lane group lg
         // is key kb + 8*lg + 4*blk + i.
         bf16x8_v kf[2][KST];
         #pragma unroll
         for (int blk = 0; blk < 2; ++blk) {
-            int key = kb + 8 * (lr >> 2) + 4 * blk + (lr & 3);
-            key = min(key, len - 1);
-            const bf16_t *krow = K + (size_t)key * D + 8 * lg;
+            const int j = 8 * (lr >> 2) + 4 * blk + (lr & 3);
+            const unsigned char *krow = st + j * SL::KROW;
             #pragma unroll
-            for (int ks = 0; ks < KST; ++ks) kf[blk][ks] = *reinterpret_cast<const bf16x8_v *>(krow + ks * 32);
+            for (int ks = 0; ks < KST; ++ks)
+                kf[blk][ks] = *reinterpret_cast<const bf16x8_v *>(krow + 16 * ((ks * 4 + lg) ^ kswz<SL::KCH>(j)));
         }
-        // V^T: feature db*16 + lr, keys kb + 8*lg .. +7 (cap is a multiple of 8)
+        // V^T: feature db*16 + lr, keys kb + 8*lg .. +7
         const int kg = kb + 8 * lg;
         bf16x8_v vf[DB];
         #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            if (kg < len) {
-                u32x4_v w = *reinterpret_cast<const u32x4_v *>(VT + (size_t)(db * 16 + lr) * cap + kg);
-                if (kg + 8 > len) {   // zero the values of keys past len (they may be stale)
-                    #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int kk = kg + 2 * e;
-                        if (kk >= len) w[e] = 0u;
-                        else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
-                    }
+            const int f = db * 16 + lr;
+            u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + SL::KBYTES + f * 64 + 16 * (lg ^ vswz(f)));
+            if (kg + 8 > len) {   // zero the values of keys past len (they may be stale)
+                #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int kk = kg + 2 * e;
+                    if (kk >= len) w[e] = 0u;
+                    else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
                 }
-                vf[db] = __builtin_bit_cast(bf16x8_v, w);
-            } else {
-                vf[db] = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
             }
+            vf[db] = __builtin_bit_cast(bf16x8_v, w);
+        }
+        if (issued < nsl) {   // the stage of slab i is read into registers: refill it
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): those reads are complete
+            issue(issued, issued % SL::STAGES);
+            ++issued;
         }
         // S^T
         f32x4_v sacc[2][NB];
@@ -147,13 +200,13 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
             mt = max_over_row_lanes(mt);
             const float mn = fmaxf(m_run[rb], mt);
             const float ms = (mn == -INFINITY) ? 0.f : mn;
-            const float alpha = exp2f(m_run[rb] - ms);
+            const float alpha = __builtin_amdgcn_exp2f(m_run[rb] - ms);
             m_run[rb] = mn;
             float ps = 0.f;
             uint32_t pk[4];
             #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float p0 = exp2f(sv[2 * e] - ms), p1 = exp2f(sv[2 * e + 1] - ms);
+                const float p0 = __builtin_amdgcn_exp2f(sv[2 * e] - ms), p1 = __builtin_amdgcn_exp2f(sv[2 * e + 1] - ms);
                 ps += p0 + p1;
                 pk[e] = pack_bf16x2(p0, p1);
             }
@@ -167,7 +220,10 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         }
     }
 
-    // ---- merge the four waves in LDS ----
+    // ---- merge the four waves in LDS (the rings are free once all waves are here) ----
+    __syncthreads();
+    float *sML = reinterpret_cast<float *>(smem);          // [4 waves][RP][2]
+    float *sO = sML + 4 * RP * 2;                          // [4 waves][RP][D]
     #pragma unroll
     for (int rb = 0; rb < NB; ++rb) {
         const float lt = sum_over_row_lanes(l_run[rb]);
@@ -192,7 +248,7 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         float acc = 0.f, L = 0.f;
         #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const float wt = exp2f(sML[(w * RP + r) * 2] - Ms);
+            const float wt = __builtin_amdgcn_exp2f(sML[(w * RP + r) * 2] - Ms);
             acc = fmaf(wt, sO[((size_t)w * RP + r) * D + col], acc);
             L = fmaf(wt, sML[(w * RP + r) * 2 + 1], L);
         }
@@ -204,31 +260,62 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     }
 }
 
-// One workgroup per (unit, query row): log-sum-exp merge of the splits.
+// One workgroup (D threads) per (unit, query row): log-sum-exp merge of the
+// splits.  Threads first turn the splits' (max, sum) into weights in parallel,
+// then every thread sums its feature over the splits in batches of reads.
 template <int D>
 __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     const int R = a.T * a.G;
     const int u = blockIdx.x / R, r = blockIdx.x - u * R;
     const int b = u / a.Hkv, c = u - b * a.Hkv;
     const int t = r / a.G, g = r - t * a.G;
-    const int col = threadIdx.x;
-    const float *po = a.part + (size_t)u * a.n_splits * a.part_rows * D + (size_t)r * D + col;
-    const float *pml = a.part_ml + (size_t)u * a.n_splits * a.part_rows * 2 + 2 * r;
-    const size_t sstride_o = (size_t)a.part_rows * D, sstride_ml = (size_t)a.part_rows * 2;
-    float M = -INFINITY;
-    for (int s = 0; s < a.n_splits; ++s) M = fmaxf(M, pml[s * sstride_ml]);
-    float acc = 0.f, L = 0.f;
-    if (M != -INFINITY) {
-        #pragma unroll 8
-        for (int s = 0; s < a.n_splits; ++s) {
-            const float wt = exp2f(pml[s * sstride_ml] - M);
-            L = fmaf(wt, pml[s * sstride_ml + 1], L);
-            acc = fmaf(wt, po[s * sstride_o], acc);
-        }
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int NW = D / 64;
+    const int ns = a.n_splits;
+    const float *po = a.part + (size_t)u * ns * a.part_rows * D + (size_t)r * D + tid;
+    const float *pml = a.part_ml + (size_t)u * ns * a.part_rows * 2 + 2 * r;
+    const size_t so = (size_t)a.part_rows * D, sml = (size_t)a.part_rows * 2;
+    __shared__ float s_w[kVerifyMaxSplits];
+    __shared__ float s_red[2][NW];
+
+    // split weights: thread i handles splits i and i + D (ns <= kVerifyMaxSplits <= 2 D)
+    float m0 = -INFINITY, m1 = -INFINITY, l0 = 0.f, l1 = 0.f;
+    if (tid < ns) { m0 = pml[tid * sml]; l0 = pml[tid * sml + 1]; }
+    if (tid + D < ns) { m1 = pml[(tid + D) * sml]; l1 = pml[(tid + D) * sml + 1]; }
+    float m = fmaxf(m0, m1);
+    #pragma unroll
+    for (int x = 1; x < 64; x <<= 1) m = fmaxf(m, __shfl_xor(m, x, 64));
+    if (lane == 0) s_red[0][wave] = m;
+    __syncthreads();
+    float M = s_red[0][0];
+    #pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, s_red[0][w]);
+    const float w0 = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
+    const float w1 = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+    float lsum = w0 * l0 + w1 * l1;
+    #pragma unroll
+    for (int x = 1; x < 64; x <<= 1) lsum += __shfl_xor(lsum, x, 64);
+    if (lane == 0) s_red[1][wave] = lsum;
+    __syncthreads();
+    float L = 0.f;
+    #pragma unroll
+    for (int w = 0; w < NW; ++w) L += s_red[1][w];
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    if (tid < ns) s_w[tid] = w0 * inv;
+    if (tid + D < ns) s_w[tid + D] = w1 * inv;
+    __syncthreads();
+
+    float acc = 0.f;
+    for (int s0 = 0; s0 < ns; s0 += 8) {
+        float v[8];
+        #pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = s0 + e < ns ? po[(s0 + e) * so] : 0.f;
+        #pragma unroll
+        for (int e = 0; e < 8; ++e) if (s0 + e < ns) acc = fmaf(s_w[s0 + e], v[e], acc);
     }
     const size_t head = ((size_t)b * a.T + t) * a.Hq + (size_t)c * a.G + g;
-    reinterpret_cast<bf16_t *>(a.out)[head * D + col].bits = f32_to_bf16(L > 0.f ? acc / L : 0.f);
-    if (a.lse && col == 0) a.lse[head] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+    reinterpret_cast<bf16_t *>(a.out)[head * D + tid].bits = f32_to_bf16(acc);
+    if (a.lse && tid == 0) a.lse[head] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 
 // ------------------------------------------------------------------ host ----
@@ -273,7 +360,9 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
     constexpr int RP = NB * 16;
-    const size_t lds = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
+    const size_t merge = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
+    const size_t rings = (size_t)4 * VerifySlab<D>::WAVE_BYTES;
+    const size_t lds = merge > rings ? merge : rings;
     hipLaunchKernelGGL((verify_split_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256), lds, st, a);
     return hipGetLastError();
 }
