@@ -15,12 +15,13 @@
 //     probabilities from the lane's own scores (rounded to bf16);
 //   * online softmax per query row: the row's 8 scores sit in one lane, the
 //     row max needs two cross-lane exchanges.
-// Each wave of a workgroup streams its own 32-key slabs (K rows and the V^T
-// columns) from HBM straight into a private LDS ring (global_load_lds_dwordx4,
-// 16-byte chunks XOR-swizzled so the operand reads are conflict-free) and waits
-// only on its own loads: no workgroup barrier inside the key loop.  The four
-// waves' (max, sum, o) are merged in LDS into one split partial; a second small
-// kernel merges the splits of every query row with the log-sum-exp rule.
+// Each wave of a workgroup streams its own 32-key slabs (K rows and V^T
+// columns, 16 bytes a lane) straight into registers, DEPTH slabs deep:
+// the loads of slab i + DEPTH - 1 are issued before slab i is used, so about
+// (DEPTH - 1) x 16 KB per wave are in flight -- the register file is a far
+// larger buffer than LDS.  The four waves' (max, sum, o) are merged in LDS into
+// one split partial; a second small kernel merges the splits of every query row
+// with the log-sum-exp rule.
 #include "mad_device.h"
 #include "mad_internal.h"
 
@@ -42,32 +43,15 @@ __device__ __forceinline__ float sum_over_row_lanes(float v) {
     return v;
 }
 
-// Geometry of one wave's 32-key slab in LDS: [K: 32 rows of D bf16][V^T: D features x 32 keys].
-template <int D> struct VerifySlab {
-    static constexpr int KROW = D * 2;                  // bytes per K row
-    static constexpr int KCH = KROW / 16;               // 16-byte chunks per K row (8 or 16)
-    static constexpr int KBYTES = 32 * KROW;
-    static constexpr int BYTES = KBYTES + D * 64;       // + V^T: 64 bytes (32 keys) per feature
-    static constexpr int KI = KBYTES / 1024;            // load instructions per lane: K
-    static constexpr int VI = D * 64 / 1024;            //                             V^T
-    static constexpr int NI = KI + VI;
-    static constexpr int STAGES = 65536 / 2 / BYTES;    // 2 (d 128) or 4 (d 64): 32 KB per wave
-    static constexpr int WAVE_BYTES = STAGES * BYTES;
-};
-// K chunk swizzle: the 16 rows an A-operand read touches differ in key bits
-// 0, 1, 3 and 4 (key = 8 q + 4 blk + r); those bits pick the slot.
-template <int KCH> __device__ __forceinline__ int kswz(int j) {
-    const int v = (j & 3) | (((j >> 3) & 3) << 2);
-    return v & (KCH - 1);
-}
-__device__ __forceinline__ int vswz(int f) { return (f >> 1) & 3; }
+// slabs per wave in flight or in use: three where the registers allow it
+template <int D, int NB> constexpr int verify_depth() { return D == 128 ? (NB >= 4 ? 1 : NB == 3 ? 2 : 3) : 3; }
 
 template <int D, int NB>
 __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
-    using SL = VerifySlab<D>;
     constexpr int KST = D / 32;   // 32-feature k steps of the QK product
     constexpr int DB = D / 16;    // 16-feature output blocks of the PV product
     constexpr int RP = NB * 16;   // padded query rows
+    constexpr int DEPTH = verify_depth<D, NB>();
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -80,34 +64,8 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
     const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
     const int lr = lane & 15, lg = lane >> 4;   // row within a 16-block, lane group
-    unsigned char *ring = smem + wave * SL::WAVE_BYTES;
-
-    // ---- this wave's slabs: keys kb = k0 + 32 wave + 128 i ----
-    const int nsl = (k1 > k0 + wave * 32) ? (k1 - k0 - wave * 32 + 127) / 128 : 0;
-    auto issue = [&](int i, int stage) {
-        const int kb = k0 + wave * 32 + i * 128;
-        unsigned char *st = ring + stage * SL::BYTES;
-        #pragma unroll
-        for (int q = 0; q < SL::KI; ++q) {
-            const int ci = q * 64 + lane;
-            const int j = ci / SL::KCH, sl = ci % SL::KCH;
-            const int key = min(kb + j, len - 1);   // rows past len load a valid row (masked below)
-            lds_stream16(K + (size_t)key * D + 8 * (sl ^ kswz<SL::KCH>(j)), st + q * 1024);
-        }
-        #pragma unroll
-        for (int q = 0; q < SL::VI; ++q) {
-            const int ci = q * 64 + lane;
-            const int f = ci >> 2, sl = ci & 3;
-            int kg = kb + 8 * (sl ^ vswz(f));
-            if (kg >= len) kg = (len - 1) & ~7;     // past len: any valid chunk (zeroed below)
-            lds_stream16(VT + (size_t)f * cap + kg, st + SL::KBYTES + q * 1024);
-        }
-    };
-    int issued = 0;
-    for (; issued < nsl && issued < SL::STAGES; ++issued) issue(issued, issued);
 
     // ---- query fragments (B operand of S^T = K Q^T) and causal limits ----
-    // (issued after the first slabs, so waiting for them also covers those)
     bf16x8_v qf[NB][KST];
     int lim[NB];
     #pragma unroll
@@ -126,6 +84,30 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         }
     }
 
+    // ---- this wave's slabs: keys kb = k0 + 32 wave + 128 i ----
+    const int nsl = (k1 > k0 + wave * 32) ? (k1 - k0 - wave * 32 + 127) / 128 : 0;
+    // K rows of the two 16-key blocks: A row m of block blk holds key
+    // kb + 8*(m/4) + 4*blk + m%4, so accumulator element i of lane group lg is
+    // key kb + 8*lg + 4*blk + i.  V^T: feature db*16 + lr, keys kb + 8*lg .. +7.
+    bf16x8_v kf[DEPTH][2][KST];
+    u32x4_v vw[DEPTH][DB];
+    auto load = [&](int i, int buf_k, int buf_v) {
+        (void)buf_v;
+        const int kb = k0 + wave * 32 + i * 128;
+        #pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+            const int key = min(kb + 8 * (lr >> 2) + 4 * blk + (lr & 3), len - 1);   // past len: a valid row, masked
+            const bf16_t *krow = K + (size_t)key * D + 8 * lg;
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) kf[buf_k][blk][ks] = *reinterpret_cast<const bf16x8_v *>(krow + ks * 32);
+        }
+        int kg = kb + 8 * lg;
+        if (kg >= len) kg = (len - 1) & ~7;   // past len: any valid chunk (zeroed when used)
+        #pragma unroll
+        for (int db = 0; db < DB; ++db)
+            vw[buf_v][db] = *reinterpret_cast<const u32x4_v *>(VT + (size_t)(db * 16 + lr) * cap + kg);
+    };
+
     f32x4_v o[DB][NB];
     float m_run[NB], l_run[NB];
     #pragma unroll
@@ -136,29 +118,13 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         for (int db = 0; db < DB; ++db) o[db][rb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
     }
 
-    for (int i = 0; i < nsl; ++i) {
+    auto compute = [&](int i, int buf) {
         const int kb = k0 + wave * 32 + i * 128;
-        wait_vm(SL::NI * (issued - i - 1));   // this slab has landed (this wave's own loads)
-        const unsigned char *st = ring + (i % SL::STAGES) * SL::BYTES;
-        // K rows for the two 16-key blocks: A row m of block blk holds key
-        // kb + 8*(m/4) + 4*blk + m%4, so accumulator element i of lane group lg
-        // is key kb + 8*lg + 4*blk + i.
-        bf16x8_v kf[2][KST];
-        #pragma unroll
-        for (int blk = 0; blk < 2; ++blk) {
-            const int j = 8 * (lr >> 2) + 4 * blk + (lr & 3);
-            const unsigned char *krow = st + j * SL::KROW;
-            #pragma unroll
-            for (int ks = 0; ks < KST; ++ks)
-                kf[blk][ks] = *reinterpret_cast<const bf16x8_v *>(krow + 16 * ((ks * 4 + lg) ^ kswz<SL::KCH>(j)));
-        }
-        // V^T: feature db*16 + lr, keys kb + 8*lg .. +7
         const int kg = kb + 8 * lg;
         bf16x8_v vf[DB];
         #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            const int f = db * 16 + lr;
-            u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + SL::KBYTES + f * 64 + 16 * (lg ^ vswz(f)));
+            u32x4_v w = vw[buf][db];
             if (kg + 8 > len) {   // zero the values of keys past len (they may be stale)
                 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -169,11 +135,6 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
             }
             vf[db] = __builtin_bit_cast(bf16x8_v, w);
         }
-        if (issued < nsl) {   // the stage of slab i is read into registers: refill it
-            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): those reads are complete
-            issue(issued, issued % SL::STAGES);
-            ++issued;
-        }
         // S^T
         f32x4_v sacc[2][NB];
         #pragma unroll
@@ -183,7 +144,7 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
                 sacc[blk][rb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
                 #pragma unroll
                 for (int ks = 0; ks < KST; ++ks)
-                    sacc[blk][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[blk][ks], qf[rb][ks], sacc[blk][rb], 0, 0, 0);
+                    sacc[blk][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[buf][blk][ks], qf[rb][ks], sacc[blk][rb], 0, 0, 0);
             }
         // online softmax and PV, per 16-row block
         #pragma unroll
@@ -218,10 +179,22 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
                 o[db][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pf, o[db][rb], 0, 0, 0);
             }
         }
+    };
+
+    // software pipeline: slab i lives in buffer i % DEPTH
+    #pragma unroll
+    for (int d = 0; d < DEPTH - 1; ++d)
+        if (d < nsl) load(d, d, d);
+    for (int i0 = 0; i0 < nsl; i0 += DEPTH) {
+        #pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int i = i0 + d;
+            if (i + DEPTH - 1 < nsl) load(i + DEPTH - 1, (d + DEPTH - 1) % DEPTH, (d + DEPTH - 1) % DEPTH);
+            if (i < nsl) compute(i, d);
+        }
     }
 
-    // ---- merge the four waves in LDS (the rings are free once all waves are here) ----
-    __syncthreads();
+    // ---- merge the four waves in LDS ----
     float *sML = reinterpret_cast<float *>(smem);          // [4 waves][RP][2]
     float *sO = sML + 4 * RP * 2;                          // [4 waves][RP][D]
     #pragma unroll
@@ -360,9 +333,7 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
     constexpr int RP = NB * 16;
-    const size_t merge = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
-    const size_t rings = (size_t)4 * VerifySlab<D>::WAVE_BYTES;
-    const size_t lds = merge > rings ? merge : rings;
+    const size_t lds = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
     hipLaunchKernelGGL((verify_split_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256), lds, st, a);
     return hipGetLastError();
 }
