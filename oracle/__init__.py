@@ -14,6 +14,8 @@ K/V materialisation:
                     position id (Sec. 3.2, memory update cycle: a slot shares
                     the position id of the raw token after it).
 
+``accept_stochastic`` wraps the rejection-sampling rule (oracle.c).
+
 ``masw_sets`` holds the visible-set simulator written from the paper's set
 definitions (Sec. 3.1 and 3.2).
 
@@ -49,6 +51,8 @@ def _load():
     lib.oracle_rope.argtypes = [i, i, i, _dp, _ip, d]
     lib.oracle_argmax.argtypes = [i, i, _fp, _ip]
     lib.oracle_accept_greedy.argtypes = [i, i, i, _fp, _ip, _ip, _ip]
+    lib.oracle_accept_stochastic.argtypes = [i, i, i, _fp, _fp, _ip, _fp, _ip, _ip]
+    lib.oracle_accept_stochastic.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     for f in ("oracle_attend", "oracle_attend_batched", "oracle_verify", "oracle_project",
@@ -177,4 +181,20 @@ def accept_greedy(logits, draft):
     na = np.zeros(B, dtype=np.int32)
     nx = np.zeros(B, dtype=np.int32)
     lib.oracle_accept_greedy(B, T, V, _ptr(x, _fp), _ptr(dr, _ip), _ptr(na, _ip), _ptr(nx, _ip))
+    return na, nx
+
+
+def accept_stochastic(p, q, draft, u):
+    """p [B, T, V], q [B, T-1, V] float32 probabilities, draft [B, T-1] int,
+    u [B, T] float32 uniforms -> (n_accept [B], next [B])."""
+    lib = _load()
+    p = np.ascontiguousarray(p, dtype=np.float32)
+    B, T, V = p.shape
+    q = np.ascontiguousarray(q, dtype=np.float32).reshape(B, T - 1, V) if T > 1 else np.zeros((B, 0, V), np.float32)
+    dr = np.ascontiguousarray(_i32(draft).reshape(B, T - 1)) if T > 1 else np.zeros((B, 0), np.int32)
+    u = np.ascontiguousarray(u, dtype=np.float32).reshape(B, T)
+    na = np.zeros(B, dtype=np.int32)
+    nx = np.zeros(B, dtype=np.int32)
+    lib.oracle_accept_stochastic(B, T, V, _ptr(p, _fp), _ptr(np.ascontiguousarray(q), _fp), _ptr(dr, _ip),
+                                 _ptr(u, _fp), _ptr(na, _ip), _ptr(nx, _ip))
     return na, nx

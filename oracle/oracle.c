@@ -31,6 +31,8 @@
  *                          prefix of drafted tokens equal to the target's argmax,
  *                          then emit one target token (Sec. 2.1, Eq. sd_speedup's
  *                          L_acc + 1; Sec. 4.1 greedy decoding).
+ *   oracle_accept_stochastic  the rejection-sampling rule with caller-supplied
+ *                          uniforms (Sec. 2.1, Sec. 3.3).
  *
  * Parallelism: OpenMP over independent units only; every unit is computed by
  * one thread in the order written here, so results do not depend on the
@@ -218,6 +220,63 @@ void oracle_accept_greedy(int B, int T, int V, const float *logits, const int *d
         next[b] = am[(size_t)b * T + a];
     }
     free(am);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stochastic accept/reject (the standard speculative-sampling rule that the */
+/* target applies, Sec. 2.1 and Sec. 3.3; it keeps the target's output       */
+/* distribution).  p [B][T][V] target probabilities, q [B][T-1][V] draft     */
+/* probabilities, draft [B][T-1] drafted tokens, u [B][T] uniforms in [0,1). */
+/* For each sequence, in double precision:                                   */
+/*   a = first i < T-1 with NOT (u[i] * q_i(x_i) < p_i(x_i)), x_i = draft[i], */
+/*       else T-1 (every drafted token accepted);                             */
+/*   the emitted token is drawn by inverse CDF with u[T-1] from              */
+/*     r(v) = max(0, p_a(v) - q_a(v))  after a rejection (a < T-1), or       */
+/*     r(v) = p_a(v)                   when everything was accepted,         */
+/*   i.e. the smallest v with r(0) + ... + r(v) > u[T-1] * Z, Z = sum_v r(v) */
+/*   (summed in index order).  If Z == 0 the draw uses p_a; if no index       */
+/*   qualifies (u[T-1] * Z >= the running total) the last v with r(v) > 0.   */
+/* n_accept[b] = a, next[b] = the drawn token.                               */
+/* ------------------------------------------------------------------------ */
+static int inverse_cdf(int V, const float *p, const float *q, double u)
+{
+    double Z = 0.0;
+    for (int v = 0; v < V; ++v) {
+        double r = q ? (double)p[v] - (double)q[v] : (double)p[v];
+        if (r > 0.0) Z += r;
+    }
+    if (Z == 0.0 && q) return inverse_cdf(V, p, NULL, u);
+    const double t = u * Z;
+    double c = 0.0;
+    int last = 0;
+    for (int v = 0; v < V; ++v) {
+        double r = q ? (double)p[v] - (double)q[v] : (double)p[v];
+        if (r <= 0.0) continue;
+        c += r;
+        last = v;
+        if (c > t) return v;
+    }
+    return last;
+}
+
+void oracle_accept_stochastic(int B, int T, int V, const float *p, const float *q, const int *draft,
+                              const float *u, int *n_accept, int *next)
+{
+    for (int b = 0; b < B; ++b) {
+        const float *ub = u + (size_t)b * T;
+        int a = 0;
+        while (a < T - 1) {
+            const int x = draft[(size_t)b * (T - 1) + a];
+            const double px = p[((size_t)b * T + a) * V + x];
+            const double qx = q[((size_t)b * (T - 1) + a) * V + x];
+            if (!((double)ub[a] * qx < px)) break;
+            ++a;
+        }
+        n_accept[b] = a;
+        const float *pa = p + ((size_t)b * T + a) * V;
+        const float *qa = a < T - 1 ? q + ((size_t)b * (T - 1) + a) * V : NULL;
+        next[b] = inverse_cdf(V, pa, qa, (double)ub[T - 1]);
+    }
 }
 
 /* Number of OpenMP threads the batched routines use (1 without OpenMP). */
