@@ -23,7 +23,8 @@ Reported in the same run (sub-objects of the JSON line):
   memory_update  the adaptor alone at 4 rows (32K) and 64 rows (16 sequences)
   verify         the target's 5-query verify attention, 8B- and 70B-shaped
                  layers at a 32768-token prefix
-  accept         greedy accept on [B, 5, 128256] fp32 logits
+  accept         greedy accept on [B, 5, 128256] fp32 logits, and the stochastic
+                 accept/reject rule on probabilities with caller uniforms
   roofline       the dominant kernel (draft decode attention): algorithmic
                  bytes per launch / mean launch duration from HIP events
   cpu_baseline   the fp64 oracle on the host cores (a bounded sample)
@@ -467,6 +468,20 @@ def main():
         acc_res[name] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3), "bytes": nbytes}
         log(f"accept {name}: {t * 1e6:.2f} us")
         del lg, fns, g
+        # stochastic accept/reject with caller uniforms: reads the drafted tokens'
+        # probabilities, then one target row (and one draft row) of the vocabulary
+        ps = [torch.softmax(torch.randn(B, T, V, device="cuda"), -1) for _ in range(4)]
+        qs = [torch.softmax(torch.randn(B, T - 1, V, device="cuda"), -1) for _ in range(4)]
+        uu = torch.rand(B, T, device="cuda")
+        wss = torch.zeros(mad.workspace_bytes(mad.MAD_OP_ACCEPT_STOCH, B, 1, 1, 64, T, V), dtype=torch.uint8,
+                          device="cuda")
+        fns = [lambda j=j: mad.accept_stochastic(ps[j], qs[j], dr, uu, na, nx, ws=wss) for j in range(4)]
+        g = graph_of(torch, lambda: [f() for f in fns])
+        g.replay()
+        t = time_graph(torch, g, reps=4) / 4
+        acc_res[name + "_stochastic"] = {"us": round(t * 1e6, 2), "bytes_max": B * 2 * V * 4}
+        log(f"accept {name} stochastic: {t * 1e6:.2f} us")
+        del ps, qs, fns, g
 
     # --------------------------------------------------------- CPU baseline ----
     cpu = None

@@ -59,6 +59,7 @@ extern "C" {
 #define MAD_OP_UPDATE 1
 #define MAD_OP_VERIFY 2
 #define MAD_OP_ACCEPT 3
+#define MAD_OP_ACCEPT_STOCH 4
 
 /*
  * A per-sequence, per-KV-head run of key/value rows in device memory.
@@ -174,11 +175,41 @@ int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok,
                       void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * Stochastic accept/reject: the rejection-sampling rule of speculative
+ * decoding, which the target applies unchanged (Sec. 2.1, Sec. 3.3), with
+ * uniforms supplied by the caller (so a host and the device can share one
+ * random stream).  For each sequence b, in double precision:
+ *   n_accept[b] = a = first i < T-1 with NOT (u[b][i] q_i(x_i) < p_i(x_i)),
+ *                 x_i = draft_tok[b][i] (a value outside [0, V) is rejected),
+ *                 else T-1;
+ *   next_tok[b] = the inverse-CDF draw with u[b][T-1] from the weights
+ *                 max(0, p_a - q_a) when a < T-1 (the correction), or
+ *                 max(0, p_{T-1}) when all drafts were accepted (the bonus
+ *                 token): the smallest v whose running weight sum exceeds
+ *                 u[b][T-1] * Z, Z the total weight.  An empty residual
+ *                 (Z = 0) draws from p_a; if no index qualifies, the last
+ *                 index of positive weight is returned.
+ * The running sums are formed in a different order than a sequential scan,
+ * so a draw can differ from one only when u[b][T-1] * Z lies within rounding
+ * of a bin edge.
+ *   p         device float32 [B][T][V] target probabilities
+ *   q         device float32 [B][T-1][V] draft probabilities (NULL when T == 1)
+ *   draft_tok device int32 [B][T-1] (NULL when T == 1)
+ *   u         device float32 [B][T] uniforms in [0, 1)
+ *   n_accept, next_tok  device int32 [B]
+ * The workspace (MAD_OP_ACCEPT_STOCH) holds per-chunk sums and arrival
+ * counters; it follows the same rules as the other workspaces.
+ */
+int mad_accept_stochastic(const float *p, const float *q, const int32_t *draft_tok, const float *u, int B, int T,
+                          int V, int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
+
+/*
  * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:
  *   DECODE: B, Hq, Hkv, d                       (T, max_keys ignored)
  *   UPDATE: B = rows (B * n_new), Hq = D, Hkv, d (T, max_keys ignored)
  *   VERIFY: B, Hq, Hkv, d, T                    (max_keys ignored)
  *   ACCEPT: B, T, max_keys = V                  (Hq, Hkv, d ignored)
+ *   ACCEPT_STOCH: B, max_keys = V               (Hq, Hkv, d, T ignored)
  * Returns 0 for an unknown op or invalid sizes.
  */
 size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max_keys);

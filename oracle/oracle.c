@@ -229,7 +229,8 @@ void oracle_accept_greedy(int B, int T, int V, const float *logits, const int *d
 /* probabilities, draft [B][T-1] drafted tokens, u [B][T] uniforms in [0,1). */
 /* For each sequence, in double precision:                                   */
 /*   a = first i < T-1 with NOT (u[i] * q_i(x_i) < p_i(x_i)), x_i = draft[i], */
-/*       else T-1 (every drafted token accepted);                             */
+/*       else T-1 (every drafted token accepted); a drafted value outside    */
+/*       [0, V) is not a token and is rejected;                               */
 /*   the emitted token is drawn by inverse CDF with u[T-1] from              */
 /*     r(v) = max(0, p_a(v) - q_a(v))  after a rejection (a < T-1), or       */
 /*     r(v) = p_a(v)                   when everything was accepted,         */
@@ -267,6 +268,7 @@ void oracle_accept_stochastic(int B, int T, int V, const float *p, const float *
         int a = 0;
         while (a < T - 1) {
             const int x = draft[(size_t)b * (T - 1) + a];
+            if (x < 0 || x >= V) break;           /* not a token: rejected */
             const double px = p[((size_t)b * T + a) * V + x];
             const double qx = q[((size_t)b * (T - 1) + a) * V + x];
             if (!((double)ub[a] * qx < px)) break;

@@ -25,7 +25,7 @@ LIB_PATH = os.path.join(_HERE, "libmad.so")
 
 MAD_OK, MAD_EINVAL, MAD_ENOTSUP, MAD_EHIP, MAD_EWS = 0, -1, -2, -3, -4
 MAD_F32, MAD_BF16 = 0, 1
-MAD_OP_DECODE, MAD_OP_UPDATE, MAD_OP_VERIFY, MAD_OP_ACCEPT = 0, 1, 2, 3
+MAD_OP_DECODE, MAD_OP_UPDATE, MAD_OP_VERIFY, MAD_OP_ACCEPT, MAD_OP_ACCEPT_STOCH = 0, 1, 2, 3, 4
 MAX_BATCH = 64
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -56,11 +56,13 @@ def _load_library():
     lib.mad_verify_attn.argtypes = [vp, i, i, i, i, i, i, f, vp, vp, ctypes.c_int64, ctypes.c_int64,
                                     ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
+    lib.mad_accept_stochastic.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
-    for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy"):
+    for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
+               "mad_accept_stochastic"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -254,5 +256,25 @@ def accept_greedy(logits: torch.Tensor, draft_tok: Optional[torch.Tensor], n_acc
     w = _ws_for(dev, nbytes, ws)
     rc = _load_library().mad_accept_greedy(_ptr(logits), _dtype_code(logits), _ptr(draft_tok), B, T, V,
                                _ptr(n_accept), _ptr(next_tok), _ptr(w), w.numel(), _stream(dev))
+    _check(rc)
+    return n_accept, next_tok
+
+
+def accept_stochastic(p: torch.Tensor, q: Optional[torch.Tensor], draft_tok: Optional[torch.Tensor], u: torch.Tensor,
+                      n_accept=None, next_tok=None, ws: Optional[torch.Tensor] = None):
+    """p [B, T, V] float32 target probabilities, q [B, T-1, V] float32 draft
+    probabilities, draft_tok int32 [B, T-1], u float32 [B, T] uniforms, all on
+    the device.  Returns (n_accept int32 [B], next_tok int32 [B])."""
+    B, T, V = p.shape
+    dev = p.device
+    if n_accept is None:
+        n_accept = torch.empty(B, dtype=torch.int32, device=dev)
+    if next_tok is None:
+        next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+    nbytes = workspace_bytes(MAD_OP_ACCEPT_STOCH, B, 1, 1, 64, T, V)
+    w = _ws_for(dev, nbytes, ws)
+    lib = _load_library()
+    rc = lib.mad_accept_stochastic(_ptr(p), _ptr(q), _ptr(draft_tok), _ptr(u), B, T, V, _ptr(n_accept),
+                                   _ptr(next_tok), _ptr(w), w.numel(), _stream(dev))
     _check(rc)
     return n_accept, next_tok

@@ -14,6 +14,17 @@
 // One launch: workgroup (chunk, row) reduces a chunk of the vocabulary; the
 // last chunk of a row (arrival counter) reduces the row; the last row to
 // finish applies the accept rule for every sequence.
+//
+// Stochastic accept/reject (the rejection-sampling rule the target applies,
+// Sec. 2.1 and Sec. 3.3) with caller-supplied uniforms: drafted token x_i is
+// accepted while u_i q_i(x_i) < p_i(x_i) (exact in double precision); the
+// emitted token is the inverse-CDF draw with u_{T-1} from max(0, p_a - q_a)
+// after the first rejection a, or from p_{T-1} when all were accepted.  One
+// launch: workgroup (chunk, sequence) re-derives a from the T-1 drafted
+// tokens, sums its vocabulary chunk of the draw's weights (and of p_a, the
+// fallback when the residual is empty) in double precision; the last chunk of
+// the sequence locates the chunk where the running sum passes u_{T-1} Z and
+// scans it.
 #include "mad_device.h"
 #include "mad_internal.h"
 
@@ -158,6 +169,189 @@ void accept_ws_layout(int B, int T, int V, size_t *off_part, size_t *off_rows) {
     const size_t chunks = ((size_t)V + kAcceptChunk - 1) / kAcceptChunk;
     *off_part = kCounterRegionBytes;
     *off_rows = kCounterRegionBytes + align256(rows * chunks * 8);
+}
+
+// ---------------------------------------------------------- stochastic ----
+
+__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
+    const uint64_t u = __double_as_longlong(v);
+    const int lo = __shfl_xor((int)(uint32_t)u, m, 64);
+    const int hi = __shfl_xor((int)(uint32_t)(u >> 32), m, 64);
+    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+__device__ __forceinline__ double wave_sum_f64(double v) {
+    #pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v += shfl_xor_f64(v, m);
+    return v;
+}
+// weight of entry v in the draw: max(0, p - q) (q given) or max(0, p)
+__device__ __forceinline__ double draw_weight(float p, float q, bool resid) {
+    const double r = resid ? (double)p - (double)q : (double)p;
+    return r > 0.0 ? r : 0.0;
+}
+
+__global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x % a.B, chunk = blockIdx.x / a.B;
+    const int T = a.T, V = a.V;
+    __shared__ int s_a;
+    __shared__ double s_w[2][4];
+    __shared__ int s_flag;
+    // ---- the first rejection a (every workgroup of the sequence derives it) ----
+    if (wave == 0) {
+        bool rej = false;
+        if (lane < T - 1) {
+            const int x = a.draft[(size_t)b * (T - 1) + lane];
+            if (x < 0 || x >= V) {
+                rej = true;   // not a token
+            } else {
+                const double px = a.p[((size_t)b * T + lane) * V + x];
+                const double qx = a.q[((size_t)b * (T - 1) + lane) * V + x];
+                rej = !((double)a.u[(size_t)b * T + lane] * qx < px);
+            }
+        }
+        const unsigned long long m = __ballot(rej);
+        if (lane == 0) s_a = m ? __ffsll((long long)m) - 1 : T - 1;
+    }
+    __syncthreads();
+    const int acc = s_a;
+    const bool resid = acc < T - 1;
+    const float *pr = a.p + ((size_t)b * T + acc) * V;
+    const float *qr = resid ? a.q + ((size_t)b * (T - 1) + acc) * V : pr;
+
+    // ---- this chunk's sums of the draw weights and of p_a ----
+    const int v0 = chunk * kAcceptChunk, v1 = min(V, v0 + kAcceptChunk);
+    double sr = 0.0, sp = 0.0;
+    if (a.vec16) {
+        constexpr int NV = kAcceptChunk / (256 * 4);
+        float4 pv[NV], qv[NV];
+        #pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int e = v0 + (tid + 256 * k) * 4;
+            const bool in = e < v1;
+            pv[k] = in ? *reinterpret_cast<const float4 *>(pr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+            qv[k] = in && resid ? *reinterpret_cast<const float4 *>(qr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        #pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            sr += draw_weight(pv[k].x, qv[k].x, resid) + draw_weight(pv[k].y, qv[k].y, resid) +
+                  draw_weight(pv[k].z, qv[k].z, resid) + draw_weight(pv[k].w, qv[k].w, resid);
+            sp += draw_weight(pv[k].x, 0.f, false) + draw_weight(pv[k].y, 0.f, false) +
+                  draw_weight(pv[k].z, 0.f, false) + draw_weight(pv[k].w, 0.f, false);
+        }
+    } else {
+        for (int v = v0 + tid; v < v1; v += 256) {
+            const float pv = pr[v];
+            sr += draw_weight(pv, resid ? qr[v] : 0.f, resid);
+            sp += draw_weight(pv, 0.f, false);
+        }
+    }
+    sr = wave_sum_f64(sr);
+    sp = wave_sum_f64(sp);
+    if (lane == 0) { s_w[0][wave] = sr; s_w[1][wave] = sp; }
+    __syncthreads();
+    double *sums = a.sums + (size_t)b * a.n_chunks * 2;
+    if (tid == 0) {
+        const double cr = s_w[0][0] + s_w[0][1] + s_w[0][2] + s_w[0][3];
+        const double cp = s_w[1][0] + s_w[1][1] + s_w[1][2] + s_w[1][3];
+        __hip_atomic_store(reinterpret_cast<uint64_t *>(sums + 2 * chunk), (uint64_t)__double_as_longlong(cr),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(reinterpret_cast<uint64_t *>(sums + 2 * chunk + 1), (uint64_t)__double_as_longlong(cp),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    wait_vm_stores();
+    __syncthreads();
+    if (tid == 0) {
+        unsigned *cnt = a.counters + (size_t)b * kCounterStride;
+        const int last = arrive(cnt) == (unsigned)(a.n_chunks - 1);
+        if (last) reset_counter(cnt);
+        s_flag = last;
+    }
+    __syncthreads();
+    if (!s_flag) return;
+
+    // ---- last chunk of the sequence: locate the chunk, then the token ----
+    __shared__ int s_c, s_mode, s_fb;
+    __shared__ double s_t;
+    if (tid == 0) {
+        double Zr = 0.0, Zp = 0.0;
+        for (int c = 0; c < a.n_chunks; ++c) {
+            Zr += __longlong_as_double((long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c)));
+            Zp += __longlong_as_double((long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c + 1)));
+        }
+        const int use_p = Zr == 0.0;   // empty residual: the draw uses p_a
+        const double t = (double)a.u[(size_t)b * T + T - 1] * (use_p ? Zp : Zr);
+        double run = 0.0;
+        int cs = -1, clast = -1;
+        for (int c = 0; c < a.n_chunks; ++c) {
+            const double w = __longlong_as_double(
+                (long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c + use_p)));
+            if (w > 0.0) clast = c;
+            if (w > 0.0 && run + w > t) { cs = c; break; }
+            run += w;
+        }
+        const int fb = cs < 0;   // no chunk passes t: the last positive entry is drawn
+        s_c = fb ? (clast >= 0 ? clast : 0) : cs;
+        s_mode = use_p;
+        s_fb = fb;
+        s_t = fb ? 0.0 : t - run;   // target measured from the chunk's start
+    }
+    __syncthreads();
+    const int cs = s_c;
+    const bool wres = resid && !s_mode;
+    // runs of RUN consecutive entries of the chunk, one per thread
+    constexpr int RUN = kAcceptChunk / 256;
+    const int cbeg = cs * kAcceptChunk, cend = min(V, cbeg + kAcceptChunk);
+    const int r0 = cbeg + tid * RUN, r1 = min(cend, r0 + RUN);
+    double mine = 0.0;
+    int lastpos = -1;
+    for (int v = r0; v < r1; ++v) {
+        const double w = draw_weight(pr[v], wres ? qr[v] : 0.f, wres);
+        mine += w;
+        if (w > 0.0) lastpos = v;
+    }
+    __shared__ double s_run[256];
+    __shared__ int s_pos[256];
+    s_run[tid] = mine;
+    s_pos[tid] = lastpos;
+    __syncthreads();
+    if (tid == 0) {
+        int last_any = -1;
+        for (int k = 0; k < 256; ++k) last_any = s_pos[k] > last_any ? s_pos[k] : last_any;
+        int v_out = last_any >= 0 ? last_any : cbeg;   // fallback: the chunk's last positive entry
+        if (!s_fb) {
+            const double tt = s_t;
+            double e = 0.0;
+            for (int k = 0; k < 256; ++k) {
+                const double w = s_run[k];
+                if (w > 0.0 && e + w > tt) {
+                    // the crossing lies in run k: walk it in index order
+                    const int q0 = cbeg + k * RUN, q1 = min(cend, q0 + RUN);
+                    v_out = s_pos[k];   // if rounding keeps the target above the run's own sum
+                    for (int v = q0; v < q1; ++v) {
+                        const double wv = draw_weight(pr[v], wres ? qr[v] : 0.f, wres);
+                        if (wv <= 0.0) continue;
+                        e += wv;
+                        if (e > tt) { v_out = v; break; }
+                    }
+                    break;
+                }
+                e += w;
+            }
+        }
+        a.n_accept[b] = acc;
+        a.next_tok[b] = v_out;
+    }
+}
+
+size_t stoch_ws_bytes(int B, int V) {
+    const size_t chunks = ((size_t)V + kAcceptChunk - 1) / kAcceptChunk;
+    return kCounterRegionBytes + align256((size_t)B * chunks * 16);
+}
+
+hipError_t launch_stoch(const StochArgs &a, hipStream_t st) {
+    hipLaunchKernelGGL(stoch_kernel, dim3((unsigned)(a.B * a.n_chunks)), dim3(256), 0, st, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_accept(const AcceptArgs &a, int dtype, hipStream_t st) {

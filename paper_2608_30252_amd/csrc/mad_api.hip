@@ -93,6 +93,9 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
         case MAD_OP_VERIFY:
             if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128) || T < 1) return 0;
             return mad::verify_ws_bytes(B, Hq, Hkv, d, T);
+        case MAD_OP_ACCEPT_STOCH:   // B, max_keys = V
+            if (B < 1 || B > MAD_MAX_BATCH || max_keys < 1) return 0;
+            return mad::stoch_ws_bytes(B, max_keys);
         case MAD_OP_ACCEPT:   // B, T, max_keys = V
             if (B < 1 || T < 1 || max_keys < 1) return 0;
             return mad::accept_ws_bytes(B, T, max_keys);
@@ -305,6 +308,36 @@ int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, i
     const size_t esz = dtype == MAD_BF16 ? 2 : 4;
     a.vec16 = aligned16(logits) && ((size_t)V * esz) % 16 == 0;
     return hip_status(mad::launch_accept(a, dtype, (hipStream_t)stream), "accept launch");
+}
+
+int mad_accept_stochastic(const float *p, const float *q, const int32_t *draft_tok, const float *u, int B, int T,
+                          int V, int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (T < 1 || T > 64) return fail(MAD_EINVAL, "T=%d outside [1, 64]", T);
+    if (V < 1) return fail(MAD_EINVAL, "V=%d", V);
+    if (!p || !u || !n_accept || !next_tok) return fail(MAD_EINVAL, "null p, u, n_accept or next_tok");
+    if (T > 1 && (!q || !draft_tok)) return fail(MAD_EINVAL, "q and draft_tok required when T > 1");
+    if ((size_t)B > (size_t)mad::kCounterLines) return fail(MAD_EINVAL, "B=%d", B);
+    const size_t need = mad::stoch_ws_bytes(B, V);
+    if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
+    if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
+    if (((uintptr_t)ws & 255u) != 0) return fail(MAD_EINVAL, "workspace not 256-byte aligned");
+    mad::StochArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p = p;
+    a.q = q;
+    a.u = u;
+    a.draft = draft_tok;
+    a.n_accept = n_accept;
+    a.next_tok = next_tok;
+    a.counters = (unsigned *)ws;
+    a.sums = (double *)((char *)ws + mad::kCounterRegionBytes);
+    a.B = B;
+    a.T = T;
+    a.V = V;
+    a.n_chunks = (V + mad::kAcceptChunk - 1) / mad::kAcceptChunk;
+    a.vec16 = aligned16(p) && (T == 1 || aligned16(q)) && V % 4 == 0;
+    return hip_status(mad::launch_stoch(a, (hipStream_t)stream), "stochastic accept launch");
 }
 
 }  // extern "C"

@@ -138,6 +138,18 @@ size_t accept_ws_bytes(int B, int T, int V);
 void accept_ws_layout(int B, int T, int V, size_t *off_part, size_t *off_rows);
 hipError_t launch_accept(const AcceptArgs &a, int dtype, hipStream_t st);
 
+struct StochArgs {
+    const float *p, *q, *u;    // [B][T][V], [B][T-1][V], [B][T]
+    const int32_t *draft;      // [B][T-1]
+    int32_t *n_accept, *next_tok;
+    double *sums;              // [B][n_chunks][2]: chunk sums of the draw's r and of p_a
+    unsigned *counters;        // line b: arrivals of sequence b's chunks
+    int B, T, V, n_chunks;
+    int vec16;                 // rows of p and q 16-byte aligned (V % 4 == 0, aligned bases)
+};
+size_t stoch_ws_bytes(int B, int V);
+hipError_t launch_stoch(const StochArgs &a, hipStream_t st);
+
 // ws layout helpers: counters first (256-byte aligned), then partials.
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 

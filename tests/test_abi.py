@@ -138,3 +138,25 @@ def test_verify_and_accept_validation(mad):
     assert acc(draft=0) == mad.MAD_EINVAL
     assert acc(dtype=5) == mad.MAD_ENOTSUP
     assert acc() == mad.MAD_EWS
+
+
+def test_stochastic_accept_validation(mad):
+    lib = mad._load_library()
+    vp = ctypes.c_void_p
+    def st(B=1, T=5, V=128256, q=1 << 21, draft=1 << 22, u=1 << 23, ws=None, ws_bytes=0):
+        return lib.mad_accept_stochastic(vp(1 << 20), vp(q) if q else None, vp(draft) if draft else None,
+                                         vp(u) if u else None, B, T, V, vp(1 << 24), vp(1 << 25),
+                                         vp(ws) if ws else None, ws_bytes, None)
+    assert st(V=0) == mad.MAD_EINVAL
+    assert st(T=0) == mad.MAD_EINVAL
+    assert st(T=65) == mad.MAD_EINVAL
+    assert st(B=0) == mad.MAD_EINVAL
+    assert st(q=0) == mad.MAD_EINVAL                      # q required when T > 1
+    assert st(draft=0) == mad.MAD_EINVAL
+    assert st(u=0) == mad.MAD_EINVAL
+    assert st() == mad.MAD_EWS                            # workspace missing
+    need = mad.workspace_bytes(mad.MAD_OP_ACCEPT_STOCH, 1, 1, 1, 64, 5, 128256)
+    assert need > 0
+    assert st(ws=1 << 26, ws_bytes=need - 1) == mad.MAD_EWS
+    assert st(ws=(1 << 26) + 16, ws_bytes=need) == mad.MAD_EINVAL   # not 256-byte aligned
+    assert st(T=1, q=0, draft=0) == mad.MAD_EWS          # T == 1 needs neither q nor drafts
