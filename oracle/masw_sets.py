@@ -26,6 +26,12 @@ Sec. 3.2, memory materialisation and the memory update cycle):
   Sec. 3.1 with sinks excluded.
 * Rollback (Sec. 3.3): a state rolled back to t processed tokens is the state
   after t tokens; slots materialised in passes of positions >= t are dropped.
+* Batched schedule (reading adopted for "compressing each evicted 64-token
+  block"): with u slots per update, the slots of u consecutive boundaries are
+  materialised together in the pass of the block's last raw token
+  S + k*u*r - 1, as extra positions after it; a raw query sees a slot only
+  once it is materialised.  A slot's write scope is unchanged (it is defined
+  by the slot's position id).  u = 1 is the per-boundary schedule above.
 """
 from dataclasses import dataclass, field
 from typing import List
@@ -43,9 +49,9 @@ class View:
 
 
 class MaswSets:
-    def __init__(self, S: int, W: int, r: int):
-        assert S >= 0 and W >= 1 and r >= 1
-        self.S, self.W, self.r = S, W, r
+    def __init__(self, S: int, W: int, r: int, u: int = 1):
+        assert S >= 0 and W >= 1 and r >= 1 and u >= 1
+        self.S, self.W, self.r, self.u = S, W, r, u
 
     def boundary(self, m: int) -> int:
         """Position id b_m of slot g_m (m >= 1)."""
@@ -56,20 +62,23 @@ class MaswSets:
         """Number of slots materialised once raw positions 0..t-1 are processed."""
         if t <= self.S:
             return 0
-        return (t - self.S) // self.r
+        return (t - self.S) // (self.r * self.u) * self.u
+
+    def slots_made_in_pass_of(self, p: int) -> List[int]:
+        """Slot indices m materialised in the forward pass of raw position p."""
+        return list(range(self.slots_after(p) + 1, self.slots_after(p + 1) + 1))
 
     def materialised_in_pass_of(self, p: int):
-        """Slot index m materialised in the forward pass of raw position p, or None."""
-        if p + 1 <= self.S:
-            return None
-        if (p + 1 - self.S) % self.r == 0:
-            return (p + 1 - self.S) // self.r
-        return None
+        """Per-boundary schedule: the slot index m made in the pass of p, or None."""
+        made = self.slots_made_in_pass_of(p)
+        return made[-1] if made else None
 
     def raw_view(self, p: int) -> View:
         """What the raw query at position p attends to."""
         sink = list(range(0, min(self.S, p + 1)))
-        slots = [m for m in range(1, self.slots_after(p + 1) + 1) if self.boundary(m) <= p]
+        # slots made in passes of earlier positions (a slot made in p's own pass
+        # sits after p; the same holds under the batched schedule)
+        slots = list(range(1, self.slots_after(p) + 1))
         lo = max(self.S, p - self.W + 1)
         window = list(range(lo, p + 1)) if p >= self.S else []
         return View(sink, slots, window)

@@ -107,3 +107,45 @@ def test_slot_scope():
         b = sets.boundary(m)
         assert sets.slot_scope(m).window == sets.raw_view(b - 1).window
         assert sets.slot_scope(m).slots == sets.raw_view(b).slots
+
+
+def _cycle_batched(S, W, r, u, n_tokens):
+    """Step-by-step cycle of the batched schedule: count non-sink raw tokens;
+    every r of them a boundary is passed (its slot is pending, named by the
+    next raw position); after u boundaries the pending slots are made in the
+    pass of the current token."""
+    made = []       # (pass position, slot position id)
+    pending = []
+    since = 0
+    for p in range(n_tokens):
+        if p >= S:
+            since += 1
+        if since == r:
+            pending.append(p + 1)
+            since = 0
+            if len(pending) == u:
+                made += [(p, pid) for pid in pending]
+                pending = []
+    return made
+
+
+@pytest.mark.parametrize("S,W,r,u", [(0, 8, 4, 2), (3, 5, 2, 3), (0, 1024, 16, 4), (128, 128, 4, 4)])
+def test_batched_schedule_matches_stepwise_cycle(S, W, r, u):
+    sets = MaswSets(S, W, r, u)
+    n = S + 30 * r * u + 5
+    made = _cycle_batched(S, W, r, u, n)
+    for m, (p_pass, pos_id) in enumerate(made, start=1):
+        assert sets.boundary(m) == pos_id
+        assert m in sets.slots_made_in_pass_of(p_pass)
+    per_boundary = MaswSets(S, W, r)
+    for p in range(S, n):
+        view = sets.raw_view(p)
+        assert view.slots == [m for m, (q, _) in enumerate(made, 1) if q < p]
+        # never ahead of the per-boundary schedule, at most u - 1 slots behind it,
+        # and level with it right after every batch
+        lag = len(per_boundary.raw_view(p).slots) - len(view.slots)
+        assert 0 <= lag <= u - 1
+        if (p - S) % (r * u) == 0:
+            assert lag == 0
+        assert view.window == per_boundary.raw_view(p).window
+        assert sets.slot_scope(1 + p % 7) == per_boundary.slot_scope(1 + p % 7)
