@@ -116,6 +116,28 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
                           void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * The same attention with a per-row choice for the new token, so that one
+ * launch serves the raw query of a step and the write-scope queries of the
+ * memory slots materialised in that step (Sec. 3.2: a slot is an extra
+ * position of the pass; its write scope is the sinks, the slots up to it and
+ * the W raw tokens before its position id, which for the newest slot end at
+ * the current token).
+ *   new_mode  host uint8 [B]: 0 = the row has no new token; 1 = the row's key
+ *             sequence ends with k_new/v_new[b] (not written anywhere);
+ *             2 = as 1, and the token is appended to the row's window ring at
+ *             (start + len) % cap, as mad_draft_decode_attn does.
+ * Rows may alias one sequence's buffers (seq_stride 0); at most one row of a
+ * shared ring may append, and no row's window may include the ring row being
+ * appended (the window of a mode-1 row stops before the current token, which
+ * it reads from k_new/v_new instead).  k_new/v_new are required when any row
+ * has mode 1 or 2.  Everything else (layouts, workspace, errors) is as for
+ * mad_draft_decode_attn.
+ */
+int mad_draft_step_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                        const mad_kv_view *mem, const mad_kv_view *win, const void *k_new, const void *v_new,
+                        const uint8_t *new_mode, void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
  * Memory update by the memory adaptor (Sec. 3.2, projection and KV
  * materialisation): for every firing sequence b and slot i < n_new,
  *   [k~ | v] = x[b][i] . [W_K,g ; W_V,g]^T          (mirrored projections)

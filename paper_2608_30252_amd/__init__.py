@@ -57,12 +57,13 @@ def _load_library():
                                     ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_accept_stochastic.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp, vp, sz, vp]
+    lib.mad_draft_step_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, _u8p, vp, vp, vp, sz, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
-               "mad_accept_stochastic"):
+               "mad_accept_stochastic", "mad_draft_step_attn"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -188,6 +189,37 @@ def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
                                    ctypes.byref(wv) if wv is not None else None,
                                    _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(lse),
                                    _ptr(w), w.numel(), _stream(q.device))
+    _check(rc)
+    return out, lse
+
+
+def draft_step_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV], k_new: Optional[torch.Tensor],
+                    v_new: Optional[torch.Tensor], new_mode, out: Optional[torch.Tensor] = None,
+                    lse: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                    ws: Optional[torch.Tensor] = None):
+    """draft_decode_attn with a per-row new-token mode (host list of B values):
+    0 = no new token, 1 = attend k_new/v_new[b] only, 2 = attend and append it
+    to the row's ring.  Rows may alias one sequence's buffers (batch dim 1)."""
+    B, Hq, d = q.shape
+    Hkv = (mem.k if mem is not None else win.k).shape[1]
+    if len(new_mode) != B:
+        raise ValueError("new_mode needs one entry per row")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    if scale is None:
+        scale = d ** -0.5
+    mv = mem.view(B) if mem is not None else None
+    wv = win.view(B) if win is not None else None
+    modes = (ctypes.c_uint8 * B)(*[int(m) for m in new_mode])
+    nbytes = workspace_bytes(MAD_OP_DECODE, B, Hq, Hkv, d)
+    w = _ws_for(q.device, nbytes, ws)
+    rc = _load_library().mad_draft_step_attn(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
+                                             ctypes.byref(mv) if mv is not None else None,
+                                             ctypes.byref(wv) if wv is not None else None,
+                                             _ptr(k_new), _ptr(v_new), modes, _ptr(out), _ptr(lse),
+                                             _ptr(w), w.numel(), _stream(q.device))
     _check(rc)
     return out, lse
 

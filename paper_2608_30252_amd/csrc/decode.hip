@@ -4,7 +4,10 @@
 // G = Hq/Hkv query heads of the current token over the logical key sequence
 //     [ memory rows 0..mlen-1 (sinks, then slots) | window ring rows 0..wlen-1 | new token ]
 // (the working memory M_t of Sec. 3.1) and appends the new token's K/V to the
-// window ring in the same pass (Sec. 3.2).
+// window ring in the same pass (Sec. 3.2).  Per row the new token can also be
+// attended without being appended (a slot's write scope that ends at the
+// current token) or left out, so one launch serves a raw query and the write
+// scopes of the slots made in the same pass.
 //
 // Work decomposition (split-K / flash-decoding), grid = n_splits * units
 // workgroups, units = B * Hkv; workgroup w handles unit u = w % units and key
@@ -249,7 +252,9 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int u = blockIdx.x % units, s = a.n_splits - 1 - (int)(blockIdx.x / units);
     const int b = u / a.Hkv, c = u - b * a.Hkv;
     const int mlen = a.mlen[b], wlen = a.wlen[b], wst = a.wstart[b];
-    const bool has_new = a.kn != nullptr;
+    const int nmode = a.kn != nullptr ? a.nmode[b] : 0;
+    const bool has_new = nmode >= 1;      // the key sequence ends with the current token
+    const bool appends = nmode == 2;      // ... which this row also writes into its ring
     const int n = mlen + wlen + (has_new ? 1 : 0);
     const int k0 = s * a.chunk;
     const int k1 = min(n, k0 + a.chunk);
@@ -474,7 +479,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     // ---- append the new token to the window ring (the workgroup holding it) ----
     // Its row is outside every window of this launch (the window ends just
     // before it), and attention above read the token from k_new / v_new.
-    if (has_new && k0 <= n - 1 && n - 1 < k1) {
+    if (appends && k0 <= n - 1 && n - 1 < k1) {
         if (tid < 2 * C::CPR) {
             int r = wst + wlen;
             if (r >= w_cap) r -= w_cap;

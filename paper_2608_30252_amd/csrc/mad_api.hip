@@ -47,9 +47,10 @@ int check_heads(int B, int Hq, int Hkv, int d, int dtype) {
     return MAD_OK;
 }
 
-// Validate a kv view for B sequences; `ring` enables the start array check.
+// Validate a kv view for B sequences; `ring` enables the start array check;
+// rows with append[b] != 0 need room for one more row.
 int check_view(const mad_kv_view *v, const char *name, int B, int Hkv, int d, int dtype, bool ring,
-               bool need_write_room) {
+               const unsigned char *append) {
     if (!v->k || !v->v) return fail(MAD_EINVAL, "%s: null k or v", name);
     if (!aligned16(v->k) || !aligned16(v->v)) return fail(MAD_EINVAL, "%s: k/v not 16-byte aligned", name);
     if (v->cap < 1) return fail(MAD_EINVAL, "%s: cap=%d", name, v->cap);
@@ -62,7 +63,7 @@ int check_view(const mad_kv_view *v, const char *name, int B, int Hkv, int d, in
         return fail(MAD_EINVAL, "%s: seq_stride %lld overlaps heads", name, (long long)v->seq_stride);
     for (int b = 0; b < B; ++b) {
         int len = v->len[b];
-        int room = need_write_room ? 1 : 0;
+        int room = (append && append[b]) ? 1 : 0;
         if (len < 0 || len + room > v->cap)
             return fail(MAD_EINVAL, "%s: len[%d]=%d (+%d) exceeds cap %d", name, b, len, room, v->cap);
         if (ring && v->start) {
@@ -104,20 +105,35 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
     }
 }
 
-int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
-                          const mad_kv_view *mem, const mad_kv_view *win, const void *k_new,
-                          const void *v_new, void *out, float *lse, void *ws, size_t ws_bytes,
-                          void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The draft decode attention with a per-row new-token mode (0: none, 1: attend
+// k_new/v_new, 2: attend and append to the ring); both entry points use it.
+int decode_impl(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale, const mad_kv_view *mem,
+                const mad_kv_view *win, const void *k_new, const void *v_new, const unsigned char *mode, void *out,
+                float *lse, void *ws, size_t ws_bytes, void *stream) {
     int rc = check_heads(B, Hq, Hkv, d, dtype);
     if (rc) return rc;
     if (!q || !out) return fail(MAD_EINVAL, "null q or out");
     if (!aligned16(q) || !aligned16(out)) return fail(MAD_EINVAL, "q/out not 16-byte aligned");
     if ((k_new == nullptr) != (v_new == nullptr)) return fail(MAD_EINVAL, "k_new and v_new must both be given or both null");
     if (k_new && (!aligned16(k_new) || !aligned16(v_new))) return fail(MAD_EINVAL, "k_new/v_new not 16-byte aligned");
-    if (k_new && !win) return fail(MAD_EINVAL, "k_new needs a window ring to append to");
+    unsigned char append[MAD_MAX_BATCH];
+    int n_append = 0;
+    for (int b = 0; b < B; ++b) {
+        if (mode[b] > 2) return fail(MAD_EINVAL, "new_mode[%d]=%d outside {0, 1, 2}", b, (int)mode[b]);
+        if (mode[b] && !k_new) return fail(MAD_EINVAL, "new_mode[%d]=%d needs k_new and v_new", b, (int)mode[b]);
+        append[b] = mode[b] == 2;
+        n_append += append[b];
+    }
+    if (n_append && !win) return fail(MAD_EINVAL, "appending the new token needs a window ring");
+    if (n_append > 1 && win->seq_stride == 0)
+        return fail(MAD_EINVAL, "rows that share one window ring (seq_stride 0) cannot all append to it");
     if (!(scale > 0.f) || scale != scale) return fail(MAD_EINVAL, "scale must be positive");
-    if (mem && (rc = check_view(mem, "mem", B, Hkv, d, dtype, false, false))) return rc;
-    if (win && (rc = check_view(win, "win", B, Hkv, d, dtype, true, k_new != nullptr))) return rc;
+    if (mem && (rc = check_view(mem, "mem", B, Hkv, d, dtype, false, nullptr))) return rc;
+    if (win && (rc = check_view(win, "win", B, Hkv, d, dtype, true, append))) return rc;
     const int G = Hq / Hkv;
     if ((size_t)B * Hkv > (size_t)mad::kCounterLines)
         return fail(MAD_ENOTSUP, "B*Hkv=%d too large for the counter region", B * Hkv);
@@ -129,7 +145,8 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
         a.mlen[b] = mem ? mem->len[b] : 0;
         a.wlen[b] = win ? win->len[b] : 0;
         a.wstart[b] = (win && win->start) ? win->start[b] : 0;
-        n_keys[b] = a.mlen[b] + a.wlen[b] + (k_new ? 1 : 0);
+        n_keys[b] = a.mlen[b] + a.wlen[b] + (mode[b] ? 1 : 0);
+        a.nmode[b] = mode[b];
     }
     mad::DecodePlan p = mad::plan_decode(B, Hkv, G, d, dtype, n_keys);
     size_t need = p.n_splits > 1 ? mad::decode_ws_bytes(B, Hq, Hkv, d) : 0;
@@ -167,6 +184,31 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     return hip_status(mad::launch_decode(a, dtype, d, G, (hipStream_t)stream), "decode launch");
 }
 
+}  // namespace
+
+extern "C" {
+
+int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                          const mad_kv_view *mem, const mad_kv_view *win, const void *k_new,
+                          const void *v_new, void *out, float *lse, void *ws, size_t ws_bytes,
+                          void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (k_new && !win) return fail(MAD_EINVAL, "k_new needs a window ring to append to");
+    unsigned char mode[MAD_MAX_BATCH];
+    for (int b = 0; b < B; ++b) mode[b] = k_new ? 2 : 0;
+    return decode_impl(q, B, Hq, Hkv, d, dtype, scale, mem, win, k_new, v_new, mode, out, lse, ws, ws_bytes,
+                       stream);
+}
+
+int mad_draft_step_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                        const mad_kv_view *mem, const mad_kv_view *win, const void *k_new, const void *v_new,
+                        const uint8_t *new_mode, void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    if (!new_mode) return fail(MAD_EINVAL, "null new_mode");
+    return decode_impl(q, B, Hq, Hkv, d, dtype, scale, mem, win, k_new, v_new, new_mode, out, lse, ws, ws_bytes,
+                       stream);
+}
+
 int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const uint8_t *fire, int B, int n_new,
                       int D, int Hkv, int d, int dtype, double rope_base, const mad_kv_view *mem, void *ws,
                       size_t ws_bytes, void *stream) {
@@ -181,7 +223,7 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
     if (!aligned16(x) || !aligned16(w_kv)) return fail(MAD_EINVAL, "x/w_kv not 16-byte aligned");
     if (!(rope_base > 1.0) || rope_base != rope_base || rope_base > 1e300)
         return fail(MAD_EINVAL, "rope_base must be finite and > 1");
-    int rc = check_view(mem, "mem", B, Hkv, d, dtype, false, false);
+    int rc = check_view(mem, "mem", B, Hkv, d, dtype, false, nullptr);
     if (rc) return rc;
     for (int b = 0; b < B; ++b) {
         const bool f = fire ? fire[b] != 0 : true;

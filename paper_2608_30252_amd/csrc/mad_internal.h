@@ -50,6 +50,7 @@ struct DecodeArgs {
     int Hq, Hkv, units, n_splits, chunk, w_cap;
     int nsub;             // wave groups per workgroup (1 or 2)
     int mlen[kMaxB], wstart[kMaxB], wlen[kMaxB];
+    unsigned char nmode[kMaxB];   // per row: 0 no new token, 1 attend it, 2 attend and append it
 };
 
 struct DecodePlan {

@@ -90,6 +90,28 @@ class MemoryLayout:
         start = (b - win_len - self.S) % self.ring_cap
         return DecodeView(self.S + m, start, win_len)
 
+    def step_views(self, p: int):
+        """Rows of one fused launch for raw position p (draft_step_attn): the raw
+        query (mode 2: attends and appends the current token) and, when slots
+        are materialised in this pass, one row per new slot's write scope.  A
+        scope that ends at the current token stops one ring row short and
+        attends the token from k_new (mode 1); older scopes have no new token
+        (mode 0).  The memory update of the pass must run before the launch.
+        Returns ([DecodeView, ...], [mode, ...])."""
+        views, modes = [self.decode_view(p)], [2]
+        upd = self.update_in_pass_of(p)
+        if upd is not None:
+            for i in range(len(upd.positions)):
+                m = upd.first_slot + i
+                v = self.slot_scope_view(m)
+                if self.slot_position(m) - 1 == p:   # the scope ends at the current token
+                    views.append(DecodeView(v.mem_len, v.win_start, v.win_len - 1))
+                    modes.append(1)
+                else:
+                    views.append(v)
+                    modes.append(0)
+        return views, modes
+
     def rollback_ok(self, p_furthest: int, p_new: int) -> bool:
         """True if the ring still holds every raw row the window of p_new needs
         after speculative writes up to raw position p_furthest - 1."""

@@ -160,3 +160,34 @@ def test_stochastic_accept_validation(mad):
     assert st(ws=1 << 26, ws_bytes=need - 1) == mad.MAD_EWS
     assert st(ws=(1 << 26) + 16, ws_bytes=need) == mad.MAD_EINVAL   # not 256-byte aligned
     assert st(T=1, q=0, draft=0) == mad.MAD_EWS          # T == 1 needs neither q nor drafts
+
+
+def test_step_attn_validation(mad):
+    """mad_draft_step_attn: per-row new-token modes are checked before launch."""
+    lib = mad._load_library()
+    vp = ctypes.c_void_p
+    B = 3
+    ln = (ctypes.c_int32 * B)(100, 50, 50)
+    st = (ctypes.c_int32 * B)(0, 0, 0)
+    ring = lambda seq_stride: mad._KVView(1 << 24, 1 << 25, seq_stride, 256 * 64, 256, st, ln)
+
+    def call(modes, kn=1 << 22, vn=1 << 23, win=ring(0), B=B):
+        m = None if modes is None else (ctypes.c_uint8 * len(modes))(*modes)
+        w = None if win is None else ctypes.byref(win)
+        return lib.mad_draft_step_attn(vp(1 << 20), B, 32, 8, 64, mad.MAD_BF16, 0.125, None, w,
+                                       vp(kn) if kn else None, vp(vn) if vn else None, m, vp(1 << 21),
+                                       None, None, 0, None)
+    assert call(None) == mad.MAD_EINVAL and "new_mode" in _last_error(mad)
+    assert call([2, 3, 0]) == mad.MAD_EINVAL and "outside" in _last_error(mad)
+    assert call([2, 1, 0], kn=None, vn=None) == mad.MAD_EINVAL             # modes 1/2 need k_new
+    assert call([0, 1, 0], kn=1 << 22, vn=None) == mad.MAD_EINVAL
+    assert call([2, 1, 0], win=None) == mad.MAD_EINVAL                      # append without a ring
+    assert call([2, 2, 0]) == mad.MAD_EINVAL and "share" in _last_error(mad)  # two appends, one ring
+    assert call([2, 1, 0], B=0) == mad.MAD_EINVAL
+    assert call([2, 1, 0], B=65) == mad.MAD_EINVAL
+    # a full ring cannot take the appended row; with mode 1 (attend only) the same
+    # ring passes validation and the call stops at the missing split workspace
+    full = (ctypes.c_int32 * B)(32768, 30000, 30000)
+    w = mad._KVView(1 << 24, 1 << 25, 0, 32768 * 64, 32768, st, full)
+    assert call([2, 1, 0], win=w) == mad.MAD_EINVAL and "exceeds cap" in _last_error(mad)
+    assert call([1, 1, 0], win=w) == mad.MAD_EWS
