@@ -10,9 +10,9 @@ token through all 16 layers:
   * per layer, the fused draft decode attention over [memory | window ring]
     with the current token's K/V appended to the ring in the same launch;
   * when a sequence crosses a 64-token boundary, per layer the memory update
-    (mirrored projection of 4 slot rows + RoPE + append) and the four new
-    slots' write-scope attention (one launch, the four queries alias one
-    sequence's buffers).
+    (mirrored projection of 4 slot rows + RoPE + append) and then one launch
+    for the raw query and the four new slots' write scopes (five rows aliasing
+    one sequence's buffers).
 Six independent sequences are decoded round-robin so that each layer's data
 (6.3 MB, 100 MB per sequence) has left the 256 MB Infinity Cache before it is
 read again: the timed reads come from HBM.  The timed steps are captured in
@@ -190,38 +190,43 @@ class DraftModel:
             self.u = u
             self.x = [mk(1, u, self.D) for _ in range(L)]
             self.w_g = [(torch.randn(2 * Hkv * d, self.D, device=dev) * 0.02).to(bf) for _ in range(L)]
-            self.qg = [mk(u, Hq, d) for _ in range(L)]
-            self.outg = [torch.empty(u, Hq, d, device=dev, dtype=bf) for _ in range(L)]
-        self.ws = torch.zeros(max(mad.workspace_bytes(mad.MAD_OP_DECODE, u if not full_kv else 1, Hq, Hkv, d),
+            # boundary steps: one launch for the raw query (row 0) and the u new
+            # slots' write scopes (rows 1..u), all rows aliasing the sequence
+            self.qf = [mk(1 + u, Hq, d) for _ in range(L)]
+            self.knf = [self.kn[l].expand(1 + u, Hkv, d).contiguous() for l in range(L)]
+            self.vnf = [self.vn[l].expand(1 + u, Hkv, d).contiguous() for l in range(L)]
+            self.outf = [torch.empty(1 + u, Hq, d, device=dev, dtype=bf) for _ in range(L)]
+            self.lsef = [torch.empty(1 + u, Hq, device=dev, dtype=torch.float32) for _ in range(L)]
+        self.ws = torch.zeros(max(mad.workspace_bytes(mad.MAD_OP_DECODE, 1 + u if not full_kv else 1, Hq, Hkv, d),
                                   mad.workspace_bytes(mad.MAD_OP_UPDATE, u if not full_kv else 1, self.D, Hkv, d)),
                               dtype=torch.uint8, device=dev)
-        self.decode_calls = []   # (keys attended) per decode launch, for the roofline
+        self.decode_calls = []   # keys the raw query attends, per layer-step (slot-scope rows not counted)
         self.n_updates = 0
 
-    def step(self, set_idx, p, decode_hook=None):
-        """One draft step of sequence `set_idx` at raw position p through all layers."""
+    def step(self, set_idx, p):
+        """One draft step of sequence `set_idx` at raw position p through all layers.
+        A step whose pass materialises memory slots runs, per layer, the memory
+        update and then one launch for the raw query and the slots' write scopes."""
         mad, lay = self.mad, self.lay
         view = lay.decode_view(p)
         upd = None if self.full_kv else lay.update_in_pass_of(p)
+        fused = None if upd is None else lay.step_views(p)
         for l in range(self.layers):
             rk, rv = self.ring_k[set_idx][l], self.ring_v[set_idx][l]
-            mem = None if self.full_kv else mad.KV(self.mem_k[set_idx][l], self.mem_v[set_idx][l], [view.mem_len])
-            win = mad.KV(rk, rv, [view.win_len], [view.win_start])
-            if decode_hook:
-                decode_hook(True)
-            mad.draft_decode_attn(self.q[l], mem, win, self.kn[l], self.vn[l], self.out[l], self.lse[l], ws=self.ws)
-            if decode_hook:
-                decode_hook(False)
+            if upd is None:
+                mem = None if self.full_kv else mad.KV(self.mem_k[set_idx][l], self.mem_v[set_idx][l],
+                                                       [view.mem_len])
+                mad.draft_decode_attn(self.q[l], mem, mad.KV(rk, rv, [view.win_len], [view.win_start]),
+                                      self.kn[l], self.vn[l], self.out[l], self.lse[l], ws=self.ws)
+                self.decode_calls.append(view.mem_len + view.win_len + 1)
+                continue
+            mk, mv = self.mem_k[set_idx][l], self.mem_v[set_idx][l]
+            mad.memory_update(self.x[l], self.w_g[l], [upd.positions], mad.KV(mk, mv, [upd.mem_row]), ws=self.ws)
+            views, modes = fused
+            mad.draft_step_attn(self.qf[l], mad.KV(mk, mv, [v.mem_len for v in views]),
+                                mad.KV(rk, rv, [v.win_len for v in views], [v.win_start for v in views]),
+                                self.knf[l], self.vnf[l], modes, self.outf[l], self.lsef[l], ws=self.ws)
             self.decode_calls.append(view.mem_len + view.win_len + 1)
-            if upd is not None:
-                mk, mv = self.mem_k[set_idx][l], self.mem_v[set_idx][l]
-                mad.memory_update(self.x[l], self.w_g[l], [upd.positions], mad.KV(mk, mv, [upd.mem_row]),
-                                  ws=self.ws)
-                # the new slots' write scopes: u queries over one sequence's buffers
-                views = [lay.slot_scope_view(upd.first_slot + i) for i in range(self.u)]
-                mad.draft_decode_attn(self.qg[l], mad.KV(mk, mv, [v.mem_len for v in views]),
-                                      mad.KV(rk, rv, [v.win_len for v in views], [v.win_start for v in views]),
-                                      out=self.outg[l], ws=self.ws)
         if upd is not None:
             self.n_updates += 1
 
@@ -250,20 +255,14 @@ def time_graph(torch, g, reps=1):
     return e0.elapsed_time(e1) * 1e-3 / reps   # seconds per replay
 
 
-def mean_launch_seconds(torch, launches):
-    """Mean device duration of individual launches, each bracketed by HIP
-    events on the launching stream; a spin kernel keeps the stream busy while
-    the host enqueues the event/launch/event triple, so host latency stays out."""
-    evs = []
-    for fn in launches:
-        torch.cuda._sleep(200000)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        fn()
-        e1.record()
-        evs.append((e0, e1))
-    torch.cuda.synchronize()
-    return sum(a.elapsed_time(b) for a, b in evs) * 1e-3 / len(evs)
+def mean_launch_seconds(torch, launches, reps=3):
+    """Mean device time per launch: the launches are captured in one HIP graph
+    and replayed back to back between two HIP events on the replaying stream.
+    The figure includes the graph's gaps between kernels, so it bounds the
+    profiler's per-kernel duration from above."""
+    g = graph_of(torch, lambda: [fn() for fn in launches])
+    g.replay()
+    return time_graph(torch, g, reps=reps) / len(launches)
 
 
 def source_digest(*names):

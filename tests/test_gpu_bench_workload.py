@@ -4,7 +4,8 @@ bench.py times draft steps of a 16-layer draft at a 32K prefix (2048 memory
 slots + a 1024-token window per layer, 32/8 heads, head_dim 64, bf16) as a
 replayed HIP graph.  This test builds the same DraftModel (two layers, two
 sequences round-robin) and runs a schedule that crosses a 64-token boundary
-(memory update of four slots + their write-scope attention):
+(memory update of four slots, then one launch for the raw query and the
+slots' write scopes):
 
   * eager run: every decode output (all heads) and, at the boundary, every
     slot-scope output is compared with the oracle.  The oracle's key lists are
@@ -52,11 +53,11 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
             h[i, l] = dict(mk=to_np(model.mem_k[i][l][0]), mv=to_np(model.mem_v[i][l][0]),
                            rk=to_np(model.ring_k[i][l][0]), rv=to_np(model.ring_v[i][l][0]))
     q = [to_np(t[0]) for t in model.q]
+    qf = [to_np(t) for t in model.qf]
     kn = [to_np(t[0]) for t in model.kn]
     vn = [to_np(t[0]) for t in model.vn]
     x = [to_np(t[0]) for t in model.x]
     wg = [to_np(t) for t in model.w_g]
-    qg = [to_np(t) for t in model.qg]
     scale = d ** -0.5
 
     def attend(qrows, st, view, new):
@@ -75,12 +76,16 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
     for i, p in schedule:
         view = lay.decode_view(p)
         upd = lay.update_in_pass_of(p)
-        refs = [attend(q[l], h[i, l], view, (kn[l], vn[l])) for l in range(L)]
+        if upd is None:
+            refs = [attend(q[l], h[i, l], view, (kn[l], vn[l])) for l in range(L)]
+        else:   # the fused launch: row 0 is the raw query, rows 1.. the slots' scopes
+            refs = [attend(qf[l][0], h[i, l], view, (kn[l], vn[l])) for l in range(L)]
         model.step(i, p)
         torch.cuda.synchronize()
+        out, lse = (model.out, model.lse) if upd is None else (model.outf, model.lsef)
         for l in range(L):
-            check_out(to_np(model.out[l][0]), refs[l][0][0], True, f"set {i} pos {p} layer {l} out")
-            check(to_np(model.lse[l][0]), refs[l][1][0], F32_ATOL, None, f"set {i} pos {p} layer {l} lse")
+            check_out(to_np(out[l][0]), refs[l][0][0], True, f"set {i} pos {p} layer {l} out")
+            check(to_np(lse[l][0]), refs[l][1][0], F32_ATOL, None, f"set {i} pos {p} layer {l} lse")
         for l in range(L):
             st = h[i, l]
             st["rk"][:, lay.ring_row(p)] = kn[l]
@@ -93,22 +98,24 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
                 st["mv"][:, upd.mem_row + r] = _bf16(v_ref[r])
             for r in range(len(upd.positions)):
                 sview = lay.slot_scope_view(upd.first_slot + r)
-                o_ref, _ = attend(qg[l][r], st, sview, None)
-                check_out(to_np(model.outg[l][r]), o_ref[0], True, f"set {i} slot {upd.first_slot + r} layer {l}")
-    eager = [(model.out[l].clone(), model.lse[l].clone(), model.outg[l].clone()) for l in range(L)]
+                o_ref, l_ref = attend(qf[l][1 + r], st, sview, None)
+                check_out(to_np(model.outf[l][1 + r]), o_ref[0], True, f"set {i} slot {upd.first_slot + r} layer {l}")
+                check(to_np(model.lsef[l][1 + r]), l_ref[0], F32_ATOL, None, f"set {i} slot {upd.first_slot + r} lse")
+    eager = [(model.out[l].clone(), model.lse[l].clone(), model.outf[l].clone(), model.lsef[l].clone())
+             for l in range(L)]
 
     # ---- graph capture, three replays with eager work between ----
     g = bench.graph_of(torch, lambda: [model.step(i, p) for i, p in schedule])
     for rep in range(3):
         for l in range(L):   # clobber the outputs so a replay that skips a write shows
-            model.out[l].fill_(float("nan"))
-            model.lse[l].fill_(float("nan"))
-            model.outg[l].fill_(float("nan"))
+            for t in (model.out[l], model.lse[l], model.outf[l], model.lsef[l]):
+                t.fill_(float("nan"))
         scratch = torch.randn(1 << 20, device="cuda").sum()   # unrelated eager work
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         assert torch.isfinite(scratch)
         for l in range(L):
-            for a, b, what in zip((model.out[l], model.lse[l], model.outg[l]), eager[l], ("out", "lse", "outg")):
+            for a, b, what in zip((model.out[l], model.lse[l], model.outf[l], model.lsef[l]), eager[l],
+                                  ("out", "lse", "outf", "lsef")):
                 assert torch.equal(a, b), f"replay {rep} layer {l} {what} differs from the eager run"
