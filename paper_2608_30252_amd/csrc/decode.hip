@@ -36,7 +36,8 @@
 //   * the last workgroup of a unit (one arrival counter per unit, on its own
 //     256-byte line) pulls every split's partial into LDS with device-coherent
 //     direct loads in a single round trip and merges them with the
-//     log-sum-exp rule, all splits of a head in parallel lanes.
+//     log-sum-exp rule, one wave per head: all splits of the head in parallel
+//     lanes for the weights, then the features in parallel lanes.
 #include <type_traits>
 
 #include "mad_device.h"
@@ -73,15 +74,13 @@ struct DecodeCfg {
     // a 64-key tile gives every wave one head per pass: its query rows (at most
     // two) come through the scalar cache, loaded at kernel start
     static constexpr bool QS = TILE == 64 && HW <= 2;
-    // LDS: [stages | Q: the unit's query rows | P: per-wave probabilities | WN: merge weights]
+    // LDS: [stages (also the merge buffer) | Q: the unit's query rows | P: per-wave probabilities]
     static constexpr int SZ_ST = STAGES * SB;
     static constexpr int OFF_Q = SZ_ST > kMergeLds ? SZ_ST : kMergeLds;
     static constexpr int SZ_Q = (G * RB + 1023) / 1024 * 1024;
     static constexpr int OFF_P = OFF_Q + SZ_Q;
     static constexpr int SZ_P = NW * TILE * HW * 4;
-    static constexpr int OFF_WN = OFF_P + SZ_P;
-    static constexpr int SZ_WN = 1024;
-    static constexpr int SMEM = OFF_WN + SZ_WN;
+    static constexpr int SMEM = OFF_P + SZ_P;
     static_assert(TILE * RB == 8192 && 4 * LPT * 1024 == 8192, "tile = 8 KB per tensor");
     static_assert(CPR % KB == 0 && KPL % 2 == 0 && 64 % DW == 0, "shape");
     static_assert(NSUB * G * (D + 2) * 4 <= SZ_ST, "group merge buffer fits the stages");
@@ -149,12 +148,15 @@ __device__ __forceinline__ float wave_sum_b(float v) {
 
 // Merge of a unit's split partials by its last-arriving workgroup (NT threads).
 //   blk   unit block in the workspace: [o: n_splits][G][D] [ml: n_splits][G][2]
-//   lds   >= n_splits * G * (D + 2) * 4 bytes of LDS (16-byte aligned); wn: n_splits * G floats
+//   lds   >= n_splits * G * (D + 2) * 4 bytes of LDS (16-byte aligned)
+// One round trip pulls the whole block into LDS; then each wave merges whole
+// heads on its own, with no further barrier: lanes over splits for the
+// log-sum-exp weights 2^(m_s - M) (all splits of the head in parallel, at most
+// kDecodeMaxSplits / 64 per lane), then lanes over features for
+// o = sum_s w_s o_s / L, each split's weight read back from its lane.
 template <typename T, int D, int G, int NT>
-__device__ __forceinline__ void merge_splits(const float *blk, int n_splits, unsigned char *lds, float *wn, T *out,
-                                             float *lse) {
+__device__ __forceinline__ void merge_splits(const float *blk, int n_splits, unsigned char *lds, T *out, float *lse) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // ---- pull all partials into LDS in one round trip (1 KB per wave instruction) ----
     const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
     for (int off = wave * 1024; off < nbytes; off += NT * 16) {
         if (off + lane * 16 < nbytes)
@@ -162,20 +164,19 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
     }
     wait_vmcnt(0);
     __syncthreads();
-    const float *lo = reinterpret_cast<const float *>(lds);   // [n_splits][G][D]
-    const float *lml = lo + (size_t)n_splits * G * D;          // [n_splits][G][2]: max, sum
+    const float *lo = reinterpret_cast<const float *>(lds);                               // [n_splits][G][D]
+    const float2 *lml = reinterpret_cast<const float2 *>(lo + (size_t)n_splits * G * D);  // [n_splits][G]
 
-    // phase 1, one wave per head: M = max_s m_s, L = sum_s 2^(m_s - M) l_s and the
-    // split weights 2^(m_s - M) / L (all splits of a head in parallel lanes, at
-    // most kDecodeMaxSplits / 64 per lane)
     constexpr int SPL = kDecodeMaxSplits / 64;
+    constexpr int FPL = D / 64;   // features per lane
+    constexpr int SB = 8;         // splits whose rows are read together
     for (int g = wave; g < G; g += NT / 64) {
         float2 ml[SPL];
         float mloc = -INFINITY;
         #pragma unroll
         for (int i = 0; i < SPL; ++i) {
             const int sp = lane + 64 * i;
-            ml[i] = sp < n_splits ? reinterpret_cast<const float2 *>(lml)[sp * G + g] : make_float2(-INFINITY, 0.f);
+            ml[i] = sp < n_splits ? lml[sp * G + g] : make_float2(-INFINITY, 0.f);
             mloc = fmaxf(mloc, ml[i].x);
         }
         const float M = group_max_b<64>(mloc, lane);
@@ -187,54 +188,43 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
         }
         const float L = wave_sum_b(lsum);
         const float inv = L > 0.f ? 1.f / L : 0.f;
-        #pragma unroll
-        for (int i = 0; i < SPL; ++i)
-            if (lane + 64 * i < n_splits) wn[g * n_splits + lane + 64 * i] = w[i] * inv;
         if (lse && lane == 0) lse[g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
-    }
-    __syncthreads();
 
-    // phase 2: o = sum_s weight_s o_s, one 16-byte group of outputs per NQ
-    // neighbouring lanes, each lane summing every NQ-th split; the reads of a
-    // batch of MB splits are issued together (indices past the last split read
-    // the last one with weight 0)
-    constexpr int NG4 = G * D / 4;
-    constexpr int NQ = NG4 >= NT ? 1 : (NT / NG4 > 64 ? 64 : NT / NG4);
-    constexpr int MB = 16;
-    for (int grp = tid / NQ; grp < NG4; grp += NT / NQ) {
-        const int qq = tid % NQ;
-        const float *wg = wn + (grp * 4 / D) * n_splits;
-        const float4 *lo4 = reinterpret_cast<const float4 *>(lo) + grp;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int sb = qq; sb < n_splits; sb += MB * NQ) {
-            float4 o4[MB];
-            float wt[MB];
-            #pragma unroll
-            for (int i = 0; i < MB; ++i) {
-                const int sp = sb + i * NQ;
-                const int spc = sp < n_splits ? sp : n_splits - 1;
-                o4[i] = lo4[(size_t)spc * NG4];
-                wt[i] = wg[spc];
-                if (sp >= n_splits) wt[i] = 0.f;
+        float acc[FPL];
+        #pragma unroll
+        for (int f = 0; f < FPL; ++f) acc[f] = 0.f;
+        const float *og = lo + (size_t)g * D + lane * FPL;
+        #pragma unroll
+        for (int i = 0; i < SPL; ++i) {
+            const int s0 = 64 * i;
+            if (s0 >= n_splits) break;
+            const int cnt = n_splits - s0 < 64 ? n_splits - s0 : 64;
+            int j = 0;
+            for (; j + SB <= cnt; j += SB) {
+                float ov[SB][FPL], ws[SB];
+                #pragma unroll
+                for (int k = 0; k < SB; ++k) {
+                    ws[k] = read_lane(w[i], j + k);
+                    #pragma unroll
+                    for (int f = 0; f < FPL; ++f) ov[k][f] = og[(size_t)(s0 + j + k) * G * D + f];
+                }
+                #pragma unroll
+                for (int k = 0; k < SB; ++k)
+                    #pragma unroll
+                    for (int f = 0; f < FPL; ++f) acc[f] = fmaf(ws[k], ov[k][f], acc[f]);
             }
-            #pragma unroll
-            for (int i = 0; i < MB; ++i) {
-                acc.x = fmaf(wt[i], o4[i].x, acc.x);
-                acc.y = fmaf(wt[i], o4[i].y, acc.y);
-                acc.z = fmaf(wt[i], o4[i].z, acc.z);
-                acc.w = fmaf(wt[i], o4[i].w, acc.w);
+            for (; j < cnt; ++j) {
+                const float ws = read_lane(w[i], j);
+                #pragma unroll
+                for (int f = 0; f < FPL; ++f) acc[f] = fmaf(ws, og[(size_t)(s0 + j) * G * D + f], acc[f]);
             }
         }
-        acc.x = group_sum<NQ>(acc.x);
-        acc.y = group_sum<NQ>(acc.y);
-        acc.z = group_sum<NQ>(acc.z);
-        acc.w = group_sum<NQ>(acc.w);
-        if (qq == 0) {
-            if constexpr (std::is_same<T, bf16_t>::value) {
-                reinterpret_cast<uint2 *>(out)[grp] = make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
-            } else {
-                reinterpret_cast<float4 *>(out)[grp] = acc;
-            }
+        T *og_out = out + (size_t)g * D + lane * FPL;
+        if constexpr (std::is_same<T, bf16_t>::value && FPL == 2) {
+            *reinterpret_cast<uint32_t *>(og_out) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+        } else {
+            #pragma unroll
+            for (int f = 0; f < FPL; ++f) Elem<T>::store1(og_out + f, acc[f] * inv);
         }
     }
 }
@@ -574,8 +564,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     }
     __syncthreads();
     if (!s_last) return;
-    merge_splits<T, D, G, C::NT>(blk, n_splits, sStage, reinterpret_cast<float *>(smem + C::OFF_WN), out,
-                                 a.lse ? a.lse + head0 : nullptr);
+    merge_splits<T, D, G, C::NT>(blk, n_splits, sStage, out, a.lse ? a.lse + head0 : nullptr);
 }
 
 // ------------------------------------------------------------------ host ----
