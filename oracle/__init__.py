@@ -16,6 +16,12 @@ K/V materialisation:
 
 ``accept_stochastic`` wraps the rejection-sampling rule (oracle.c).
 
+``memory_prefill`` is the draft's memory-prefill attention (Sec. 3.3 prefill;
+the appendix on memory prefill): the prefill mask applies the write policy of
+decoding, so each query of the pass attends over the set ``masw_sets`` gives
+it -- a raw token its decode-time view, a slot its write scope -- and the
+attention itself is oracle_attend over that explicit key list.
+
 ``masw_sets`` holds the visible-set simulator written from the paper's set
 definitions (Sec. 3.1 and 3.2).
 
@@ -198,3 +204,40 @@ def accept_stochastic(p, q, draft, u):
     lib.oracle_accept_stochastic(B, T, V, _ptr(p, _fp), _ptr(np.ascontiguousarray(q), _fp), _ptr(dr, _ip),
                                  _ptr(u, _fp), _ptr(na, _ip), _ptr(nx, _ip))
     return na, nx
+
+
+def memory_prefill(q_raw, q_slot, mem_k, mem_v, raw_k, raw_v, P, S, W, r, u, scale, raw_idx=None, slot_idx=None):
+    """Memory-prefill attention of one sequence.
+
+    q_raw [>=P, Hq, d]; q_slot [>=M, Hq, d] (row m-1 = slot m) or None;
+    mem_k/mem_v [Hkv, >=S+M, d] (sinks in rows 0..S-1, slot m in row S+m-1);
+    raw_k/raw_v [Hkv, >=P, d] (position x in row x); M = slots materialised by
+    the prefix.  raw_idx / slot_idx restrict the queries computed (default:
+    all).  Returns dicts {p: (o [Hq, d], lse [Hq])} and {m: (o, lse)}."""
+    from .masw_sets import MaswSets
+    sets = MaswSets(S, W, r, u)
+    M = sets.slots_after(P)
+    Hq = q_raw.shape[1]
+    Hkv = mem_k.shape[0]
+    G = Hq // Hkv
+
+    def run(qrows, view):
+        mrows = list(view.sink) + [S + m - 1 for m in view.slots]
+        rrows = list(view.window)
+        o = np.zeros((Hq, qrows.shape[1]))
+        lse = np.zeros(Hq)
+        for c in range(Hkv):
+            d = mem_k.shape[-1]
+            K = np.concatenate([_f64(mem_k[c][mrows]).reshape(len(mrows), d),
+                                _f64(raw_k[c][rrows]).reshape(len(rrows), d)])
+            V = np.concatenate([_f64(mem_v[c][mrows]).reshape(len(mrows), d),
+                                _f64(raw_v[c][rrows]).reshape(len(rrows), d)])
+            o[c * G:(c + 1) * G], lse[c * G:(c + 1) * G] = attend(qrows[c * G:(c + 1) * G], K, V, scale)
+        return o, lse
+
+    raw_out = {p: run(_f64(q_raw[p]), sets.raw_view(p)) for p in (range(P) if raw_idx is None else raw_idx)}
+    slot_out = {}
+    if q_slot is not None:
+        for m in (range(1, M + 1) if slot_idx is None else slot_idx):
+            slot_out[m] = run(_f64(q_slot[m - 1]), sets.slot_scope(m))
+    return raw_out, slot_out
