@@ -9,7 +9,8 @@
  *   - the memory adaptor's update: mirrored K/V projection of new slot
  *     hidden states, RoPE at the slot's position id, append-only write Sec. 3.2
  *   - the target's (gamma+1)-query verify attention over its full KV  Sec. 2.1, 3.3
- *   - the greedy accept/reject rule                                  Sec. 2.1, 4.1
+ *   - the greedy and the stochastic accept/reject rules              Sec. 2.1, 4.1
+ *   - the draft's memory-prefill attention                          Sec. 3.3, App.
  *
  * Conventions shared by every entry point
  *   - Tensors are DEVICE memory owned by the caller, row-major; a key/value row
@@ -224,6 +225,42 @@ int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok,
  */
 int mad_accept_stochastic(const float *p, const float *q, const int32_t *draft_tok, const float *u, int B, int T,
                           int V, int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Memory-prefill attention (Sec. 3.3, prefill; the appendix on memory
+ * prefill): the draft's single masked pass over a prefix, which builds its
+ * initial compact memory.  The mask applies the write policy of decoding, so
+ * every query of the pass attends exactly what it would attend while
+ * decoding.  With s(t) = u * floor((t - S) / (u r)) for t > S, else 0 (the
+ * slots materialised once raw tokens 0..t-1 are processed; u = slots per
+ * update, 1 = one slot per boundary), for sequence b and KV head c = h / G:
+ *   raw token p < P[b]:  keys = sinks [0, min(S, p+1)), slots 1..s(p) and the
+ *                        raw tokens [max(S, p-W+1), p];
+ *   slot m <= M[b]:      keys = sinks [0, S), slots 1..m (itself included) and
+ *                        the raw tokens [max(S, b_m - W), b_m - 1], b_m = S + m r
+ *                        (its write scope);
+ * where M[b] = s(P[b]) is the number of slots the prefix materialises.  Sinks
+ * are read from mem rows 0..S-1, slot m from mem row S + m - 1, raw token x
+ * from raw row x.  Outputs and lse are as for mad_draft_decode_attn.
+ *   q_raw     device [B][q_cap][Hq][d]: row p of sequence b for p < P[b]
+ *   out_raw   device [B][q_cap][Hq][d]; lse_raw device fp32 [B][q_cap][Hq] or NULL
+ *   q_slot    device [B][slot_cap][Hq][d], row m-1 for slot m; NULL = no slot
+ *             queries (out_slot and lse_slot are then ignored)
+ *   out_slot  device [B][slot_cap][Hq][d]; lse_slot fp32 [B][slot_cap][Hq] or NULL
+ *   P         HOST int32[B], 0 <= P[b] <= q_cap
+ *   mem       linear view (start ignored): len[b] >= S + M[b] (>= P[b] when
+ *             P[b] <= S)
+ *   raw       linear view of the prefix's raw K/V (start must be NULL):
+ *             len[b] >= P[b]
+ *   S >= 0 sinks, W >= 1 window, r >= 1 slot interval, u >= 1 slots per update
+ * dtype BF16 only (the products run on the matrix cores), d in {64, 128},
+ * G in {1, 2, 4, 8}.  No workspace.  A slot count M[b] > slot_cap (with slot
+ * queries) is MAD_EINVAL.
+ */
+int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq, int Hkv, int d, int dtype,
+                            float scale, const int32_t *P, int q_cap, int slot_cap, int S, int W, int r, int u,
+                            const mad_kv_view *mem, const mad_kv_view *raw, void *out_raw, float *lse_raw,
+                            void *out_slot, float *lse_slot, void *stream);
 
 /*
  * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:

@@ -58,12 +58,14 @@ def _load_library():
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_accept_stochastic.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_draft_step_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, _u8p, vp, vp, vp, sz, vp]
+    lib.mad_memory_prefill_attn.argtypes = [vp, vp, i, i, i, i, i, f, _i32p, i, i, i, i, i, i, kvp, kvp,
+                                            vp, vp, vp, vp, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
-               "mad_accept_stochastic", "mad_draft_step_attn"):
+               "mad_accept_stochastic", "mad_draft_step_attn", "mad_memory_prefill_attn"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -310,3 +312,42 @@ def accept_stochastic(p: torch.Tensor, q: Optional[torch.Tensor], draft_tok: Opt
                                    _ptr(next_tok), _ptr(w), w.numel(), _stream(dev))
     _check(rc)
     return n_accept, next_tok
+
+
+def slots_after(t: int, S: int, r: int, u: int = 1) -> int:
+    """Slots materialised once raw tokens 0..t-1 are processed (u slots per update)."""
+    return 0 if t <= S else (t - S) // (r * u) * u
+
+
+def memory_prefill_attn(q_raw: torch.Tensor, q_slot: Optional[torch.Tensor], mem: KV, raw: KV, P: Sequence[int],
+                        S: int, W: int, r: int, u: int = 1, out_raw: Optional[torch.Tensor] = None,
+                        lse_raw: Optional[torch.Tensor] = None, out_slot: Optional[torch.Tensor] = None,
+                        lse_slot: Optional[torch.Tensor] = None, scale: Optional[float] = None):
+    """The draft's memory-prefill attention over a prefix of P[b] raw tokens.
+
+    q_raw [B, q_cap, Hq, d]; q_slot [B, slot_cap, Hq, d] (row m-1 = slot m) or None;
+    mem: sinks then slots (rows 0..S-1, S+m-1); raw: the prefix's K/V (row x = position x).
+    Returns (out_raw, lse_raw, out_slot, lse_slot); the slot outputs are None without q_slot."""
+    B, q_cap, Hq, d = q_raw.shape
+    Hkv = mem.k.shape[1]
+    slot_cap = q_slot.shape[1] if q_slot is not None else 0
+    if out_raw is None:
+        out_raw = torch.empty_like(q_raw)
+    if lse_raw is None:
+        lse_raw = torch.empty((B, q_cap, Hq), dtype=torch.float32, device=q_raw.device)
+    if q_slot is not None:
+        if out_slot is None:
+            out_slot = torch.empty_like(q_slot)
+        if lse_slot is None:
+            lse_slot = torch.empty((B, slot_cap, Hq), dtype=torch.float32, device=q_raw.device)
+    if scale is None:
+        scale = d ** -0.5
+    mv, rv = mem.view(B), raw.view(B)
+    plen = _host_i32(P, B)
+    rc = _load_library().mad_memory_prefill_attn(
+        _ptr(q_raw), _ptr(q_slot), B, Hq, Hkv, d, _dtype_code(q_raw), float(scale), plen, q_cap, slot_cap,
+        S, W, r, u, ctypes.byref(mv), ctypes.byref(rv), _ptr(out_raw), _ptr(lse_raw),
+        _ptr(out_slot) if q_slot is not None else None, _ptr(lse_slot) if q_slot is not None else None,
+        _stream(q_raw.device))
+    _check(rc)
+    return out_raw, lse_raw, (out_slot if q_slot is not None else None), (lse_slot if q_slot is not None else None)

@@ -320,6 +320,77 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
     return hip_status(mad::launch_verify(a, (hipStream_t)stream), "verify launch");
 }
 
+int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq, int Hkv, int d, int dtype,
+                            float scale, const int32_t *P, int q_cap, int slot_cap, int S, int W, int r, int u,
+                            const mad_kv_view *mem, const mad_kv_view *raw, void *out_raw, float *lse_raw,
+                            void *out_slot, float *lse_slot, void *stream) {
+    int rc = check_heads(B, Hq, Hkv, d, dtype);
+    if (rc) return rc;
+    if (dtype != MAD_BF16) return fail(MAD_ENOTSUP, "memory-prefill attention runs in bf16 only");
+    const int G = Hq / Hkv;
+    if (G > 8) return fail(MAD_ENOTSUP, "group size %d not supported by the prefill (1, 2, 4, 8)", G);
+    if (!q_raw || !out_raw || !P || !mem || !raw) return fail(MAD_EINVAL, "null q_raw, out_raw, P, mem or raw");
+    if (q_slot && !out_slot) return fail(MAD_EINVAL, "q_slot given without out_slot");
+    if (!aligned16(q_raw) || !aligned16(out_raw) || (q_slot && (!aligned16(q_slot) || !aligned16(out_slot))))
+        return fail(MAD_EINVAL, "q/out not 16-byte aligned");
+    if (!(scale > 0.f) || scale != scale) return fail(MAD_EINVAL, "scale must be positive");
+    if (S < 0 || W < 1 || r < 1 || u < 1) return fail(MAD_EINVAL, "S=%d W=%d r=%d u=%d", S, W, r, u);
+    if (q_cap < 1 || (q_slot && slot_cap < 1)) return fail(MAD_EINVAL, "q_cap=%d slot_cap=%d", q_cap, slot_cap);
+    if (raw->start) return fail(MAD_EINVAL, "raw: the prefix's K/V are linear (start must be NULL)");
+    if ((rc = check_view(mem, "mem", B, Hkv, d, dtype, false, nullptr))) return rc;
+    if ((rc = check_view(raw, "raw", B, Hkv, d, dtype, false, nullptr))) return rc;
+    if ((size_t)r * (size_t)u > 0x3fffffff) return fail(MAD_EINVAL, "r*u too large");
+    int Mtot[MAD_MAX_BATCH];
+    int P_max = 0, M_max = 0;
+    for (int b = 0; b < B; ++b) {
+        if (P[b] < 0 || P[b] > q_cap) return fail(MAD_EINVAL, "P[%d]=%d outside [0, q_cap=%d]", b, P[b], q_cap);
+        Mtot[b] = P[b] <= S ? 0 : (P[b] - S) / (r * u) * u;
+        const int need_mem = P[b] <= S ? P[b] : S + Mtot[b];
+        if (mem->len[b] < need_mem)
+            return fail(MAD_EINVAL, "mem: len[%d]=%d < %d rows (sinks + slots of the prefix)", b, mem->len[b], need_mem);
+        if (raw->len[b] < P[b]) return fail(MAD_EINVAL, "raw: len[%d]=%d < P=%d", b, raw->len[b], P[b]);
+        if (q_slot && Mtot[b] > slot_cap)
+            return fail(MAD_EINVAL, "sequence %d has %d slots > slot_cap=%d", b, Mtot[b], slot_cap);
+        P_max = P[b] > P_max ? P[b] : P_max;
+        M_max = Mtot[b] > M_max ? Mtot[b] : M_max;
+    }
+    if (P_max == 0) return ok();
+    const int QT = mad::prefill_tokens_per_block(d, G);
+    mad::PrefillArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q_raw = q_raw;
+    a.q_slot = q_slot;
+    a.o_raw = out_raw;
+    a.o_slot = out_slot;
+    a.lse_raw = lse_raw;
+    a.lse_slot = q_slot ? lse_slot : nullptr;
+    a.mk = mem->k;
+    a.mv = mem->v;
+    a.m_seq = mem->seq_stride;
+    a.m_head = mem->head_stride;
+    a.rk = raw->k;
+    a.rv = raw->v;
+    a.r_seq = raw->seq_stride;
+    a.r_head = raw->head_stride;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.q_cap = q_cap;
+    a.slot_cap = q_slot ? slot_cap : 0;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.units = B * Hkv;
+    a.nrb = (P_max + QT - 1) / QT;
+    a.nsb = q_slot ? (M_max + QT - 1) / QT : 0;
+    a.S = S;
+    a.W = W;
+    a.r = r;
+    a.u = u;
+    for (int b = 0; b < B; ++b) {
+        a.P[b] = P[b];
+        a.Mtot[b] = Mtot[b];
+    }
+    return hip_status(mad::launch_prefill(a, d, G, (hipStream_t)stream), "memory prefill launch");
+}
+
 int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, int B, int T, int V,
                       int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
     if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);

@@ -112,6 +112,24 @@ struct VerifyArgs {
     int len[kMaxB];
 };
 
+// --------------------------------------------------------------- prefill ----
+struct PrefillArgs {
+    const void *q_raw, *q_slot;
+    void *o_raw, *o_slot;
+    float *lse_raw, *lse_slot;
+    const void *mk, *mv;  // memory segment: sinks, then slots
+    int64_t m_seq, m_head;
+    const void *rk, *rv;  // the prefix's raw K/V, position x in row x
+    int64_t r_seq, r_head;
+    float scale_log2;
+    int q_cap, slot_cap, Hq, Hkv, units, nrb, nsb;
+    int S, W, r, u;
+    int P[kMaxB], Mtot[kMaxB];
+};
+
+int prefill_tokens_per_block(int d, int G);
+hipError_t launch_prefill(const PrefillArgs &a, int d, int G, hipStream_t st);
+
 struct VerifyPlan {
     int units, n_splits, chunk;
 };

@@ -1,0 +1,350 @@
+// prefill.hip -- memory-prefill attention: the draft's one masked pass over a
+// prefix that builds its initial compact memory (Sec. 3.3 prefill; the
+// appendix on memory prefill).
+//
+// The prefill mask applies the same write policy as decoding, so every query
+// of the pass attends exactly the set it would attend during decoding:
+//   raw token at position p : sinks [0, min(S, p+1)), the slots materialised
+//                             in passes of earlier tokens (1 .. slots_after(p)),
+//                             and the window [max(S, p-W+1), p];
+//   memory slot g_m         : the sinks, slots 1..m (itself included) and the
+//                             W raw tokens before its position id b_m = S + m r:
+//                             [max(S, b_m - W), b_m - 1].
+// Keys come from two places: the memory segment (sinks in rows 0..S-1, slot m
+// in row S + m - 1) and the prefix's raw K/V (position x in row x).  For every
+// query the visible keys are one prefix of the memory segment, [0, mem_hi),
+// and one interval of raw rows, [raw_lo, raw_hi).
+//
+// Both products run on the matrix cores (v_mfma_f32_16x16x32_bf16, fp32
+// accumulation).  A workgroup of four waves owns one (sequence, KV head) unit
+// and a block of query tokens; its rows are (token, query head of the GQA
+// group) pairs in 16-token blocks, each wave holding NB of them with their
+// query fragments in registers for the whole pass.  Keys stream in 64-key
+// tiles through two LDS stages, loaded into registers one tile ahead:
+//   * K rows are stored with their 16-byte chunks XOR-swizzled so the A
+//     operand reads of S^T = K Q^T are conflict-free; the A rows are permuted
+//     so that each lane's S^T accumulators hold the 8 consecutive keys that
+//     the PV product's B operand needs (no shuffle of probabilities);
+//   * V is written transposed into LDS ([feature][key], 16-byte key chunks
+//     swizzled by feature), so the A operand of O^T = V^T P^T is one 16-byte
+//     read of 8 consecutive keys;
+//   * online softmax per query row (16 scores per lane per tile, two
+//     cross-lane steps); one barrier per tile.
+// Query blocks of every unit are dealt round-robin over the units (with a
+// multiple of 8 units all blocks of one KV head share an XCD and its L2), the
+// heaviest blocks first.
+#include "mad_device.h"
+#include "mad_internal.h"
+
+namespace mad {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
+typedef __attribute__((ext_vector_type(4))) float f32x4_v;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
+
+template <int D>
+struct PrefillCfg {
+    static constexpr int NB = D == 64 ? 4 : 2;        // 16-row blocks per wave
+    static constexpr int KT = 64;                      // keys per tile
+    static constexpr int RB = D * 2;                   // bytes per K row
+    static constexpr int CPR = RB / 16;                // 16-byte chunks per K row
+    static constexpr int KTILE = KT * RB;              // K tile bytes
+    static constexpr int VROW = KT * 2;                // bytes per V^T row (one feature, 64 keys)
+    static constexpr int STAGE = 2 * KTILE;            // K tile + V^T tile (same size)
+    static constexpr int SMEM = 2 * STAGE;
+    static constexpr int KCH = KT * CPR / 256;         // K chunks per thread per tile
+    static constexpr int VCH = KT * (D / 8) / 256;     // V chunks per thread per tile
+};
+
+// swizzle of K row k's 16-byte chunks: distinct for the 8 rows one group of
+// eight lanes reads (k mod 4 and bit 3 of k vary across them)
+__device__ __forceinline__ int k_swz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+
+__device__ __forceinline__ float prefill_row_max(float v) {
+    // lanes l, l^16, l^32, l^48 hold the same query row
+    v = fmaxf(v, xor_lane<16>(v));
+    v = fmaxf(v, xor_lane<32>(v));
+    return v;
+}
+__device__ __forceinline__ float prefill_row_sum(float v) {
+    v += xor_lane<16>(v);
+    v += xor_lane<32>(v);
+    return v;
+}
+
+__device__ __forceinline__ int prefill_slots_after(int t, int S, int ru, int u) {
+    return t <= S ? 0 : (t - S) / ru * u;
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const PrefillArgs a) {
+    using C = PrefillCfg<D>;
+    constexpr int NB = C::NB, KST = D / 32, DB = D / 16;
+    constexpr int TBW = 4 * NB / G;   // 16-token blocks per workgroup
+    constexpr int QT = 16 * TBW;      // query tokens per workgroup
+    static_assert(4 * NB % G == 0, "row blocks cover whole token blocks");
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lr = lane & 15, lg = lane >> 4;
+    const int unit = blockIdx.x % a.units;
+    const int qb = a.nrb + a.nsb - 1 - (int)(blockIdx.x / a.units);   // slot blocks, then raw blocks, late first
+    const int b = unit / a.Hkv, c = unit - b * a.Hkv;
+    const bool slot_kind = qb >= a.nrb;
+    const int S = a.S, W = a.W, r = a.r, u = a.u, ru = a.r * a.u;
+    const int nq = slot_kind ? a.Mtot[b] : a.P[b];
+    const int q0 = (slot_kind ? qb - a.nrb : qb) * QT;   // first token: raw position, or slot index - 1
+    if (q0 >= nq) return;                                 // the whole workgroup: no barrier crossed
+    const int qlast = min(nq, q0 + QT) - 1;
+
+    // ---- the workgroup's key ranges: the union of its rows' ranges ----
+    int mem_hi, raw_lo, raw_hi;
+    if (!slot_kind) {
+        mem_hi = qlast < S ? qlast + 1 : S + prefill_slots_after(qlast, S, ru, u);
+        raw_lo = max(S, q0 - W + 1);
+        raw_hi = qlast + 1;
+    } else {
+        mem_hi = S + qlast + 1;
+        raw_lo = max(S, S + (q0 + 1) * r - W);
+        raw_hi = S + (qlast + 1) * r;
+    }
+    if (raw_hi < raw_lo) raw_hi = raw_lo;
+    const int n_mem_t = (mem_hi + C::KT - 1) / C::KT;
+    const int nt = n_mem_t + (raw_hi - raw_lo + C::KT - 1) / C::KT;
+
+    const bf16_t *mk = reinterpret_cast<const bf16_t *>(a.mk) + b * a.m_seq + c * a.m_head;
+    const bf16_t *mv = reinterpret_cast<const bf16_t *>(a.mv) + b * a.m_seq + c * a.m_head;
+    const bf16_t *rk = reinterpret_cast<const bf16_t *>(a.rk) + b * a.r_seq + c * a.r_head;
+    const bf16_t *rv = reinterpret_cast<const bf16_t *>(a.rv) + b * a.r_seq + c * a.r_head;
+    const bf16_t *qbase = reinterpret_cast<const bf16_t *>(slot_kind ? a.q_slot : a.q_raw) +
+                          (size_t)b * (slot_kind ? a.slot_cap : a.q_cap) * a.Hq * D;
+
+    // ---- this lane's rows: query fragments and visible ranges ----
+    bf16x8_v qf[NB][KST];
+    int m_lim[NB], r_lo[NB], r_hi[NB];
+    #pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int j = wave + 4 * i, g = j % G, tb = j / G;
+        const int tok = q0 + tb * 16 + lr;
+        if (tok <= qlast) {
+            const bf16_t *qrow = qbase + ((size_t)tok * a.Hq + c * G + g) * D;
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) qf[i][ks] = *reinterpret_cast<const bf16x8_v *>(qrow + ks * 32 + 8 * lg);
+            if (!slot_kind) {
+                m_lim[i] = tok < S ? tok + 1 : S + prefill_slots_after(tok, S, ru, u);
+                r_lo[i] = max(S, tok - W + 1);
+                r_hi[i] = tok < S ? r_lo[i] : tok + 1;
+            } else {
+                const int bm = S + (tok + 1) * r;
+                m_lim[i] = S + tok + 1;
+                r_lo[i] = max(S, bm - W);
+                r_hi[i] = bm;
+            }
+        } else {
+            #pragma unroll
+            for (int ks = 0; ks < KST; ++ks) qf[i][ks] = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
+            m_lim[i] = 0;
+            r_lo[i] = r_hi[i] = 0;
+        }
+    }
+
+    // ---- tile loader: registers one tile ahead, then LDS ----
+    uint4 kreg[C::KCH], vreg[C::VCH];
+    auto tile_base = [&](int t, bool &is_mem, int &end) -> int {
+        is_mem = t < n_mem_t;
+        if (is_mem) {
+            end = mem_hi;
+            return t * C::KT;
+        }
+        end = raw_hi;
+        return raw_lo + (t - n_mem_t) * C::KT;
+    };
+    auto load_regs = [&](int t) {
+        bool is_mem;
+        int end;
+        const int base = tile_base(t, is_mem, end);
+        const bf16_t *ks = is_mem ? mk : rk, *vs = is_mem ? mv : rv;
+        #pragma unroll
+        for (int i = 0; i < C::KCH; ++i) {
+            const int idx = tid + 256 * i, row = idx / C::CPR, ch = idx % C::CPR;
+            const int key = min(base + row, end - 1);   // rows past the range load a valid row (masked)
+            kreg[i] = *reinterpret_cast<const uint4 *>(ks + (size_t)key * D + ch * 8);
+        }
+        #pragma unroll
+        for (int i = 0; i < C::VCH; ++i) {
+            const int idx = tid + 256 * i, row = idx % C::KT, ch = idx / C::KT;
+            const int key = min(base + row, end - 1);
+            vreg[i] = *reinterpret_cast<const uint4 *>(vs + (size_t)key * D + ch * 8);
+        }
+    };
+    auto store_lds = [&](int stage) {
+        unsigned char *sk = smem + stage * C::STAGE, *sv = sk + C::KTILE;
+        #pragma unroll
+        for (int i = 0; i < C::KCH; ++i) {
+            const int idx = tid + 256 * i, row = idx / C::CPR, ch = idx % C::CPR;
+            *reinterpret_cast<uint4 *>(sk + row * C::RB + ((ch ^ k_swz(row)) << 4)) = kreg[i];
+        }
+        #pragma unroll
+        for (int i = 0; i < C::VCH; ++i) {
+            const int idx = tid + 256 * i, row = idx % C::KT, ch = idx / C::KT;
+            const uint32_t w[4] = {vreg[i].x, vreg[i].y, vreg[i].z, vreg[i].w};
+            // feature ch*8 + e, key `row`: V^T row (ch*8 + e), key chunk row/8 swizzled by e
+            #pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint16_t h = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
+                *reinterpret_cast<uint16_t *>(sv + (ch * 8 + e) * C::VROW + ((((row >> 3) ^ e)) << 4) + (row & 7) * 2) = h;
+            }
+        }
+    };
+
+    f32x4_v o[DB][NB];
+    float m_run[NB], l_run[NB];
+    #pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        m_run[i] = -INFINITY;
+        l_run[i] = 0.f;
+        #pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][i] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+    }
+
+    auto compute = [&](int t, int stage) {
+        const unsigned char *sk = smem + stage * C::STAGE, *sv = sk + C::KTILE;
+        bool is_mem;
+        int end;
+        const int base = tile_base(t, is_mem, end);
+        // S^T = K Q^T for the tile's 64 keys: pair h holds keys 32h .. 32h+31;
+        // A row m of block blk of pair h is key 32h + 8(m/4) + 4 blk + m%4, so
+        // accumulator element e&3 of block e>>2 in lane group lg is key 32h + 8 lg + e
+        f32x4_v sacc[2][2][NB];
+        #pragma unroll
+        for (int h = 0; h < 2; ++h)
+            #pragma unroll
+            for (int blk = 0; blk < 2; ++blk) {
+                const int kr = 32 * h + 8 * (lr >> 2) + 4 * blk + (lr & 3);
+                bf16x8_v kf[KST];
+                #pragma unroll
+                for (int ks = 0; ks < KST; ++ks)
+                    kf[ks] = *reinterpret_cast<const bf16x8_v *>(sk + kr * C::RB + (((4 * ks + lg) ^ k_swz(kr)) << 4));
+                #pragma unroll
+                for (int i = 0; i < NB; ++i) {
+                    sacc[h][blk][i] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+                    #pragma unroll
+                    for (int ks = 0; ks < KST; ++ks)
+                        sacc[h][blk][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks], qf[i][ks], sacc[h][blk][i], 0, 0, 0);
+                }
+            }
+        // online softmax per row block; probabilities become the B operand of PV
+        bf16x8_v pf[NB][2];
+        #pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int lo = is_mem ? 0 : r_lo[i];
+            const int hi = min(end, is_mem ? m_lim[i] : r_hi[i]);
+            float sv16[2][8];
+            float mt = -INFINITY;
+            #pragma unroll
+            for (int h = 0; h < 2; ++h)
+                #pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int key = base + 32 * h + 8 * lg + e;
+                    const bool ok = key >= lo && key < hi;
+                    sv16[h][e] = ok ? sacc[h][e >> 2][i][e & 3] * a.scale_log2 : -INFINITY;
+                    mt = fmaxf(mt, sv16[h][e]);
+                }
+            mt = prefill_row_max(mt);
+            const float mn = fmaxf(m_run[i], mt);
+            const float ms = (mn == -INFINITY) ? 0.f : mn;
+            const float alpha = __builtin_amdgcn_exp2f(m_run[i] - ms);
+            m_run[i] = mn;
+            float ps = 0.f;
+            #pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                uint32_t pk[4];
+                #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float p0 = __builtin_amdgcn_exp2f(sv16[h][2 * e] - ms);
+                    const float p1 = __builtin_amdgcn_exp2f(sv16[h][2 * e + 1] - ms);
+                    ps += p0 + p1;
+                    pk[e] = pack_bf16x2(p0, p1);
+                }
+                pf[i][h] = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
+            }
+            l_run[i] = fmaf(l_run[i], alpha, ps);
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) o[db][i] *= alpha;
+        }
+        // O^T += V^T P^T: A = V^T rows (features db*16 + lr), keys 32h + 8 lg .. +7
+        #pragma unroll
+        for (int h = 0; h < 2; ++h)
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int f = db * 16 + lr;
+                const bf16x8_v vf = *reinterpret_cast<const bf16x8_v *>(sv + f * C::VROW + (((4 * h + lg) ^ (f & 7)) << 4));
+                #pragma unroll
+                for (int i = 0; i < NB; ++i) o[db][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i][h], o[db][i], 0, 0, 0);
+            }
+    };
+
+    load_regs(0);
+    store_lds(0);
+    __syncthreads();
+    for (int t = 0; t < nt; ++t) {
+        if (t + 1 < nt) load_regs(t + 1);
+        compute(t, t & 1);
+        if (t + 1 < nt) store_lds((t + 1) & 1);
+        __syncthreads();
+    }
+
+    // ---- normalise and store: lane (lr, lg) holds features db*16 + 4 lg .. +3 of row lr ----
+    bf16_t *obase = reinterpret_cast<bf16_t *>(slot_kind ? a.o_slot : a.o_raw) +
+                    (size_t)b * (slot_kind ? a.slot_cap : a.q_cap) * a.Hq * D;
+    float *lbase = slot_kind ? a.lse_slot : a.lse_raw;
+    #pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int j = wave + 4 * i, g = j % G, tb = j / G;
+        const int tok = q0 + tb * 16 + lr;
+        const float lt = prefill_row_sum(l_run[i]);
+        if (tok > qlast) continue;
+        const float inv = lt > 0.f ? 1.f / lt : 0.f;
+        const size_t head = (size_t)tok * a.Hq + c * G + g;
+        #pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const f32x4_v v = o[db][i];
+            *reinterpret_cast<uint2 *>(obase + head * D + db * 16 + 4 * lg) =
+                make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+        }
+        if (lbase && lg == 0)
+            lbase[(size_t)b * (slot_kind ? a.slot_cap : a.q_cap) * a.Hq + head] =
+                lt > 0.f ? (m_run[i] + log2f(lt)) * kLn2 : -INFINITY;
+    }
+}
+
+// ------------------------------------------------------------------ host ----
+
+int prefill_tokens_per_block(int d, int G) { return 16 * 4 * (d == 64 ? 4 : 2) / G; }
+
+template <int D, int G>
+static hipError_t launch_t(const PrefillArgs &a, hipStream_t st) {
+    using C = PrefillCfg<D>;
+    dim3 grid((unsigned)(a.units * (a.nrb + a.nsb))), block(256);
+    hipLaunchKernelGGL((prefill_kernel<D, G>), grid, block, C::SMEM, st, a);
+    return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_g(const PrefillArgs &a, int G, hipStream_t st) {
+    switch (G) {
+        case 1: return launch_t<D, 1>(a, st);
+        case 2: return launch_t<D, 2>(a, st);
+        case 4: return launch_t<D, 4>(a, st);
+        case 8: return launch_t<D, 8>(a, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill(const PrefillArgs &a, int d, int G, hipStream_t st) {
+    if (d == 64) return launch_g<64>(a, G, st);
+    if (d == 128) return launch_g<128>(a, G, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace mad

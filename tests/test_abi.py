@@ -191,3 +191,44 @@ def test_step_attn_validation(mad):
     w = mad._KVView(1 << 24, 1 << 25, 0, 32768 * 64, 32768, st, full)
     assert call([2, 1, 0], win=w) == mad.MAD_EINVAL and "exceeds cap" in _last_error(mad)
     assert call([1, 1, 0], win=w) == mad.MAD_EWS
+
+
+def test_prefill_validation(mad):
+    """mad_memory_prefill_attn rejects bad arguments before anything is launched."""
+    lib = mad._load_library()
+    vp = ctypes.c_void_p
+    P = (ctypes.c_int32 * 2)(1000, 777)
+    mlen = (ctypes.c_int32 * 2)(60, 48)        # S + slots: 0 + 4 * floor(P / 64)
+    rlen = (ctypes.c_int32 * 2)(1000, 777)
+
+    def call(q_raw=1 << 20, q_slot=1 << 21, B=2, Hq=32, Hkv=8, d=64, dtype=None, scale=0.125, P=P,
+             q_cap=1005, slot_cap=64, S=0, W=128, r=16, u=4, mlen=mlen, rlen=rlen, rstart=None, out_raw=1 << 22,
+             out_slot=1 << 23):
+        mem = mad._KVView(1 << 24, 1 << 25, 8 * 300 * 64, 300 * 64, 300, None, mlen)
+        raw = mad._KVView(1 << 26, 1 << 27, 8 * 1024 * 64, 1024 * 64, 1024, rstart, rlen)
+        return lib.mad_memory_prefill_attn(vp(q_raw) if q_raw else None, vp(q_slot) if q_slot else None, B, Hq,
+                                           Hkv, d, mad.MAD_BF16 if dtype is None else dtype, scale, P, q_cap,
+                                           slot_cap, S, W, r, u, ctypes.byref(mem), ctypes.byref(raw),
+                                           vp(out_raw) if out_raw else None, None,
+                                           vp(out_slot) if out_slot else None, None, None)
+    assert call(dtype=mad.MAD_F32) == mad.MAD_ENOTSUP
+    assert call(Hq=128) == mad.MAD_ENOTSUP                 # group 16
+    assert call(d=96) == mad.MAD_ENOTSUP
+    assert call(q_raw=0) == mad.MAD_EINVAL
+    assert call(out_slot=0) == mad.MAD_EINVAL              # slot queries without an output
+    assert call(q_raw=(1 << 20) + 8) == mad.MAD_EINVAL     # unaligned
+    assert call(W=0) == mad.MAD_EINVAL and call(r=0) == mad.MAD_EINVAL and call(u=0) == mad.MAD_EINVAL
+    assert call(S=-1) == mad.MAD_EINVAL
+    assert call(q_cap=999) == mad.MAD_EINVAL and "q_cap" in _last_error(mad)
+    assert call(slot_cap=59) == mad.MAD_EINVAL and "slot_cap" in _last_error(mad)
+    short = (ctypes.c_int32 * 2)(59, 48)
+    assert call(mlen=short) == mad.MAD_EINVAL and "mem" in _last_error(mad)
+    rshort = (ctypes.c_int32 * 2)(1000, 776)
+    assert call(rlen=rshort) == mad.MAD_EINVAL and "raw" in _last_error(mad)
+    st = (ctypes.c_int32 * 2)(0, 0)
+    assert call(rstart=st) == mad.MAD_EINVAL and "linear" in _last_error(mad)
+    assert call(scale=0.0) == mad.MAD_EINVAL
+    assert call(B=0) == mad.MAD_EINVAL
+    # nothing to do: every prefix empty
+    zero = (ctypes.c_int32 * 2)(0, 0)
+    assert call(P=zero) == mad.MAD_OK
