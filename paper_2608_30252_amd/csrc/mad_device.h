@@ -29,6 +29,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+// The same rounding (nearest even) by the hardware conversion, one instruction
+// for two values; for finite inputs it equals pack_bf16x2.
+typedef __bf16 bf16x2_cvt_v __attribute__((ext_vector_type(2)));
+typedef float f32x2_cvt_v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_cvt_v{lo, hi}), bf16x2_cvt_v));
+}
+
 // Element type traits: T = float or bf16_t; a 16-byte vector holds VEC elements.
 template <typename T> struct Elem;
 template <> struct Elem<float> {

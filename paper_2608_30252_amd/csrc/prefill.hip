@@ -44,7 +44,6 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
 
 template <int D>
 struct PrefillCfg {
-    static constexpr int NB = D == 64 ? 4 : 2;        // 16-row blocks per wave
     static constexpr int KT = 64;                      // keys per tile
     static constexpr int RB = D * 2;                   // bytes per K row
     static constexpr int CPR = RB / 16;                // 16-byte chunks per K row
@@ -76,10 +75,10 @@ __device__ __forceinline__ int prefill_slots_after(int t, int S, int ru, int u) 
     return t <= S ? 0 : (t - S) / ru * u;
 }
 
-template <int D, int G>
-__global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const PrefillArgs a) {
+template <int D, int G, int NB>
+__global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const PrefillArgs a) {
     using C = PrefillCfg<D>;
-    constexpr int NB = C::NB, KST = D / 32, DB = D / 16;
+    constexpr int KST = D / 32, DB = D / 16;
     constexpr int TBW = 4 * NB / G;   // 16-token blocks per workgroup
     constexpr int QT = 16 * TBW;      // query tokens per workgroup
     static_assert(4 * NB % G == 0, "row blocks cover whole token blocks");
@@ -233,12 +232,17 @@ __global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const Pre
                         sacc[h][blk][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks], qf[i][ks], sacc[h][blk][i], 0, 0, 0);
                 }
             }
-        // online softmax per row block; probabilities become the B operand of PV
+        // online softmax per row block; probabilities become the B operand of PV.
+        // The running max is kept on unscaled scores (the scale is positive);
+        // p = 2^(s c - m c) is one fma into the exponential.  A tile inside
+        // every row's visible range of this wave skips the masks.
         bf16x8_v pf[NB][2];
+        const float cs = a.scale_log2;
         #pragma unroll
         for (int i = 0; i < NB; ++i) {
             const int lo = is_mem ? 0 : r_lo[i];
             const int hi = min(end, is_mem ? m_lim[i] : r_hi[i]);
+            const bool full = __all(base >= lo && base + C::KT <= hi);
             float sv16[2][8];
             float mt = -INFINITY;
             #pragma unroll
@@ -246,14 +250,14 @@ __global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const Pre
                 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int key = base + 32 * h + 8 * lg + e;
-                    const bool ok = key >= lo && key < hi;
-                    sv16[h][e] = ok ? sacc[h][e >> 2][i][e & 3] * a.scale_log2 : -INFINITY;
+                    const float sc = sacc[h][e >> 2][i][e & 3];
+                    sv16[h][e] = (full || (key >= lo && key < hi)) ? sc : -INFINITY;
                     mt = fmaxf(mt, sv16[h][e]);
                 }
             mt = prefill_row_max(mt);
             const float mn = fmaxf(m_run[i], mt);
-            const float ms = (mn == -INFINITY) ? 0.f : mn;
-            const float alpha = __builtin_amdgcn_exp2f(m_run[i] - ms);
+            const float ms = (mn == -INFINITY) ? 0.f : mn * cs;
+            const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run[i], cs, -ms));
             m_run[i] = mn;
             float ps = 0.f;
             #pragma unroll
@@ -261,10 +265,10 @@ __global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const Pre
                 uint32_t pk[4];
                 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = __builtin_amdgcn_exp2f(sv16[h][2 * e] - ms);
-                    const float p1 = __builtin_amdgcn_exp2f(sv16[h][2 * e + 1] - ms);
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(sv16[h][2 * e], cs, -ms));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(sv16[h][2 * e + 1], cs, -ms));
                     ps += p0 + p1;
-                    pk[e] = pack_bf16x2(p0, p1);
+                    pk[e] = cvt_pk_bf16(p0, p1);
                 }
                 pf[i][h] = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
             }
@@ -310,23 +314,30 @@ __global__ __launch_bounds__(256, D == 64 ? 1 : 2) void prefill_kernel(const Pre
         for (int db = 0; db < DB; ++db) {
             const f32x4_v v = o[db][i];
             *reinterpret_cast<uint2 *>(obase + head * D + db * 16 + 4 * lg) =
-                make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+                make_uint2(cvt_pk_bf16(v[0] * inv, v[1] * inv), cvt_pk_bf16(v[2] * inv, v[3] * inv));
         }
         if (lbase && lg == 0)
             lbase[(size_t)b * (slot_kind ? a.slot_cap : a.q_cap) * a.Hq + head] =
-                lt > 0.f ? (m_run[i] + log2f(lt)) * kLn2 : -INFINITY;
+                lt > 0.f ? (m_run[i] * a.scale_log2 + log2f(lt)) * kLn2 : -INFINITY;
     }
 }
 
 // ------------------------------------------------------------------ host ----
 
-int prefill_tokens_per_block(int d, int G) { return 16 * 4 * (d == 64 ? 4 : 2) / G; }
+#ifndef MAD_PREFILL_NB64
+#define MAD_PREFILL_NB64 2
+#endif
+// 16-row blocks per wave: 2 (two workgroups per CU) unless tuned otherwise
+static constexpr int prefill_nb(int d) { return d == 64 ? MAD_PREFILL_NB64 : 2; }
+
+int prefill_tokens_per_block(int d, int G) { return 16 * 4 * prefill_nb(d) / G; }
 
 template <int D, int G>
 static hipError_t launch_t(const PrefillArgs &a, hipStream_t st) {
     using C = PrefillCfg<D>;
+    constexpr int NB = prefill_nb(D);
     dim3 grid((unsigned)(a.units * (a.nrb + a.nsb))), block(256);
-    hipLaunchKernelGGL((prefill_kernel<D, G>), grid, block, C::SMEM, st, a);
+    hipLaunchKernelGGL((prefill_kernel<D, G, NB>), grid, block, C::SMEM, st, a);
     return hipGetLastError();
 }
 
