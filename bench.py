@@ -25,6 +25,9 @@ Reported in the same run (sub-objects of the JSON line):
                  layers at a 32768-token prefix
   accept         greedy accept on [B, 5, 128256] fp32 logits, and the stochastic
                  accept/reject rule on probabilities with caller uniforms
+  memory_prefill the draft's masked prefill attention over a 32K prefix (32768
+                 raw tokens + 2048 slots, 32/8 heads, d 64 and d 128), TFLOP/s
+                 against the bf16 matrix-core peak
   roofline       the dominant kernel (draft decode attention): algorithmic
                  bytes per launch / mean launch duration from HIP events
   cpu_baseline   the fp64 oracle on the host cores (a bounded sample)
@@ -482,6 +485,31 @@ def main():
         log(f"accept {name} stochastic: {t * 1e6:.2f} us")
         del ps, qs, fns, g
 
+    # ------------------------------------------------------ memory prefill ----
+    pre_res = {}
+    P, S_, W_, r_, u_ = 32768, 0, 1024, 16, 4
+    M = mad.slots_after(P, S_, r_, u_)
+    for name, Hq, Hkv, d in (("32k_d64_32_8", 32, 8, 64), ("32k_d128_32_8", 32, 8, 128)):
+        qr = torch.randn(1, P, Hq, d, device="cuda").to(torch.bfloat16)
+        qs_ = torch.randn(1, M, Hq, d, device="cuda").to(torch.bfloat16)
+        rk = torch.randn(1, Hkv, P, d, device="cuda").to(torch.bfloat16)
+        rv = torch.randn(1, Hkv, P, d, device="cuda").to(torch.bfloat16)
+        mk = torch.randn(1, Hkv, S_ + M, d, device="cuda").to(torch.bfloat16)
+        mv = torch.randn(1, Hkv, S_ + M, d, device="cuda").to(torch.bfloat16)
+        outs = mad.memory_prefill_attn(qr, qs_, mad.KV(mk, mv, [S_ + M]), mad.KV(rk, rv, [P]), [P], S_, W_, r_, u_)
+        fn = lambda: mad.memory_prefill_attn(qr, qs_, mad.KV(mk, mv, [S_ + M]), mad.KV(rk, rv, [P]), [P],
+                                             S_, W_, r_, u_, *outs)
+        g = graph_of(torch, lambda: [fn() for _ in range(3)])
+        g.replay()
+        t = time_graph(torch, g, reps=2) / 3
+        flops = prefill_flops(P, S_, W_, r_, u_, Hq, d)
+        pre_res[name] = {"us": round(t * 1e6, 1), "tflops": round(flops / t / 1e12, 1),
+                         "mfma_frac_of_bf16_peak": round(flops / t / PEAK_BF16, 4), "flops": flops,
+                         "queries": P + M}
+        log(f"memory prefill {name}: {t * 1e6:.1f} us, {flops / t / 1e12:.1f} TFLOP/s")
+        del qr, qs_, rk, rv, mk, mv, outs, g
+    torch.cuda.empty_cache()
+
     # --------------------------------------------------------- CPU baseline ----
     cpu = None
     if not args.no_cpu_baseline:
@@ -506,9 +534,27 @@ def main():
         "memory_update": upd_res,
         "verify": ver_res,
         "accept": acc_res,
+        "memory_prefill": pre_res,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
+
+
+def prefill_flops(P, S, W, r, u, Hq, d):
+    """Multiply-adds x 2 of both attention products over every query's visible
+    keys in the memory-prefill pass: a raw token at p sees min(S, p+1) sinks,
+    the slots materialised before it and its window; slot m sees S sinks, m
+    slots and the W raw tokens before its position id."""
+    import numpy as np
+    p = np.arange(P, dtype=np.int64)
+    seen_slots = np.where(p <= S, 0, (p - S) // (r * u) * u)
+    window = np.where(p < S, 0, p - np.maximum(S, p - W + 1) + 1)
+    raw = np.minimum(S, p + 1) + seen_slots + window
+    M = 0 if P <= S else (P - S) // (r * u) * u
+    m = np.arange(1, M + 1, dtype=np.int64)
+    bm = S + m * r
+    slot = S + m + (bm - np.maximum(S, bm - W))
+    return int((raw.sum() + slot.sum()) * Hq * d * 4)
 
 
 def cpu_baseline(seconds):
