@@ -16,6 +16,13 @@ K/V materialisation:
 
 ``accept_stochastic`` wraps the rejection-sampling rule (oracle.c).
 
+``rmsnorm``, ``silu``, ``bf16_round`` and ``decoder_layer`` give one draft
+decoder layer around the attention (a pre-norm Llama-family layer: RMSNorm,
+Q/K/V projection with RoPE, attention supplied by the caller, output
+projection and residual, RMSNorm, SwiGLU MLP and residual): slot tokens run
+through the same blocks (Sec. 3.2), and the layer's weights are the draft's
+per-token weight stream (Sec. 2.3, Eq. latency_decomp).
+
 ``memory_prefill`` is the draft's memory-prefill attention (Sec. 3.3 prefill;
 the appendix on memory prefill): the prefill mask applies the write policy of
 decoding, so each query of the pass attends over the set ``masw_sets`` gives
@@ -241,3 +248,53 @@ def memory_prefill(q_raw, q_slot, mem_k, mem_v, raw_k, raw_v, P, S, W, r, u, sca
         for m in (range(1, M + 1) if slot_idx is None else slot_idx):
             slot_out[m] = run(_f64(q_slot[m - 1]), sets.slot_scope(m))
     return raw_out, slot_out
+
+
+def rmsnorm(x, gamma, eps):
+    """Per row: x / sqrt(mean(x^2) + eps) * gamma."""
+    x = _f64(x)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * _f64(gamma)
+
+
+def silu(x):
+    """x * sigmoid(x)."""
+    x = _f64(x)
+    return x / (1.0 + np.exp(-x))
+
+
+def bf16_round(a):
+    """Values rounded to bfloat16 (nearest, ties to even), returned as float64:
+    the float32 value, then the low 16 bits of its pattern rounded away."""
+    f = np.ascontiguousarray(a, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def decoder_layer(x, params, pos, attend_rows, rnd=None):
+    """One pre-norm decoder layer for the rows x [R, D] at position ids pos [R].
+
+    params: gamma1 [D], w_qkv [(Hq + 2 Hkv) d, D] (W_q, W_k, W_v rows), w_o
+    [D, Hq d], gamma2 [D], w_gate_up [2F, D] (W_gate, W_up rows), w_down [D, F],
+    and Hq, Hkv, d, base, eps.  attend_rows(q [R, Hq, d], k [R, Hkv, d],
+    v [R, Hkv, d], xn [R, D]) -> o [R, Hq, d] is the attention of each row
+    over its own key set.  rnd, if given, is applied to every stored
+    intermediate (the layer's tensors are held in that precision).
+    Returns a dict of xn, q, k, v, o, h, a, y."""
+    rnd = rnd or (lambda t: t)
+    Hq, Hkv, d = params["Hq"], params["Hkv"], params["d"]
+    R = x.shape[0]
+    x = _f64(x)
+    xn = rnd(rmsnorm(x, params["gamma1"], params["eps"]))
+    qkv = project(xn, params["w_qkv"])
+    q = rnd(rope(qkv[:, :Hq * d].reshape(R, Hq, d), pos, params["base"]))
+    k = rnd(rope(qkv[:, Hq * d:(Hq + Hkv) * d].reshape(R, Hkv, d), pos, params["base"]))
+    v = rnd(qkv[:, (Hq + Hkv) * d:].reshape(R, Hkv, d))
+    o = rnd(_f64(attend_rows(q, k, v, xn)))
+    h = rnd(x + project(o.reshape(R, Hq * d), params["w_o"]))
+    hn = rnd(rmsnorm(h, params["gamma2"], params["eps"]))
+    gu = project(hn, params["w_gate_up"])
+    F = gu.shape[1] // 2
+    a = rnd(silu(gu[:, :F]) * gu[:, F:])
+    y = rnd(h + project(a, params["w_down"]))
+    return {"xn": xn, "q": q, "k": k, "v": v, "o": o, "h": h, "a": a, "y": y}
