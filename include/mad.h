@@ -11,6 +11,7 @@
  *   - the target's (gamma+1)-query verify attention over its full KV  Sec. 2.1, 3.3
  *   - the greedy and the stochastic accept/reject rules              Sec. 2.1, 4.1
  *   - the draft's memory-prefill attention                          Sec. 3.3, App.
+ *   - the linear maps of a draft decoder layer around the attention  Sec. 2.3, 3.2
  *
  * Conventions shared by every entry point
  *   - Tensors are DEVICE memory owned by the caller, row-major; a key/value row
@@ -55,6 +56,7 @@ extern "C" {
 #define MAD_MAX_BATCH 64
 #define MAD_MAX_UPDATE_ROWS 64 /* B * n_new per mad_memory_update call */
 #define MAD_MAX_VERIFY_ROWS 64 /* T * (Hq / Hkv) per mad_verify_attn call */
+#define MAD_MAX_LAYER_ROWS 8   /* rows (raw token + slot tokens) per draft-layer linear map */
 
 #define MAD_OP_DECODE 0
 #define MAD_OP_UPDATE 1
@@ -261,6 +263,45 @@ int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq
                             float scale, const int32_t *P, int q_cap, int slot_cap, int S, int W, int r, int u,
                             const mad_kv_view *mem, const mad_kv_view *raw, void *out_raw, float *lse_raw,
                             void *out_slot, float *lse_slot, void *stream);
+
+/*
+ * The linear maps of a draft decoder layer around its attention.  A decode
+ * step runs, per layer, for R rows: the raw token and, in a materialisation
+ * pass, the memory-slot tokens, which go through the same transformer blocks
+ * and whose hidden states leaving layer l enter layer l+1 (Sec. 3.2); these
+ * maps stream the layer's weights, the alpha d^2 term of the draft's cost
+ * (Sec. 2.3, Eq. latency_decomp).  A pre-norm (RMSNorm) layer with a SwiGLU
+ * MLP, the Llama family the paper uses (Sec. 4.1):
+ *   xn  = rmsnorm(x) * gamma1        (fp32, rounded to bf16)
+ *   q, k, v = xn W_qkv^T; q and k rotated at pos[r] (rotate-half RoPE, base)
+ *   o   = attention(q, ...)          (mad_draft_decode_attn / _step_attn)
+ *   h   = x + o W_o^T
+ *   a   = silu(hn W_gate^T) * (hn W_up^T),  hn = rmsnorm(h) * gamma2
+ *   y   = h + a W_down^T
+ * Every tensor is BF16, row-major; weights in nn.Linear layout [out][in];
+ * products accumulate in fp32.  R <= MAD_MAX_LAYER_ROWS.
+ *
+ * mad_rmsnorm_qkv_rope: x [R][D]; gamma [D]; w_qkv [(Hq + 2 Hkv) d][D] (the
+ *   rows of W_q, then W_k, then W_v); pos HOST int32[R] position ids;
+ *   outputs q [R][Hq][d], k and v [R][Hkv][d]; xn [R][D] or NULL receives the
+ *   normalised rows (the input of the memory adaptor for slot rows).  With
+ *   kv_from_row0 != 0 every row's k and v are row 0's (the current token's,
+ *   which the rows of a fused step attend).  D in {2048, 4096}; d in {64, 128}.
+ * mad_linear_residual: out [R][N] = res + x W^T, x [R][D], w [N][D],
+ *   res [R][N]; D in {2048, 4096, 8192}; N a multiple of 8 (of 4 for D 8192).
+ *   out may be res; it must not overlap x.
+ * mad_rmsnorm_swiglu: out [R][F] = silu(xn W_gate^T) * (xn W_up^T),
+ *   xn = rmsnorm(x) * gamma, w_gate_up [2F][D] (W_gate rows, then W_up);
+ *   D in {2048, 4096}; F a multiple of 4.
+ * Errors: MAD_EINVAL (null or unaligned pointers, R, sizes), MAD_ENOTSUP
+ * (dtype is implied BF16; D or d outside the sets above).  No workspace.
+ */
+int mad_rmsnorm_qkv_rope(const void *x, const void *gamma, float eps, const void *w_qkv, const int32_t *pos, int R,
+                         int D, int Hq, int Hkv, int d, double rope_base, int kv_from_row0, void *q, void *k,
+                         void *v, void *xn, void *stream);
+int mad_linear_residual(const void *x, const void *w, const void *res, int R, int D, int N, void *out, void *stream);
+int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *w_gate_up, int R, int D, int F,
+                       void *out, void *stream);
 
 /*
  * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:

@@ -60,12 +60,16 @@ def _load_library():
     lib.mad_draft_step_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, _u8p, vp, vp, vp, sz, vp]
     lib.mad_memory_prefill_attn.argtypes = [vp, vp, i, i, i, i, i, f, _i32p, i, i, i, i, i, i, kvp, kvp,
                                             vp, vp, vp, vp, vp]
+    lib.mad_rmsnorm_qkv_rope.argtypes = [vp, vp, f, vp, _i32p, i, i, i, i, i, d, i, vp, vp, vp, vp, vp]
+    lib.mad_linear_residual.argtypes = [vp, vp, vp, i, i, i, vp, vp]
+    lib.mad_rmsnorm_swiglu.argtypes = [vp, vp, f, vp, i, i, i, vp, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
-               "mad_accept_stochastic", "mad_draft_step_attn", "mad_memory_prefill_attn"):
+               "mad_accept_stochastic", "mad_draft_step_attn", "mad_memory_prefill_attn",
+               "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -351,3 +355,45 @@ def memory_prefill_attn(q_raw: torch.Tensor, q_slot: Optional[torch.Tensor], mem
         _stream(q_raw.device))
     _check(rc)
     return out_raw, lse_raw, (out_slot if q_slot is not None else None), (lse_slot if q_slot is not None else None)
+
+
+def rmsnorm_qkv_rope(x: torch.Tensor, gamma: torch.Tensor, w_qkv: torch.Tensor, pos: Sequence[int], Hq: int,
+                     Hkv: int, d: int, q: Optional[torch.Tensor] = None, k: Optional[torch.Tensor] = None,
+                     v: Optional[torch.Tensor] = None, xn: Optional[torch.Tensor] = None, eps: float = 1e-5,
+                     rope_base: float = 500000.0, kv_from_row0: bool = False):
+    """x [R, D] -> q [R, Hq, d], k and v [R, Hkv, d] (q, k rotated at pos), and the
+    normalised rows xn [R, D] when given."""
+    R, D = x.shape
+    if q is None:
+        q = torch.empty((R, Hq, d), dtype=x.dtype, device=x.device)
+    if k is None:
+        k = torch.empty((R, Hkv, d), dtype=x.dtype, device=x.device)
+    if v is None:
+        v = torch.empty((R, Hkv, d), dtype=x.dtype, device=x.device)
+    rc = _load_library().mad_rmsnorm_qkv_rope(_ptr(x), _ptr(gamma), float(eps), _ptr(w_qkv), _host_i32(pos, R), R,
+                                              D, Hq, Hkv, d, float(rope_base), 1 if kv_from_row0 else 0, _ptr(q),
+                                              _ptr(k), _ptr(v), _ptr(xn), _stream(x.device))
+    _check(rc)
+    return q, k, v
+
+
+def linear_residual(x: torch.Tensor, w: torch.Tensor, res: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """out [R, N] = res + x W^T."""
+    R, D = x.shape
+    N = w.shape[0]
+    if out is None:
+        out = torch.empty((R, N), dtype=x.dtype, device=x.device)
+    _check(_load_library().mad_linear_residual(_ptr(x), _ptr(w), _ptr(res), R, D, N, _ptr(out), _stream(x.device)))
+    return out
+
+
+def rmsnorm_swiglu(x: torch.Tensor, gamma: torch.Tensor, w_gate_up: torch.Tensor,
+                   out: Optional[torch.Tensor] = None, eps: float = 1e-5):
+    """out [R, F] = silu(xn W_gate^T) * (xn W_up^T), xn = rmsnorm(x) * gamma."""
+    R, D = x.shape
+    Fd = w_gate_up.shape[0] // 2
+    if out is None:
+        out = torch.empty((R, Fd), dtype=x.dtype, device=x.device)
+    _check(_load_library().mad_rmsnorm_swiglu(_ptr(x), _ptr(gamma), float(eps), _ptr(w_gate_up), R, D, Fd,
+                                              _ptr(out), _stream(x.device)))
+    return out

@@ -391,6 +391,83 @@ int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq
     return hip_status(mad::launch_prefill(a, d, G, (hipStream_t)stream), "memory prefill launch");
 }
 
+int mad_rmsnorm_qkv_rope(const void *x, const void *gamma, float eps, const void *w_qkv, const int32_t *pos, int R,
+                         int D, int Hq, int Hkv, int d, double rope_base, int kv_from_row0, void *q, void *k,
+                         void *v, void *xn, void *stream) {
+    if (R < 1 || R > MAD_MAX_LAYER_ROWS) return fail(MAD_EINVAL, "R=%d outside [1, %d]", R, MAD_MAX_LAYER_ROWS);
+    if (D != 2048 && D != 4096) return fail(MAD_ENOTSUP, "D=%d not supported (2048, 4096)", D);
+    if (d != 64 && d != 128) return fail(MAD_ENOTSUP, "head_dim %d not supported (64 or 128)", d);
+    if (Hq < 1 || Hkv < 1 || Hq % Hkv) return fail(MAD_EINVAL, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+    if (!x || !gamma || !w_qkv || !pos || !q || !k || !v) return fail(MAD_EINVAL, "null x, gamma, w_qkv, pos, q, k or v");
+    if (!aligned16(x) || !aligned16(gamma) || !aligned16(w_qkv) || (xn && !aligned16(xn)))
+        return fail(MAD_EINVAL, "x/gamma/w_qkv/xn not 16-byte aligned");
+    if (!(eps > 0.f) || !(rope_base > 1.0) || rope_base != rope_base || isinf(rope_base))
+        return fail(MAD_EINVAL, "eps must be positive and rope_base finite and > 1");
+    mad::LinearArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.w = w_qkv;
+    a.gamma = gamma;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.xn = xn;
+    a.eps = eps;
+    a.log2_base = log2(rope_base);
+    a.R = R;
+    a.D = D;
+    a.N = (Hq + 2 * Hkv) * d;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.head_dim = d;
+    a.kv_from_row0 = kv_from_row0 ? 1 : 0;
+    for (int r = 0; r < R; ++r) a.pos[r] = pos[r];
+    return hip_status(mad::launch_linear(a, 0, (hipStream_t)stream), "qkv projection launch");
+}
+
+int mad_linear_residual(const void *x, const void *w, const void *res, int R, int D, int N, void *out, void *stream) {
+    if (R < 1 || R > MAD_MAX_LAYER_ROWS) return fail(MAD_EINVAL, "R=%d outside [1, %d]", R, MAD_MAX_LAYER_ROWS);
+    if (D != 2048 && D != 4096 && D != 8192) return fail(MAD_ENOTSUP, "D=%d not supported (2048, 4096, 8192)", D);
+    if (N < 8 || N % (D == 8192 ? 4 : 8)) return fail(MAD_EINVAL, "N=%d must be a positive multiple of %d", N, D == 8192 ? 4 : 8);
+    if (!x || !w || !res || !out) return fail(MAD_EINVAL, "null x, w, res or out");
+    if (!aligned16(x) || !aligned16(w)) return fail(MAD_EINVAL, "x/w not 16-byte aligned");
+    const char *xb = (const char *)x, *ob = (const char *)out;
+    if (ob < xb + (size_t)R * D * 2 && xb < ob + (size_t)R * N * 2) return fail(MAD_EINVAL, "out overlaps x");
+    mad::LinearArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.w = w;
+    a.res = res;
+    a.out = out;
+    a.R = R;
+    a.D = D;
+    a.N = N;
+    return hip_status(mad::launch_linear(a, 1, (hipStream_t)stream), "linear launch");
+}
+
+int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *w_gate_up, int R, int D, int F,
+                       void *out, void *stream) {
+    if (R < 1 || R > MAD_MAX_LAYER_ROWS) return fail(MAD_EINVAL, "R=%d outside [1, %d]", R, MAD_MAX_LAYER_ROWS);
+    if (D != 2048 && D != 4096) return fail(MAD_ENOTSUP, "D=%d not supported (2048, 4096)", D);
+    if (F < 4 || F % 4) return fail(MAD_EINVAL, "F=%d must be a positive multiple of 4", F);
+    if (!x || !gamma || !w_gate_up || !out) return fail(MAD_EINVAL, "null x, gamma, w_gate_up or out");
+    if (!aligned16(x) || !aligned16(gamma) || !aligned16(w_gate_up)) return fail(MAD_EINVAL, "x/gamma/w not 16-byte aligned");
+    if (!(eps > 0.f)) return fail(MAD_EINVAL, "eps must be positive");
+    const char *xb = (const char *)x, *ob = (const char *)out;
+    if (ob < xb + (size_t)R * D * 2 && xb < ob + (size_t)R * F * 2) return fail(MAD_EINVAL, "out overlaps x");
+    mad::LinearArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.w = w_gate_up;
+    a.gamma = gamma;
+    a.out = out;
+    a.eps = eps;
+    a.R = R;
+    a.D = D;
+    a.N = F;
+    return hip_status(mad::launch_linear(a, 2, (hipStream_t)stream), "swiglu projection launch");
+}
+
 int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, int B, int T, int V,
                       int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
     if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);

@@ -112,6 +112,20 @@ struct VerifyArgs {
     int len[kMaxB];
 };
 
+// ----------------------------------------------------------------- layer ----
+constexpr int kMaxLinRows = MAD_MAX_LAYER_ROWS;
+
+struct LinearArgs {
+    const void *x, *w, *gamma, *res;
+    void *out, *xn, *q, *k, *v;
+    float eps;
+    double log2_base;
+    int R, D, N, Hq, Hkv, head_dim, kv_from_row0;
+    int pos[kMaxLinRows];
+};
+
+hipError_t launch_linear(const LinearArgs &a, int mode, hipStream_t st);
+
 // --------------------------------------------------------------- prefill ----
 struct PrefillArgs {
     const void *q_raw, *q_slot;

@@ -26,22 +26,6 @@ namespace mad {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 
-// Rotate-half RoPE: theta_j = base^(-2j/d) in double precision (one table per
-// workgroup), the angle pos * theta_j formed and reduced modulo 2 pi in double
-// precision (Cody-Waite with a two-part 2 pi), its sine and cosine taken in
-// single precision on the reduced angle in [-pi, pi].
-__device__ __forceinline__ double rope_theta(int j, int d, double log2_base) {
-    return exp2(-2.0 * (double)j / (double)d * log2_base);
-}
-__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
-    const double a = (double)pos * theta;
-    const double n = rint(a * 0.15915494309189535);            // 1 / (2 pi)
-    const double r = fma(-n, 1.2246467991473532e-16, fma(-n, 6.283185307179586, a));   // 2 pi = hi + lo
-    float s, c;
-    sincosf((float)r, &s, &c);
-    *k0 = y0 * c - y1 * s;
-    *k1 = y1 * c + y0 * s;
-}
 
 constexpr int kUpdSubK = 64;                 // k elements per ring stage (8 chunks of 16 bytes a row)
 

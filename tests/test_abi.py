@@ -232,3 +232,24 @@ def test_prefill_validation(mad):
     # nothing to do: every prefix empty
     zero = (ctypes.c_int32 * 2)(0, 0)
     assert call(P=zero) == mad.MAD_OK
+
+
+def test_layer_linear_validation(mad):
+    lib = mad._load_library()
+    vp = ctypes.c_void_p
+    pos = (ctypes.c_int32 * 8)(*range(8))
+    qkv = lambda R=1, D=2048, Hq=32, Hkv=8, d=64, eps=1e-5, base=5e5, x=1 << 20: lib.mad_rmsnorm_qkv_rope(
+        vp(x) if x else None, vp(1 << 21), eps, vp(1 << 22), pos, R, D, Hq, Hkv, d, base, 0, vp(1 << 23),
+        vp(1 << 24), vp(1 << 25), None, None)
+    assert qkv(R=0) == mad.MAD_EINVAL and qkv(R=9) == mad.MAD_EINVAL
+    assert qkv(D=3072) == mad.MAD_ENOTSUP and qkv(d=96) == mad.MAD_ENOTSUP
+    assert qkv(Hq=30) == mad.MAD_EINVAL and qkv(x=0) == mad.MAD_EINVAL and qkv(x=(1 << 20) + 2) == mad.MAD_EINVAL
+    assert qkv(eps=0.0) == mad.MAD_EINVAL and qkv(base=1.0) == mad.MAD_EINVAL
+    lin = lambda R=1, D=2048, N=2048, out=1 << 26, x=1 << 20: lib.mad_linear_residual(
+        vp(x), vp(1 << 22), vp(1 << 23), R, D, N, vp(out), None)
+    assert lin(D=1024) == mad.MAD_ENOTSUP and lin(N=12) == mad.MAD_EINVAL and lin(R=9) == mad.MAD_EINVAL
+    assert lin(out=(1 << 20) + 64) == mad.MAD_EINVAL and "overlaps" in _last_error(mad)
+    swi = lambda R=1, D=2048, F=8192, out=1 << 26: lib.mad_rmsnorm_swiglu(
+        vp(1 << 20), vp(1 << 21), 1e-5, vp(1 << 22), R, D, F, vp(out), None)
+    assert swi(F=6) == mad.MAD_EINVAL and swi(D=8192) == mad.MAD_ENOTSUP and swi(R=0) == mad.MAD_EINVAL
+    assert swi(out=(1 << 20) + 16) == mad.MAD_EINVAL
