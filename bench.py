@@ -25,6 +25,10 @@ Reported in the same run (sub-objects of the JSON line):
                  layers at a 32768-token prefix
   accept         greedy accept on [B, 5, 128256] fp32 logits, and the stochastic
                  accept/reject rule on probabilities with caller uniforms
+  draft_layer    whole draft steps through 16 random-init decoder layers
+                 (RMSNorm, Q/K/V + RoPE, attention, projections, SwiGLU) with
+                 the compact memory and with the full KV, and the weight
+                 stream of the linear maps alone
   memory_prefill the draft's masked prefill attention over a 32K prefix (32768
                  raw tokens + 2048 slots, 32/8 heads, d 64 and d 128), TFLOP/s
                  against the bf16 matrix-core peak
@@ -485,6 +489,10 @@ def main():
         log(f"accept {name} stochastic: {t * 1e6:.2f} us")
         del ps, qs, fns, g
 
+    # ------------------------------------------------ draft layer, end to end ----
+    lay_res = draft_layer_bench(torch, mad, K)
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------------ memory prefill ----
     pre_res = {}
     P, S_, W_, r_, u_ = 32768, 0, 1024, 16, 4
@@ -535,9 +543,79 @@ def main():
         "verify": ver_res,
         "accept": acc_res,
         "memory_prefill": pre_res,
+        "draft_layer": lay_res,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
+
+
+def draft_layer_bench(torch, mad, K):
+    """Whole draft steps through 16 random-init decoder layers of the 32K draft
+    (D 2048, 32/8 heads, d 64, SwiGLU FFN 8192: the attention shapes of the
+    headline): RMSNorm + Q/K/V + RoPE, attention, output projection, RMSNorm +
+    SwiGLU, down projection, per layer, with the compact memory and with the
+    full 32768-token KV.  The layers' 1.9 GB of weights are streamed from HBM
+    every step.  A step crossing a 64-token boundary carries four slot rows
+    through every layer (memory update + fused attention)."""
+    from paper_2608_30252_amd.layer import DraftLayer, LayerWeights
+    L, D, Hq, Hkv, d, F = 16, 2048, 32, 8, 64, 8192
+    dev = torch.device("cuda")
+    bf = torch.bfloat16
+
+    def rnd(*shape, std=0.02):
+        return (torch.randn(*shape, device=dev) * std).to(bf)
+    layers = []
+    for _ in range(L):
+        w = LayerWeights(gamma1=(1 + rnd(D, std=0.1).float()).to(bf), w_qkv=rnd((Hq + 2 * Hkv) * d, D),
+                         w_kv_g=rnd(2 * Hkv * d, D), w_o=rnd(D, Hq * d), gamma2=(1 + rnd(D, std=0.1).float()).to(bf),
+                         w_gate_up=rnd(2 * F, D), w_down=rnd(D, F))
+        layers.append(DraftLayer(w, D, Hq, Hkv, d, F, device=dev))
+    wbytes = layers[0].w.weight_bytes()
+    out = {"workload": "16 random-init layers, D 2048, 32/8 heads, d 64, FFN 8192, bf16, batch 1, 32K prefix",
+           "weight_bytes_per_layer": wbytes}
+    emb = rnd(5, D, std=1.0)   # row 0: the raw token entering layer 0; rows 1..4: slot tokens
+    for name, full in (("compact", False), ("full_kv", True)):
+        m = DraftModel(torch, mad, 1, layers=L, full_kv=full)
+        ws = m.ws
+        if full:
+            start = m.prefix
+        else:   # a few steps before a 64-token boundary, so one materialisation step is timed
+            start = m.prefix + 64 - 3
+
+        def step(p):
+            upd = None if full else m.lay.update_in_pass_of(p)
+            x = emb[:1] if upd is None else emb[:1 + len(upd.positions)]
+            for l in range(L):
+                x = layers[l].step(x, p, m.lay, None if full else m.mem_k[0][l], None if full else m.mem_v[0][l],
+                                   m.ring_k[0][l], m.ring_v[0][l], ws=ws, full_kv=full)
+        nsteps = min(K, 16)
+        warm = graph_of(torch, lambda: step(start))
+        g = graph_of(torch, lambda: [step(start + 1 + i) for i in range(nsteps)])
+        warm.replay()
+        t = time_graph(torch, g, reps=2) / nsteps
+        out[name] = {"ms_per_step": round(t * 1e3, 4), "us_per_layer": round(t * 1e6 / L, 2),
+                     "tokens_per_s": round(1.0 / t, 1), "steps": nsteps}
+        log(f"draft layer {name}: {t * 1e6 / L:.2f} us/layer, {t * 1e3:.3f} ms per 16-layer step")
+        del m, warm, g
+        torch.cuda.empty_cache()
+    # the weight stream alone: the four linear maps of one decode row per layer
+    x1 = emb[:1]
+
+    def maps():
+        for lyr in layers:
+            w = lyr.w
+            mad.rmsnorm_qkv_rope(x1, w.gamma1, w.w_qkv, [40000], Hq, Hkv, d, lyr.q[:1], lyr.k[:1], lyr.v[:1])
+            h = mad.linear_residual(lyr.o[:1].view(1, Hq * d), w.w_o, x1, out=lyr.h[:1])
+            a = mad.rmsnorm_swiglu(h, w.gamma2, w.w_gate_up, out=lyr.a[:1])
+            mad.linear_residual(a, w.w_down, h, out=lyr.y[:1])
+    g = graph_of(torch, maps)
+    g.replay()
+    t = time_graph(torch, g, reps=4)
+    out["linear_maps"] = {"us_per_layer": round(t * 1e6 / L, 2), "tbps": round(wbytes * L / t / 1e12, 3),
+                          "hbm_frac": round(wbytes * L / t / PEAK_HBM, 4)}
+    out["speedup_vs_full_kv"] = round(out["full_kv"]["us_per_layer"] / out["compact"]["us_per_layer"], 3)
+    log(f"draft layer linear maps: {t * 1e6 / L:.2f} us/layer, {wbytes * L / t / 1e12:.2f} TB/s")
+    return out
 
 
 def prefill_flops(P, S, W, r, u, Hq, d):

@@ -288,7 +288,7 @@ int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq
  *   kv_from_row0 != 0 every row's k and v are row 0's (the current token's,
  *   which the rows of a fused step attend).  D in {2048, 4096}; d in {64, 128}.
  * mad_linear_residual: out [R][N] = res + x W^T, x [R][D], w [N][D],
- *   res [R][N]; D in {2048, 4096, 8192}; N a multiple of 8 (of 4 for D 8192).
+ *   res [R][N]; D in {2048, 4096, 8192}; N a multiple of 4.
  *   out may be res; it must not overlap x.
  * mad_rmsnorm_swiglu: out [R][F] = silu(xn W_gate^T) * (xn W_up^T),
  *   xn = rmsnorm(x) * gamma, w_gate_up [2F][D] (W_gate rows, then W_up);

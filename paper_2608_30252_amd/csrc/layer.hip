@@ -221,14 +221,16 @@ static hipError_t launch_kd(const LinearArgs &a, int grid, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-// Features per workgroup: 8 (two loads of 16 B per thread and feature pair in
-// flight per KB of input), 4 for the wide down projection.
+// Features per workgroup (measured): 4 for Q/K/V (768 workgroups, all
+// resident at once), 8 for the output projection (one workgroup per CU), 4 for
+// the wide down projection, 8 (4 gate + 4 up) for the SwiGLU map.
 hipError_t launch_linear(const LinearArgs &a, int mode, hipStream_t st) {
-    if (mode == kLinQKV) return launch_kd<kLinQKV, 8>(a, a.N / 8, st);
+    if (mode == kLinQKV) return launch_kd<kLinQKV, 4>(a, a.N / 4, st);
     if (mode == kLinSwiglu) return launch_kd<kLinSwiglu, 8>(a, a.N / 4, st);
     if (mode == kLinRes) {
         if (a.D / 2048 == 4) return launch_rr<kLinRes, 4, 4>(a, a.N / 4, st);
-        return launch_kd<kLinRes, 8>(a, a.N / 8, st);
+        if (a.N % 8 == 0) return launch_kd<kLinRes, 8>(a, a.N / 8, st);
+        return launch_kd<kLinRes, 4>(a, a.N / 4, st);
     }
     return hipErrorInvalidValue;
 }

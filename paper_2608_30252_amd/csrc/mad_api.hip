@@ -428,7 +428,7 @@ int mad_rmsnorm_qkv_rope(const void *x, const void *gamma, float eps, const void
 int mad_linear_residual(const void *x, const void *w, const void *res, int R, int D, int N, void *out, void *stream) {
     if (R < 1 || R > MAD_MAX_LAYER_ROWS) return fail(MAD_EINVAL, "R=%d outside [1, %d]", R, MAD_MAX_LAYER_ROWS);
     if (D != 2048 && D != 4096 && D != 8192) return fail(MAD_ENOTSUP, "D=%d not supported (2048, 4096, 8192)", D);
-    if (N < 8 || N % (D == 8192 ? 4 : 8)) return fail(MAD_EINVAL, "N=%d must be a positive multiple of %d", N, D == 8192 ? 4 : 8);
+    if (N < 4 || N % 4) return fail(MAD_EINVAL, "N=%d must be a positive multiple of 4", N);
     if (!x || !w || !res || !out) return fail(MAD_EINVAL, "null x, w, res or out");
     if (!aligned16(x) || !aligned16(w)) return fail(MAD_EINVAL, "x/w not 16-byte aligned");
     const char *xb = (const char *)x, *ob = (const char *)out;
