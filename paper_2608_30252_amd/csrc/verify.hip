@@ -84,6 +84,10 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         }
     }
 
+    int lim_min = lim[0];
+    #pragma unroll
+    for (int rb = 1; rb < NB; ++rb) lim_min = min(lim_min, lim[rb]);
+
     // ---- this wave's slabs: keys kb = k0 + 32 wave + 128 i ----
     const int nsl = (k1 > k0 + wave * 32) ? (k1 - k0 - wave * 32 + 127) / 128 : 0;
     // K rows of the two 16-key blocks: A row m of block blk holds key
@@ -147,6 +151,12 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
                     sacc[blk][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[buf][blk][ks], qf[rb][ks], sacc[blk][rb], 0, 0, 0);
             }
         // online softmax and PV, per 16-row block
+        // the running max is kept on unscaled scores (the scale is positive):
+        // p = 2^(s c - m c) is one fma into the exponential.  A slab that is
+        // visible to every row of the wave skips the masks, and a row block
+        // whose max did not move in any lane skips the rescale of o.
+        const float cs = a.scale_log2;
+        const bool full = __all(kg + 8 <= k1 && kg + 7 <= lim_min);
         #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
             float sv[8];
@@ -154,30 +164,34 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
             #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int key = kg + j;
-                const bool ok = key < k1 && key <= lim[rb];
-                sv[j] = ok ? sacc[j >> 2][rb][j & 3] * a.scale_log2 : -INFINITY;
+                const bool ok = full || (key < k1 && key <= lim[rb]);
+                sv[j] = ok ? sacc[j >> 2][rb][j & 3] : -INFINITY;
                 mt = fmaxf(mt, sv[j]);
             }
             mt = max_over_row_lanes(mt);
             const float mn = fmaxf(m_run[rb], mt);
-            const float ms = (mn == -INFINITY) ? 0.f : mn;
-            const float alpha = __builtin_amdgcn_exp2f(m_run[rb] - ms);
+            const bool same = mn == m_run[rb];
+            const float ms = (mn == -INFINITY) ? 0.f : mn * cs;
+            const float alpha = same ? 1.f : __builtin_amdgcn_exp2f(fmaf(m_run[rb], cs, -ms));
             m_run[rb] = mn;
             float ps = 0.f;
             uint32_t pk[4];
             #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float p0 = __builtin_amdgcn_exp2f(sv[2 * e] - ms), p1 = __builtin_amdgcn_exp2f(sv[2 * e + 1] - ms);
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e], cs, -ms));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e + 1], cs, -ms));
                 ps += p0 + p1;
-                pk[e] = pack_bf16x2(p0, p1);
+                pk[e] = cvt_pk_bf16(p0, p1);
             }
             l_run[rb] = fmaf(l_run[rb], alpha, ps);
             const bf16x8_v pf = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
-            #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                o[db][rb] *= alpha;
-                o[db][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pf, o[db][rb], 0, 0, 0);
+            if (!__all(same)) {
+                #pragma unroll
+                for (int db = 0; db < DB; ++db) o[db][rb] *= alpha;
             }
+            #pragma unroll
+            for (int db = 0; db < DB; ++db)
+                o[db][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pf, o[db][rb], 0, 0, 0);
         }
     };
 
@@ -201,7 +215,7 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     for (int rb = 0; rb < NB; ++rb) {
         const float lt = sum_over_row_lanes(l_run[rb]);
         if (lg == 0) {
-            sML[(wave * RP + rb * 16 + lr) * 2] = m_run[rb];
+            sML[(wave * RP + rb * 16 + lr) * 2] = m_run[rb] == -INFINITY ? -INFINITY : m_run[rb] * a.scale_log2;
             sML[(wave * RP + rb * 16 + lr) * 2 + 1] = lt;
         }
         #pragma unroll
