@@ -245,15 +245,25 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
             const bool full = __all(base >= lo && base + C::KT <= hi);
             float sv16[2][8];
             float mt = -INFINITY;
-            #pragma unroll
-            for (int h = 0; h < 2; ++h)
+            if (full) {   // wave-uniform: no masks
                 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int key = base + 32 * h + 8 * lg + e;
-                    const float sc = sacc[h][e >> 2][i][e & 3];
-                    sv16[h][e] = (full || (key >= lo && key < hi)) ? sc : -INFINITY;
-                    mt = fmaxf(mt, sv16[h][e]);
-                }
+                for (int h = 0; h < 2; ++h)
+                    #pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        sv16[h][e] = sacc[h][e >> 2][i][e & 3];
+                        mt = fmaxf(mt, sv16[h][e]);
+                    }
+            } else {
+                #pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    #pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int key = base + 32 * h + 8 * lg + e;
+                        const bool ok = (key >= lo) & (key < hi);   // no short circuit: straight-line selects
+                        sv16[h][e] = ok ? sacc[h][e >> 2][i][e & 3] : -INFINITY;
+                        mt = fmaxf(mt, sv16[h][e]);
+                    }
+            }
             mt = prefill_row_max(mt);
             const float mn = fmaxf(m_run[i], mt);
             const float ms = (mn == -INFINITY) ? 0.f : mn * cs;

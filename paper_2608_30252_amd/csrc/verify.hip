@@ -161,12 +161,20 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
         for (int rb = 0; rb < NB; ++rb) {
             float sv[8];
             float mt = -INFINITY;
-            #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int key = kg + j;
-                const bool ok = full || (key < k1 && key <= lim[rb]);
-                sv[j] = ok ? sacc[j >> 2][rb][j & 3] : -INFINITY;
-                mt = fmaxf(mt, sv[j]);
+            if (full) {   // wave-uniform: no masks
+                #pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    sv[j] = sacc[j >> 2][rb][j & 3];
+                    mt = fmaxf(mt, sv[j]);
+                }
+            } else {
+                #pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int key = kg + j;
+                    const bool ok = (key < k1) & (key <= lim[rb]);   // no short circuit: straight-line selects
+                    sv[j] = ok ? sacc[j >> 2][rb][j & 3] : -INFINITY;
+                    mt = fmaxf(mt, sv[j]);
+                }
             }
             mt = max_over_row_lanes(mt);
             const float mn = fmaxf(m_run[rb], mt);
