@@ -280,15 +280,18 @@ def source_digest(*names):
     return h.hexdigest()
 
 
-def traffic_from_profile(kernel_file, bytes_default=None):
+DECODE_SOURCES = ("decode.hip", "mad_device.h", "mad_internal.h")   # what the decode kernel is built from
+
+
+def traffic_from_profile(sources, bytes_default=None):
     """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source; else None."""
+    taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", "decode_32k_compressed_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_sha256") != source_digest(kernel_file):
+    if t.get("source_sha256") != source_digest(*sources):
         return None
     return t.get("traffic_bytes_per_launch")
 
@@ -367,7 +370,7 @@ def main():
     log(f"decode launch: {t_launch * 1e6:.2f} us mean over {len(launches)}, {bytes_launch:,.0f} B -> "
         f"{achieved / 1e12:.2f} TB/s")
     roofline = {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM, 4), "traffic": traffic_from_profile("decode.hip"),
+                "frac": round(achieved / PEAK_HBM, 4), "traffic": traffic_from_profile(DECODE_SOURCES),
                 "kernel": "mad::decode_kernel<bf16_t, 64, 4, 1>", "bytes_per_launch": int(bytes_launch),
                 "mean_launch_us": round(t_launch * 1e6, 3)}
     del model

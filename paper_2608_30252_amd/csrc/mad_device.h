@@ -244,13 +244,17 @@ __device__ __forceinline__ void wait_vm(int n) {
 // for the builtin it places a wait for *every* outstanding vector-memory
 // operation before the next LDS read, which serialises a multi-stage ring.
 // Callers of lds_stream16 therefore own the waits: s_waitcnt vmcnt(n) plus a
-// workgroup barrier before the stage is read.
+// workgroup barrier before the stage is read.  M0 (the LDS base of the load)
+// is a register the compiler reserves and also sets for its own direct loads,
+// so the sequence saves and restores it rather than clobbering it.
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
 __device__ __forceinline__ void lds_stream16(const void *src, void *lds_base) {
     const uint32_t m = __builtin_amdgcn_readfirstlane(lds_addr(lds_base));
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(m) : "memory", "m0");
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved) : "v"(src), "s"(m) : "memory");
 }
 // Load N dwords at a wave-uniform address through the scalar cache (s_load).
 template <int N>
