@@ -179,6 +179,27 @@ __device__ __forceinline__ double shfl_xor_f64(double v, int m) {
     const int hi = __shfl_xor((int)(uint32_t)(u >> 32), m, 64);
     return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
 }
+__device__ __forceinline__ double shfl_up_f64(double v, int d) {
+    const uint64_t u = __double_as_longlong(v);
+    const int lo = __shfl_up((int)(uint32_t)u, d, 64);
+    const int hi = __shfl_up((int)(uint32_t)(u >> 32), d, 64);
+    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+// inclusive prefix sum over the 64 lanes of a wave (lane order)
+__device__ __forceinline__ double wave_scan_f64(double v, int lane) {
+    #pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const double y = shfl_up_f64(v, d);
+        if (lane >= d) v += y;
+    }
+    return v;
+}
+__device__ __forceinline__ double read_lane_f64(double v, int l) {
+    const uint64_t u = __double_as_longlong(v);
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, l);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
 __device__ __forceinline__ double wave_sum_f64(double v) {
     #pragma unroll
     for (int m = 1; m < 64; m <<= 1) v += shfl_xor_f64(v, m);
@@ -271,72 +292,105 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     if (!s_flag) return;
 
     // ---- last chunk of the sequence: locate the chunk, then the token ----
+    // (1) one wave reads the chunk sums (64 per pass), totals them and finds,
+    // by a prefix sum over chunks, the first chunk of positive weight whose
+    // running sum passes the target u * Z
     __shared__ int s_c, s_mode, s_fb;
     __shared__ double s_t;
-    if (tid == 0) {
-        double Zr = 0.0, Zp = 0.0;
-        for (int c = 0; c < a.n_chunks; ++c) {
-            Zr += __longlong_as_double((long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c)));
-            Zp += __longlong_as_double((long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c + 1)));
-        }
+    if (wave == 0) {
+        const int nc = a.n_chunks;
+        auto chunk_sum = [&](int c, int which) -> double {
+            return __longlong_as_double(
+                (long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c + which)));
+        };
+        double zr = 0.0, zp = 0.0;
+        for (int c0 = 0; c0 < nc; c0 += 64)
+            if (c0 + lane < nc) {
+                zr += chunk_sum(c0 + lane, 0);
+                zp += chunk_sum(c0 + lane, 1);
+            }
+        const double Zr = wave_sum_f64(zr), Zp = wave_sum_f64(zp);
         const int use_p = Zr == 0.0;   // empty residual: the draw uses p_a
         const double t = (double)a.u[(size_t)b * T + T - 1] * (use_p ? Zp : Zr);
-        double run = 0.0;
+        double carry = 0.0, before = 0.0;
         int cs = -1, clast = -1;
-        for (int c = 0; c < a.n_chunks; ++c) {
-            const double w = __longlong_as_double(
-                (long long)load_agent_u64(reinterpret_cast<const uint64_t *>(sums + 2 * c + use_p)));
-            if (w > 0.0) clast = c;
-            if (w > 0.0 && run + w > t) { cs = c; break; }
-            run += w;
+        for (int c0 = 0; c0 < nc; c0 += 64) {
+            const double w = c0 + lane < nc ? chunk_sum(c0 + lane, use_p) : 0.0;
+            const double incl = wave_scan_f64(w, lane);
+            const unsigned long long pos = __ballot(w > 0.0);
+            const unsigned long long hit = __ballot(w > 0.0 && carry + incl > t);
+            if (pos) clast = c0 + 63 - __clzll((long long)pos);
+            if (hit) {
+                const int l = __ffsll((long long)hit) - 1;
+                cs = c0 + l;
+                before = carry + read_lane_f64(incl, l) - read_lane_f64(w, l);
+                break;
+            }
+            carry += read_lane_f64(incl, 63);
         }
-        const int fb = cs < 0;   // no chunk passes t: the last positive entry is drawn
-        s_c = fb ? (clast >= 0 ? clast : 0) : cs;
-        s_mode = use_p;
-        s_fb = fb;
-        s_t = fb ? 0.0 : t - run;   // target measured from the chunk's start
+        if (lane == 0) {
+            const int fb = cs < 0;   // no chunk passes t: the last positive entry is drawn
+            s_c = fb ? (clast >= 0 ? clast : 0) : cs;
+            s_mode = use_p;
+            s_fb = fb;
+            s_t = fb ? 0.0 : t - before;   // target measured from the chunk's start
+        }
     }
     __syncthreads();
     const int cs = s_c;
     const bool wres = resid && !s_mode;
-    // runs of RUN consecutive entries of the chunk, one per thread
+    // (2) runs of RUN consecutive entries of the chunk, one per thread, kept in
+    // registers; a block prefix sum over the runs finds the run where the
+    // running sum passes the target, and that thread walks its run in order
     constexpr int RUN = kAcceptChunk / 256;
     const int cbeg = cs * kAcceptChunk, cend = min(V, cbeg + kAcceptChunk);
-    const int r0 = cbeg + tid * RUN, r1 = min(cend, r0 + RUN);
+    const int r0 = cbeg + tid * RUN;
+    double w[RUN];
     double mine = 0.0;
     int lastpos = -1;
-    for (int v = r0; v < r1; ++v) {
-        const double w = draw_weight(pr[v], wres ? qr[v] : 0.f, wres);
-        mine += w;
-        if (w > 0.0) lastpos = v;
+    #pragma unroll
+    for (int i = 0; i < RUN; ++i) {
+        const int v = r0 + i;
+        w[i] = v < cend ? draw_weight(pr[v], wres ? qr[v] : 0.f, wres) : 0.0;
+        mine += w[i];
+        if (w[i] > 0.0) lastpos = v;
     }
-    __shared__ double s_run[256];
-    __shared__ int s_pos[256];
-    s_run[tid] = mine;
-    s_pos[tid] = lastpos;
+    __shared__ double s_wt[4];
+    __shared__ int s_first[4], s_last[4];
+    const double incl = wave_scan_f64(mine, lane);
+    if (lane == 63) s_wt[wave] = incl;
     __syncthreads();
-    if (tid == 0) {
-        int last_any = -1;
-        for (int k = 0; k < 256; ++k) last_any = s_pos[k] > last_any ? s_pos[k] : last_any;
-        int v_out = last_any >= 0 ? last_any : cbeg;   // fallback: the chunk's last positive entry
-        if (!s_fb) {
-            const double tt = s_t;
-            double e = 0.0;
-            for (int k = 0; k < 256; ++k) {
-                const double w = s_run[k];
-                if (w > 0.0 && e + w > tt) {
-                    // the crossing lies in run k: walk it in index order
-                    const int q0 = cbeg + k * RUN, q1 = min(cend, q0 + RUN);
-                    v_out = s_pos[k];   // if rounding keeps the target above the run's own sum
-                    for (int v = q0; v < q1; ++v) {
-                        const double wv = draw_weight(pr[v], wres ? qr[v] : 0.f, wres);
-                        if (wv <= 0.0) continue;
-                        e += wv;
-                        if (e > tt) { v_out = v; break; }
-                    }
+    double excl = incl - mine;
+    for (int k = 0; k < wave; ++k) excl += s_wt[k];
+    const double tt = s_t;
+    const bool hit = !s_fb && mine > 0.0 && excl + mine > tt;
+    const unsigned long long hm = __ballot(hit);
+    int lp = lastpos;
+    #pragma unroll
+    for (int m = 1; m < 64; m <<= 1) lp = max(lp, __shfl_xor(lp, m, 64));
+    if (lane == 0) {
+        s_first[wave] = hm ? wave * 64 + __ffsll((long long)hm) - 1 : 0x7fffffff;
+        s_last[wave] = lp;
+    }
+    __syncthreads();
+    const int first = min(min(s_first[0], s_first[1]), min(s_first[2], s_first[3]));
+    if (first == 0x7fffffff) {   // fallback: the chunk's last positive entry
+        if (tid == 0) {
+            const int la = max(max(s_last[0], s_last[1]), max(s_last[2], s_last[3]));
+            a.n_accept[b] = acc;
+            a.next_tok[b] = la >= 0 ? la : cbeg;
+        }
+    } else if (tid == first) {
+        int v_out = lastpos;   // if rounding keeps the target above the run's own sum
+        double e = excl;
+        #pragma unroll
+        for (int i = 0; i < RUN; ++i) {
+            if (w[i] > 0.0) {
+                e += w[i];
+                if (e > tt) {
+                    v_out = r0 + i;
                     break;
                 }
-                e += w;
             }
         }
         a.n_accept[b] = acc;
