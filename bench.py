@@ -20,6 +20,7 @@ one HIP graph and replayed, so the clock measures GPU work, not Python.
 
 Reported in the same run (sub-objects of the JSON line):
   full_kv        the same draft step over the uncompressed 32768-token KV
+  batched_decode the same kernel on 16 sequences per launch (50 MB of K/V)
   memory_update  the adaptor alone at 4 rows (32K) and 64 rows (16 sequences)
   verify         the target's 5-query verify attention, 8B- and 70B-shaped
                  layers at a 32768-token prefix
@@ -407,6 +408,33 @@ def main():
     del full
     torch.cuda.empty_cache()
 
+    # ------------------------------------- batched draft decode (16 sequences) ----
+    # 16 sequences, 1024 slots + 511 window tokens + the new token each (50 MB per
+    # launch), the same kernel with enough work per launch to leave the latency floor
+    Bb, Lb, setsb = 16, 16, 4
+    mkb = [torch.randn(Bb, 8, 1024, 64, device="cuda").to(torch.bfloat16) for _ in range(setsb * 2)]
+    rkb = [torch.randn(Bb, 8, 576, 64, device="cuda").to(torch.bfloat16) for _ in range(setsb * 2)]
+    qb = torch.randn(Bb, 32, 64, device="cuda").to(torch.bfloat16)
+    knb = torch.randn(Bb, 8, 64, device="cuda").to(torch.bfloat16)
+    vnb = torch.randn_like(knb)
+    ob = torch.empty_like(qb)
+    lb = torch.empty(Bb, 32, device="cuda")
+    wsb = torch.zeros(mad.workspace_bytes(mad.MAD_OP_DECODE, Bb, 32, 8, 64), dtype=torch.uint8, device="cuda")
+    starts = [(37 * i) % 64 for i in range(Bb)]
+    fns = [lambda j=j: mad.draft_decode_attn(qb, mad.KV(mkb[2 * j], mkb[2 * j + 1], [1024] * Bb),
+                                             mad.KV(rkb[2 * j], rkb[2 * j + 1], [511] * Bb, starts), knb, vnb, ob,
+                                             lb, ws=wsb) for j in range(setsb)]
+    g = graph_of(torch, lambda: [fns[i % setsb]() for i in range(Lb)])
+    g.replay()
+    t = time_graph(torch, g, reps=3) / Lb
+    nb = kv_bytes(1024 + 511 + 1, 8, 64) * Bb
+    batched = {"workload": "B16, 32/8 heads, d64, 1024 slots + 512-token window per sequence, bf16",
+               "us_per_launch": round(t * 1e6, 2), "bytes_per_launch": nb, "tbps": round(nb / t / 1e12, 3),
+               "hbm_frac": round(nb / t / PEAK_HBM, 4)}
+    log(f"batched decode B16: {t * 1e6:.2f} us/launch, {nb / t / 1e12:.2f} TB/s")
+    del mkb, rkb, fns, g
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------------- memory update ----
     upd_res = {}
     for name, B, n_new, sets in (("32k_4_rows", 1, 4, 8), ("batched_64_rows", 16, 4, 8)):
@@ -542,6 +570,7 @@ def main():
         "roofline": roofline,
         "full_kv": full_kv,
         "speedup_vs_full_kv": round(full_us_layer / us_per_layer, 3),
+        "batched_decode": batched,
         "memory_update": upd_res,
         "verify": ver_res,
         "accept": acc_res,

@@ -577,16 +577,17 @@ int decode_max_splits(int d, int G) {
 static int decode_tile(int dtype, int d) { return 8192 / (d * (dtype == MAD_BF16 ? 2 : 4)); }
 
 // Two-group workgroups (8 waves, two per CU) for bf16 with head_dim 64 and at
-// most 4 query heads per KV head when few units hold many keys (long streams,
-// where two tiles in flight per workgroup and fewer partials pay); one-group
-// workgroups (4 waves, one per CU, about two tiles per split) elsewhere, where
-// the first loads are spread over as many CUs as possible.
+// most 4 query heads per KV head when the launch holds many keys (long
+// streams or many sequences, where two tiles in flight per workgroup and fewer
+// partials pay); one-group workgroups (4 waves, about two tiles per split)
+// for short streams, where the first loads are spread over as many CUs as
+// possible.
 static int decode_nsub(int units, int n_max, int G, int d, int dtype) {
     if (!(dtype == MAD_BF16 && d == 64 && G <= 4)) return 1;
 #ifdef MAD_DECODE_FORCE_NSUB
     return MAD_DECODE_FORCE_NSUB;
 #endif
-    const bool wide = units <= kDecodeWideUnits && (int64_t)units * n_max >= kDecodeWideKeys;
+    const bool wide = (int64_t)units * n_max >= kDecodeWideKeys;
     return wide ? 2 : 1;
 }
 
@@ -597,8 +598,12 @@ DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_key
     for (int b = 0; b < B; ++b) p.n_max = n_keys[b] > p.n_max ? n_keys[b] : p.n_max;
     p.nsub = decode_nsub(p.units, p.n_max, G, d, dtype);
     const int super = p.nsub * decode_tile(dtype, d);
-    // workgroups to aim for: two per CU with 8 waves, one with 4
-    const int target = (p.nsub == 2 ? 2 * kDecodeCUs : kDecodeCUs) / kDecodeTargetDiv;
+    // workgroups to aim for: two per CU with 8 waves; with 4 waves one per CU
+    // for a short stream (the first loads spread over every CU decide the time),
+    // two per CU when there is enough work to need the loads in flight of both
+    const int64_t total = (int64_t)p.units * p.n_max;
+    const int per_cu = p.nsub == 2 ? 2 : (total >= kDecodeWideKeys ? 2 : 1);
+    const int target = per_cu * kDecodeCUs / kDecodeTargetDiv;
     int ns = (target + p.units - 1) / p.units;
     const int cap = decode_max_splits(d, G);
     if (ns > cap) ns = cap;

@@ -15,8 +15,7 @@ constexpr int kMaxB = MAD_MAX_BATCH;
 // The split count aims at one 4-wave or two 8-wave workgroups per CU; splits
 // are whole super-tiles (see plan_decode).
 constexpr int kDecodeCUs = 256;        // compute units of the device the split plan is sized for
-constexpr int kDecodeWideUnits = 32;        // 8-wave workgroups: at most this many units
-constexpr int kDecodeWideKeys = 65536;      //   holding at least this many keys in all
+constexpr int kDecodeWideKeys = 65536;      // 8-wave workgroups: launches holding at least this many keys
 #ifndef MAD_DECODE_TARGET_DIV
 #define MAD_DECODE_TARGET_DIV 1
 #endif
