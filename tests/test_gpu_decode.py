@@ -121,6 +121,11 @@ def test_ragged_batch_bf16():
     _case(torch.bfloat16, B, 32, 8, 64, mlen, wlen, 544, start, seed=8, mcap=1024)
 
 
+def test_batched_sixteen_sequences_bench_configuration():
+    # the benchmark's batched launch: 16 sequences x (1024 slots + 511 window + new), 8-wave workgroups
+    _case(torch.bfloat16, 16, 32, 8, 64, 1024, 511, 576, [(37 * i) % 64 for i in range(16)], seed=12, mcap=1024)
+
+
 def test_no_new_token_and_no_memory():
     _case(torch.bfloat16, 2, 32, 8, 64, 300, 200, 256, 100, new=False, seed=9)
     _case(torch.bfloat16, 2, 32, 8, 64, 0, 200, 256, 100, new=True, seed=10, mem=False)
