@@ -291,7 +291,7 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
     if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
     if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
     if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
-    mad::VerifyPlan p = mad::plan_verify(B, Hkv, len);
+    mad::VerifyPlan p = mad::plan_verify(B, Hkv, G, T, len);
     mad::VerifyArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;

@@ -147,7 +147,7 @@ struct VerifyPlan {
     int units, n_splits, chunk;
 };
 
-VerifyPlan plan_verify(int B, int Hkv, const int *len);
+VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len);
 size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T);
 void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml);
 hipError_t launch_verify(const VerifyArgs &a, hipStream_t st);

@@ -27,6 +27,13 @@
 
 namespace mad {
 
+#ifndef MAD_VERIFY_REGS
+#define MAD_VERIFY_REGS 0   // 1: the register-resident split kernel for every shape
+#endif
+#ifndef MAD_VERIFY_LDS_MIN_NB
+#define MAD_VERIFY_LDS_MIN_NB 3   // query row blocks from which the LDS-staged kernel is used
+#endif
+
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
@@ -255,6 +262,211 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// LDS-staged split kernel.  The register-resident kernel above keeps a full
+// copy of the output accumulators in every wave (the waves split keys), which
+// leaves room for one or two 32-key slabs in flight per wave: with HBM latency
+// under load of several microseconds that caps the stream.  Here the waves
+// split the query rows instead (wave w owns 16-row block w) and share every
+// K/V slab through a deep LDS ring filled by direct loads
+// (global_load_lds_dwordx4, issued by all four waves), so about
+// (NST - 1) x 16 KB are in flight per workgroup:
+//   * K rows land with their 16-byte chunks XOR-swizzled by row, so the
+//     permuted-row A operand reads of S^T = K Q^T are conflict-free;
+//   * V^T rows (one feature, the slab's 32 keys) land with their 16-byte
+//     key chunks swizzled by feature for the A operand of O^T = V^T P^T;
+//   * one barrier per slab; each wave writes its rows' partial (max, sum, o).
+template <int D>
+struct VerifyLdsCfg {
+    static constexpr int SLAB = 64;                        // keys per slab (128 contiguous bytes of each V^T row)
+    static constexpr int RB = D * 2;                       // bytes per K row
+    static constexpr int KBYTES = SLAB * RB;               // K bytes per slab (= V^T bytes)
+    static constexpr int VROW = SLAB * 2;                  // bytes per V^T row in a stage
+    static constexpr int STAGE = 2 * KBYTES;
+    static constexpr int NST = D == 128 ? 4 : 8;           // ring stages (128 KB)
+    static constexpr int IPW = STAGE / 1024 / 4;           // direct loads per wave per slab
+    static constexpr int SMEM = NST * STAGE;
+};
+
+__device__ __forceinline__ int vk_swz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+
+template <int D, int NB>
+__global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) {
+    using C = VerifyLdsCfg<D>;
+    constexpr int KST = D / 32, DB = D / 16, CPR = D / 8;
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int u = blockIdx.x % a.units, s = blockIdx.x / a.units;
+    const int b = u / a.Hkv, c = u - b * a.Hkv;
+    const int len = a.len[b], T = a.T, G = a.G, R = T * G;
+    const int k0 = s * a.chunk;
+    const int k1 = min(len, k0 + a.chunk);
+    const int cap = a.cap;
+    const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
+    const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
+    const int lr = lane & 15, lg = lane >> 4;
+    const bool active = wave < NB;
+
+    // ---- this wave's query fragments and causal limit (row block `wave`) ----
+    bf16x8_v qf[KST];
+    const int row = wave * 16 + lr;
+    int lim = 0x7fffffff;
+    if (active && row < R) {
+        const int t = row / G, g = row - t * G;
+        const bf16_t *qrow = reinterpret_cast<const bf16_t *>(a.q) + (((size_t)b * T + t) * a.Hq + c * G + g) * D;
+        #pragma unroll
+        for (int ks = 0; ks < KST; ++ks) qf[ks] = *reinterpret_cast<const bf16x8_v *>(qrow + ks * 32 + 8 * lg);
+        lim = len - T + t;
+    } else {
+        #pragma unroll
+        for (int ks = 0; ks < KST; ++ks) qf[ks] = bf16x8_v{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+    // the query loads complete here, before any direct load is in flight, so
+    // no wait the compiler places for them can drain the ring later
+    #pragma unroll
+    for (int ks = 0; ks < KST; ++ks) asm volatile("" : : "v"(qf[ks]));
+
+    const int nsl = k1 > k0 ? (k1 - k0 + C::SLAB - 1) / C::SLAB : 0;
+    auto issue = [&](int i) {
+        unsigned char *st = smem + (i % C::NST) * C::STAGE;
+        const int kb = k0 + i * C::SLAB;
+        #pragma unroll
+        for (int j = 0; j < C::IPW / 2; ++j) {
+            const int inst = wave * (C::IPW / 2) + j;
+            const int cidx = inst * 64 + lane;
+            // K: row cidx / CPR, LDS slot cidx % CPR holds global chunk slot ^ swz(row)
+            const int kr = cidx / CPR, slot = cidx % CPR;
+            const int key = min(kb + kr, len - 1);   // rows past len: a valid row, masked
+            lds_stream16(K + (size_t)key * D + (slot ^ vk_swz(kr)) * 8, st + inst * 1024);
+            // V^T: feature cidx / 8, LDS slot cidx % 8 holds key chunk slot ^ (f & 7)
+            const int f = cidx >> 3, vs = cidx & 7;
+            int kc = kb + ((vs ^ (f & 7)) << 3);
+            if (kc + 8 > cap) kc = cap - 8;          // chunks past the cache: any valid chunk (zeroed when used)
+            lds_stream16(VT + (size_t)f * cap + kc, st + C::KBYTES + inst * 1024);
+        }
+    };
+
+    f32x4_v o[DB];
+    #pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+    const float cs = a.scale_log2;
+
+    auto compute = [&](int i) {
+        const unsigned char *st = smem + (i % C::NST) * C::STAGE;
+        const int kb = k0 + i * C::SLAB;
+        // S^T per 32-key half h: A row m of block blk is key 32h + 8(m/4) + 4 blk + m%4
+        // of the slab, so accumulator element e&3 of block e>>2 is key 32h + 8 lg + e
+        f32x4_v sacc[2][2];
+        #pragma unroll
+        for (int h = 0; h < 2; ++h)
+            #pragma unroll
+            for (int blk = 0; blk < 2; ++blk) {
+                const int kr = 32 * h + 8 * (lr >> 2) + 4 * blk + (lr & 3);
+                sacc[h][blk] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+                #pragma unroll
+                for (int ks = 0; ks < KST; ++ks) {
+                    const bf16x8_v kf =
+                        *reinterpret_cast<const bf16x8_v *>(st + kr * C::RB + (((4 * ks + lg) ^ vk_swz(kr)) << 4));
+                    sacc[h][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sacc[h][blk], 0, 0, 0);
+                }
+            }
+        float sv[2][8];
+        float mt = -INFINITY;
+        const int kg0 = kb + 8 * lg;
+        if (__all(kb + C::SLAB <= k1 && kb + C::SLAB - 1 <= lim)) {
+            #pragma unroll
+            for (int h = 0; h < 2; ++h)
+                #pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    sv[h][j] = sacc[h][j >> 2][j & 3];
+                    mt = fmaxf(mt, sv[h][j]);
+                }
+        } else {
+            #pragma unroll
+            for (int h = 0; h < 2; ++h)
+                #pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int key = kg0 + 32 * h + j;
+                    const bool ok = (key < k1) & (key <= lim);
+                    sv[h][j] = ok ? sacc[h][j >> 2][j & 3] : -INFINITY;
+                    mt = fmaxf(mt, sv[h][j]);
+                }
+        }
+        mt = max_over_row_lanes(mt);
+        const float mn = fmaxf(m_run, mt);
+        const bool same = mn == m_run;
+        const float ms = (mn == -INFINITY) ? 0.f : mn * cs;
+        const float alpha = same ? 1.f : __builtin_amdgcn_exp2f(fmaf(m_run, cs, -ms));
+        m_run = mn;
+        float ps = 0.f;
+        bf16x8_v pf[2];
+        #pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t pk[4];
+            #pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[h][2 * e], cs, -ms));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[h][2 * e + 1], cs, -ms));
+                ps += p0 + p1;
+                pk[e] = cvt_pk_bf16(p0, p1);
+            }
+            pf[h] = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
+        }
+        l_run = fmaf(l_run, alpha, ps);
+        if (!__all(same)) {
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+        }
+        #pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int kg = kg0 + 32 * h;
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int f = db * 16 + lr;
+                u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + C::KBYTES + f * C::VROW + (((4 * h + lg) ^ (f & 7)) << 4));
+                if (kg + 8 > len) {   // values of keys past len may be anything: zero them
+                    #pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kk = kg + 2 * e;
+                        if (kk >= len) w[e] = 0u;
+                        else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
+                    }
+                }
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_v, w), pf[h], o[db], 0, 0, 0);
+            }
+        }
+    };
+
+    int issued = 0;
+    for (; issued < nsl && issued < C::NST - 1; ++issued) issue(issued);
+    for (int i = 0; i < nsl; ++i) {
+        wait_vm(C::IPW * (issued - 1 - i));   // slab i has landed (this wave's part)
+        __syncthreads();                      // ... every wave's part; stage (i-1) % NST is free
+        if (issued < nsl) {
+            issue(issued);
+            ++issued;
+        }
+        if (active) compute(i);
+    }
+
+    // ---- this wave's rows: partial (max in log2 units, sum, unnormalised o) ----
+    if (!active) return;
+    const float lt = sum_over_row_lanes(l_run);
+    if (row < R) {
+        float *po = a.part + (((size_t)u * a.n_splits + s) * a.part_rows + row) * D;
+        float *pml = a.part_ml + (((size_t)u * a.n_splits + s) * a.part_rows + row) * 2;
+        #pragma unroll
+        for (int db = 0; db < DB; ++db)
+            *reinterpret_cast<float4 *>(po + db * 16 + 4 * lg) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+        if (lg == 0) {
+            pml[0] = m_run == -INFINITY ? -INFINITY : m_run * cs;
+            pml[1] = lt;
+        }
+    }
+}
+
 // One workgroup (D threads) per (unit, query row): log-sum-exp merge of the
 // splits.  Threads first turn the splits' (max, sum) into weights in parallel,
 // then every thread sums its feature over the splits in batches of reads.
@@ -315,7 +527,7 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
 
 // ------------------------------------------------------------------ host ----
 
-VerifyPlan plan_verify(int B, int Hkv, const int *len) {
+VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len) {
     VerifyPlan p;
     p.units = B * Hkv;
     int n_max = 0;
@@ -324,8 +536,10 @@ VerifyPlan plan_verify(int B, int Hkv, const int *len) {
     if (ns > kVerifyMaxSplits) ns = kVerifyMaxSplits;
     if (ns < 1) ns = 1;
     int chunk = (n_max + ns - 1) / ns;
-    chunk = (chunk + 127) / 128 * 128;   // whole 32-key slabs for the four waves
-    if (chunk < 128) chunk = 128;
+    // whole slabs: 4 x 32 keys for the register-resident kernel, 64 for the LDS-staged one
+    const int gran = (!MAD_VERIFY_REGS && (T * G + 15) / 16 >= MAD_VERIFY_LDS_MIN_NB) ? 64 : 128;
+    chunk = (chunk + gran - 1) / gran * gran;
+    if (chunk < gran) chunk = gran;
     p.chunk = chunk;
     p.n_splits = (n_max + chunk - 1) / chunk;
     if (p.n_splits < 1) p.n_splits = 1;
@@ -354,6 +568,11 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
+    if (!MAD_VERIFY_REGS && NB >= MAD_VERIFY_LDS_MIN_NB) {
+        hipLaunchKernelGGL((verify_lds_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256),
+                           VerifyLdsCfg<D>::SMEM, st, a);
+        return hipGetLastError();
+    }
     constexpr int RP = NB * 16;
     const size_t lds = (size_t)4 * RP * 2 * 4 + (size_t)4 * RP * D * 4;
     hipLaunchKernelGGL((verify_split_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256), lds, st, a);
