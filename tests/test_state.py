@@ -98,3 +98,36 @@ def test_rollback_needs_ring_capacity():
     assert lay.rollback_ok(1000 + 5, 1001)
     lay = MemoryLayout(0, 128, 16, ring_cap=128 + 5 + 16, mem_cap=1000)
     assert lay.rollback_ok(1000 + 5, 1001)
+
+
+@pytest.mark.parametrize("S,W,r,u", [(0, 1024, 16, 4), (128, 128, 4, 1), (3, 7, 2, 3), (0, 8, 16, 1), (5, 40, 3, 2)])
+def test_step_views_match_paper_sets(S, W, r, u):
+    """The rows of a fused boundary launch: the raw view of p (mode 2) and
+    every new slot's write scope, with the current token taken from k_new
+    (mode 1) exactly when the scope ends at p."""
+    sets = MaswSets(S, W, r, u)
+    lay = MemoryLayout(S, W, r, ring_cap=W + r * u + 24, mem_cap=S + 4096, slots_per_update=u)
+    prefix = S + 3 * r * u + 1
+    emu = Emu(lay, prefix)
+    checked = 0
+    for p in range(prefix, prefix + 6 * r * u):
+        upd = lay.update_in_pass_of(p)
+        views, modes = (lay.step_views(p) if upd is not None else ([lay.decode_view(p)], [2]))
+        mem_seen, win_seen = emu.step(p)   # appends p and materialises the pass's slots
+        exp_mem, exp_win = _expected(sets, p)
+        assert modes[0] == 2 and mem_seen == exp_mem and win_seen == exp_win
+        if upd is None:
+            continue
+        assert len(views) == 1 + len(upd.positions)
+        for i, (v, mode) in enumerate(zip(views[1:], modes[1:])):
+            m = upd.first_slot + i
+            sv = sets.slot_scope(m)
+            mem = emu.mem[: v.mem_len]
+            win = [emu.ring[(v.win_start + t) % lay.ring_cap] for t in range(v.win_len)]
+            if mode == 1:
+                win = win + [p]
+            assert mode in (0, 1) and (mode == 1) == (sv.window and sv.window[-1] == p)
+            assert mem == [("sink", j) for j in sv.sink] + [("slot", j) for j in sv.slots], (p, m)
+            assert win == sv.window, (p, m)
+            checked += 1
+    assert checked >= 6
