@@ -42,13 +42,17 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
 
+#ifndef MAD_PREFILL_KT64
+#define MAD_PREFILL_KT64 64
+#endif
 template <int D>
 struct PrefillCfg {
-    static constexpr int KT = 64;                      // keys per tile
+    static constexpr int KT = D == 64 ? MAD_PREFILL_KT64 : 64;   // keys per tile (128 spills registers at d 64)
+    static constexpr int KH = KT / 32;                 // 32-key halves of a tile
     static constexpr int RB = D * 2;                   // bytes per K row
     static constexpr int CPR = RB / 16;                // 16-byte chunks per K row
     static constexpr int KTILE = KT * RB;              // K tile bytes
-    static constexpr int VROW = KT * 2;                // bytes per V^T row (one feature, 64 keys)
+    static constexpr int VROW = KT * 2;                // bytes per V^T row (one feature, KT keys)
     static constexpr int STAGE = 2 * KTILE;            // K tile + V^T tile (same size)
     static constexpr int SMEM = 2 * STAGE;
     static constexpr int KCH = KT * CPR / 256;         // K chunks per thread per tile
@@ -211,12 +215,12 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
         bool is_mem;
         int end;
         const int base = tile_base(t, is_mem, end);
-        // S^T = K Q^T for the tile's 64 keys: pair h holds keys 32h .. 32h+31;
+        // S^T = K Q^T for the tile's keys: half h holds keys 32h .. 32h+31;
         // A row m of block blk of pair h is key 32h + 8(m/4) + 4 blk + m%4, so
         // accumulator element e&3 of block e>>2 in lane group lg is key 32h + 8 lg + e
-        f32x4_v sacc[2][2][NB];
+        f32x4_v sacc[C::KH][2][NB];
         #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < C::KH; ++h)
             #pragma unroll
             for (int blk = 0; blk < 2; ++blk) {
                 const int kr = 32 * h + 8 * (lr >> 2) + 4 * blk + (lr & 3);
@@ -236,18 +240,18 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
         // The running max is kept on unscaled scores (the scale is positive);
         // p = 2^(s c - m c) is one fma into the exponential.  A tile inside
         // every row's visible range of this wave skips the masks.
-        bf16x8_v pf[NB][2];
+        bf16x8_v pf[NB][C::KH];
         const float cs = a.scale_log2;
         #pragma unroll
         for (int i = 0; i < NB; ++i) {
             const int lo = is_mem ? 0 : r_lo[i];
             const int hi = min(end, is_mem ? m_lim[i] : r_hi[i]);
             const bool full = __all(base >= lo && base + C::KT <= hi);
-            float sv16[2][8];
+            float sv16[C::KH][8];
             float mt = -INFINITY;
             if (full) {   // wave-uniform: no masks
                 #pragma unroll
-                for (int h = 0; h < 2; ++h)
+                for (int h = 0; h < C::KH; ++h)
                     #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         sv16[h][e] = sacc[h][e >> 2][i][e & 3];
@@ -255,7 +259,7 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
                     }
             } else {
                 #pragma unroll
-                for (int h = 0; h < 2; ++h)
+                for (int h = 0; h < C::KH; ++h)
                     #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const int key = base + 32 * h + 8 * lg + e;
@@ -271,7 +275,7 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
             m_run[i] = mn;
             float ps = 0.f;
             #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < C::KH; ++h) {
                 uint32_t pk[4];
                 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(256, NB == 2 ? 2 : 1) void prefill_kernel(const Pre
         }
         // O^T += V^T P^T: A = V^T rows (features db*16 + lr), keys 32h + 8 lg .. +7
         #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < C::KH; ++h)
             #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 const int f = db * 16 + lr;
