@@ -28,10 +28,6 @@ constexpr int kDecodeMaxSplits = 256;
 constexpr size_t kCounterRegionBytes = (size_t)1 << 20;
 constexpr int kCounterStride = 64;   // unsigned ints per counter line
 constexpr int kCounterLines = (int)(kCounterRegionBytes / (kCounterStride * 4));
-#ifndef MAD_ARRIVE_GROUP
-#define MAD_ARRIVE_GROUP 8
-#endif
-constexpr int kArriveGroup = MAD_ARRIVE_GROUP;   // splits per arrival group
 
 struct DecodeArgs {
     const void *q;
