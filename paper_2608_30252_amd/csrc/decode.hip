@@ -169,7 +169,8 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
 
     constexpr int SPL = kDecodeMaxSplits / 64;
     constexpr int FPL = D / 64;   // features per lane
-    constexpr int SB = 8;         // splits whose rows are read together
+    constexpr int SB = 16;        // splits whose rows are read together
+    constexpr int NA = 4;         // independent accumulators per feature (short dependency chains)
     for (int g = wave; g < G; g += NT / 64) {
         float2 ml[SPL];
         float mloc = -INFINITY;
@@ -190,9 +191,11 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
         const float inv = L > 0.f ? 1.f / L : 0.f;
         if (lse && lane == 0) lse[g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 
-        float acc[FPL];
+        float acc[NA][FPL];
         #pragma unroll
-        for (int f = 0; f < FPL; ++f) acc[f] = 0.f;
+        for (int k = 0; k < NA; ++k)
+            #pragma unroll
+            for (int f = 0; f < FPL; ++f) acc[k][f] = 0.f;
         const float *og = lo + (size_t)g * D + lane * FPL;
         #pragma unroll
         for (int i = 0; i < SPL; ++i) {
@@ -211,20 +214,23 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
                 #pragma unroll
                 for (int k = 0; k < SB; ++k)
                     #pragma unroll
-                    for (int f = 0; f < FPL; ++f) acc[f] = fmaf(ws[k], ov[k][f], acc[f]);
+                    for (int f = 0; f < FPL; ++f) acc[k % NA][f] = fmaf(ws[k], ov[k][f], acc[k % NA][f]);
             }
             for (; j < cnt; ++j) {
                 const float ws = read_lane(w[i], j);
                 #pragma unroll
-                for (int f = 0; f < FPL; ++f) acc[f] = fmaf(ws, og[(size_t)(s0 + j) * G * D + f], acc[f]);
+                for (int f = 0; f < FPL; ++f) acc[0][f] = fmaf(ws, og[(size_t)(s0 + j) * G * D + f], acc[0][f]);
             }
         }
+        float accs[FPL];
+        #pragma unroll
+        for (int f = 0; f < FPL; ++f) accs[f] = (acc[0][f] + acc[1][f]) + (acc[2][f] + acc[3][f]);
         T *og_out = out + (size_t)g * D + lane * FPL;
         if constexpr (std::is_same<T, bf16_t>::value && FPL == 2) {
-            *reinterpret_cast<uint32_t *>(og_out) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+            *reinterpret_cast<uint32_t *>(og_out) = pack_bf16x2(accs[0] * inv, accs[1] * inv);
         } else {
             #pragma unroll
-            for (int f = 0; f < FPL; ++f) Elem<T>::store1(og_out + f, acc[f] * inv);
+            for (int f = 0; f < FPL; ++f) Elem<T>::store1(og_out + f, accs[f] * inv);
         }
     }
 }
