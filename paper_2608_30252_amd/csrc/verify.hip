@@ -31,23 +31,27 @@ namespace mad {
 #define MAD_VERIFY_REGS 0   // 1: the register-resident split kernel for every shape
 #endif
 #ifndef MAD_VERIFY_LDS_MIN_NB
-#define MAD_VERIFY_LDS_MIN_NB 3   // query row blocks from which the LDS-staged kernel is used
+#define MAD_VERIFY_LDS_MIN_NB 2   // query row blocks from which the LDS-staged kernel is used
 #endif
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
 
+// Lanes l, l^16, l^32, l^48 hold the same query row.  v_permlane16_swap and
+// v_permlane32_swap (VALU lane swaps of gfx950) give every lane the values of
+// lanes l & ~16 and l | 16 (resp. 32), so two swaps reduce over the four.
 __device__ __forceinline__ float max_over_row_lanes(float v) {
-    // lanes l, l^16, l^32, l^48 hold the same query row
-    v = fmaxf(v, xor_lane<16>(v));
-    v = fmaxf(v, xor_lane<32>(v));
-    return v;
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float sum_over_row_lanes(float v) {
-    v += xor_lane<16>(v);
-    v += xor_lane<32>(v);
-    return v;
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // slabs per wave in flight or in use: three where the registers allow it
@@ -267,15 +271,18 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
 // copy of the output accumulators in every wave (the waves split keys), which
 // leaves room for one or two 32-key slabs in flight per wave: with HBM latency
 // under load of several microseconds that caps the stream.  Here the waves
-// split the query rows instead (wave w owns 16-row block w) and share every
-// K/V slab through a deep LDS ring filled by direct loads
-// (global_load_lds_dwordx4, issued by all four waves), so about
-// (NST - 1) x 16 KB are in flight per workgroup:
+// split the query rows and the keys of every slab -- wave w < 2 NB owns 16-row
+// block w % NB and the 32-key half w / NB of each 64-key slab; with two waves
+// per SIMD one wave's exponentials and matrix products overlap another's -- and share
+// every K/V slab through a deep LDS ring filled by direct loads
+// (global_load_lds_dwordx4, issued by all eight waves), so about
+// (NST - 1) x 32 KB are in flight per workgroup:
 //   * K rows land with their 16-byte chunks XOR-swizzled by row, so the
 //     permuted-row A operand reads of S^T = K Q^T are conflict-free;
-//   * V^T rows (one feature, the slab's 32 keys) land with their 16-byte
+//   * V^T rows (one feature, the slab's 64 keys) land with their 16-byte
 //     key chunks swizzled by feature for the A operand of O^T = V^T P^T;
-//   * one barrier per slab; each wave writes its rows' partial (max, sum, o).
+//   * one barrier per slab; at the end the two key halves of each row block
+//     are merged in LDS and the rows' partial (max, sum, o) is written.
 template <int D>
 struct VerifyLdsCfg {
     static constexpr int SLAB = 64;                        // keys per slab (128 contiguous bytes of each V^T row)
@@ -284,14 +291,16 @@ struct VerifyLdsCfg {
     static constexpr int VROW = SLAB * 2;                  // bytes per V^T row in a stage
     static constexpr int STAGE = 2 * KBYTES;
     static constexpr int NST = D == 128 ? 4 : 8;           // ring stages (128 KB)
-    static constexpr int IPW = STAGE / 1024 / 4;           // direct loads per wave per slab
+    static constexpr int NWV = 8;                          // waves: 4 row blocks x 2 key halves
+    static constexpr int IPW = STAGE / 1024 / NWV;         // direct loads per wave per slab
     static constexpr int SMEM = NST * STAGE;
+    static_assert(IPW % 2 == 0, "K and V loads per wave");
 };
 
 __device__ __forceinline__ int vk_swz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
 
 template <int D, int NB>
-__global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) {
+__global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) {
     using C = VerifyLdsCfg<D>;
     constexpr int KST = D / 32, DB = D / 16, CPR = D / 8;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -306,11 +315,14 @@ __global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) 
     const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
     const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
     const int lr = lane & 15, lg = lane >> 4;
-    const bool active = wave < NB;
+    // waves 0 .. 2 NB - 1 compute (row block wave % NB, key half wave / NB), so
+    // consecutive waves -- on different SIMDs -- take different row blocks
+    const int rbw = wave % NB, kh = wave / NB;
+    const bool active = wave < 2 * NB;
 
-    // ---- this wave's query fragments and causal limit (row block `wave`) ----
+    // ---- this wave's query fragments and causal limit (row block rbw) ----
     bf16x8_v qf[KST];
-    const int row = wave * 16 + lr;
+    const int row = rbw * 16 + lr;
     int lim = 0x7fffffff;
     if (active && row < R) {
         const int t = row / G, g = row - t * G;
@@ -356,43 +368,38 @@ __global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) 
     auto compute = [&](int i) {
         const unsigned char *st = smem + (i % C::NST) * C::STAGE;
         const int kb = k0 + i * C::SLAB;
-        // S^T per 32-key half h: A row m of block blk is key 32h + 8(m/4) + 4 blk + m%4
-        // of the slab, so accumulator element e&3 of block e>>2 is key 32h + 8 lg + e
-        f32x4_v sacc[2][2];
+        // S^T for this wave's 32-key half: A row m of block blk is key
+        // 32 kh + 8(m/4) + 4 blk + m%4 of the slab, so accumulator element e&3 of
+        // block e>>2 is key 32 kh + 8 lg + e
+        f32x4_v sacc[2];
         #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int blk = 0; blk < 2; ++blk) {
+            const int kr = 32 * kh + 8 * (lr >> 2) + 4 * blk + (lr & 3);
+            sacc[blk] = f32x4_v{0.f, 0.f, 0.f, 0.f};
             #pragma unroll
-            for (int blk = 0; blk < 2; ++blk) {
-                const int kr = 32 * h + 8 * (lr >> 2) + 4 * blk + (lr & 3);
-                sacc[h][blk] = f32x4_v{0.f, 0.f, 0.f, 0.f};
-                #pragma unroll
-                for (int ks = 0; ks < KST; ++ks) {
-                    const bf16x8_v kf =
-                        *reinterpret_cast<const bf16x8_v *>(st + kr * C::RB + (((4 * ks + lg) ^ vk_swz(kr)) << 4));
-                    sacc[h][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sacc[h][blk], 0, 0, 0);
-                }
+            for (int ks = 0; ks < KST; ++ks) {
+                const bf16x8_v kf =
+                    *reinterpret_cast<const bf16x8_v *>(st + kr * C::RB + (((4 * ks + lg) ^ vk_swz(kr)) << 4));
+                sacc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sacc[blk], 0, 0, 0);
             }
-        float sv[2][8];
+        }
+        float sv[8];
         float mt = -INFINITY;
-        const int kg0 = kb + 8 * lg;
+        const int kg = kb + 32 * kh + 8 * lg;
         if (__all(kb + C::SLAB <= k1 && kb + C::SLAB - 1 <= lim)) {
             #pragma unroll
-            for (int h = 0; h < 2; ++h)
-                #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    sv[h][j] = sacc[h][j >> 2][j & 3];
-                    mt = fmaxf(mt, sv[h][j]);
-                }
+            for (int j = 0; j < 8; ++j) {
+                sv[j] = sacc[j >> 2][j & 3];
+                mt = fmaxf(mt, sv[j]);
+            }
         } else {
             #pragma unroll
-            for (int h = 0; h < 2; ++h)
-                #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int key = kg0 + 32 * h + j;
-                    const bool ok = (key < k1) & (key <= lim);
-                    sv[h][j] = ok ? sacc[h][j >> 2][j & 3] : -INFINITY;
-                    mt = fmaxf(mt, sv[h][j]);
-                }
+            for (int j = 0; j < 8; ++j) {
+                const int key = kg + j;
+                const bool ok = (key < k1) & (key <= lim);
+                sv[j] = ok ? sacc[j >> 2][j & 3] : -INFINITY;
+                mt = fmaxf(mt, sv[j]);
+            }
         }
         mt = max_over_row_lanes(mt);
         const float mn = fmaxf(m_run, mt);
@@ -401,41 +408,33 @@ __global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) 
         const float alpha = same ? 1.f : __builtin_amdgcn_exp2f(fmaf(m_run, cs, -ms));
         m_run = mn;
         float ps = 0.f;
-        bf16x8_v pf[2];
+        uint32_t pk[4];
         #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            uint32_t pk[4];
-            #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[h][2 * e], cs, -ms));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[h][2 * e + 1], cs, -ms));
-                ps += p0 + p1;
-                pk[e] = cvt_pk_bf16(p0, p1);
-            }
-            pf[h] = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
+        for (int e = 0; e < 4; ++e) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e], cs, -ms));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[2 * e + 1], cs, -ms));
+            ps += p0 + p1;
+            pk[e] = cvt_pk_bf16(p0, p1);
         }
+        const bf16x8_v pf = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
         l_run = fmaf(l_run, alpha, ps);
         if (!__all(same)) {
             #pragma unroll
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
         }
         #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int kg = kg0 + 32 * h;
-            #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int f = db * 16 + lr;
-                u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + C::KBYTES + f * C::VROW + (((4 * h + lg) ^ (f & 7)) << 4));
-                if (kg + 8 > len) {   // values of keys past len may be anything: zero them
-                    #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int kk = kg + 2 * e;
-                        if (kk >= len) w[e] = 0u;
-                        else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
-                    }
+        for (int db = 0; db < DB; ++db) {
+            const int f = db * 16 + lr;
+            u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + C::KBYTES + f * C::VROW + (((4 * kh + lg) ^ (f & 7)) << 4));
+            if (kg + 8 > len) {   // values of keys past len may be anything: zero them
+                #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int kk = kg + 2 * e;
+                    if (kk >= len) w[e] = 0u;
+                    else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
                 }
-                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_v, w), pf[h], o[db], 0, 0, 0);
             }
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_v, w), pf, o[db], 0, 0, 0);
         }
     };
 
@@ -451,19 +450,40 @@ __global__ __launch_bounds__(256, 1) void verify_lds_kernel(const VerifyArgs a) 
         if (active) compute(i);
     }
 
-    // ---- this wave's rows: partial (max in log2 units, sum, unnormalised o) ----
-    if (!active) return;
+    // ---- merge the two key halves of each row block, then the rows' partial
+    // (max in log2 units, sum, unnormalised o) ----
     const float lt = sum_over_row_lanes(l_run);
-    if (row < R) {
-        float *po = a.part + (((size_t)u * a.n_splits + s) * a.part_rows + row) * D;
-        float *pml = a.part_ml + (((size_t)u * a.n_splits + s) * a.part_rows + row) * 2;
+    const float msc = m_run == -INFINITY ? -INFINITY : m_run * cs;
+    __syncthreads();   // every wave is done with the ring
+    float *xo = reinterpret_cast<float *>(smem);   // [4][16][D]: the second halves' o
+    float *xml = xo + 4 * 16 * D;                  // [4][16][2]: their (max, sum)
+    if (active && kh == 1) {
         #pragma unroll
         for (int db = 0; db < DB; ++db)
-            *reinterpret_cast<float4 *>(po + db * 16 + 4 * lg) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+            *reinterpret_cast<float4 *>(xo + (size_t)row * D + db * 16 + 4 * lg) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
         if (lg == 0) {
-            pml[0] = m_run == -INFINITY ? -INFINITY : m_run * cs;
-            pml[1] = lt;
+            xml[2 * row] = msc;
+            xml[2 * row + 1] = lt;
         }
+    }
+    __syncthreads();
+    if (!active || kh == 1 || row >= R) return;
+    const float m1 = xml[2 * row], l1 = xml[2 * row + 1];
+    const float M = fmaxf(msc, m1);
+    const float w0 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(msc - M);
+    const float w1 = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+    float *po = a.part + (((size_t)u * a.n_splits + s) * a.part_rows + row) * D;
+    float *pml = a.part_ml + (((size_t)u * a.n_splits + s) * a.part_rows + row) * 2;
+    #pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        const float4 x = *reinterpret_cast<const float4 *>(xo + (size_t)row * D + db * 16 + 4 * lg);
+        *reinterpret_cast<float4 *>(po + db * 16 + 4 * lg) =
+            make_float4(fmaf(w0, o[db][0], w1 * x.x), fmaf(w0, o[db][1], w1 * x.y), fmaf(w0, o[db][2], w1 * x.z),
+                        fmaf(w0, o[db][3], w1 * x.w));
+    }
+    if (lg == 0) {
+        pml[0] = M;
+        pml[1] = fmaf(w0, lt, w1 * l1);
     }
 }
 
@@ -569,8 +589,8 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
     if (!MAD_VERIFY_REGS && NB >= MAD_VERIFY_LDS_MIN_NB) {
-        hipLaunchKernelGGL((verify_lds_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)), dim3(256),
-                           VerifyLdsCfg<D>::SMEM, st, a);
+        hipLaunchKernelGGL((verify_lds_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)),
+                           dim3(64 * VerifyLdsCfg<D>::NWV), VerifyLdsCfg<D>::SMEM, st, a);
         return hipGetLastError();
     }
     constexpr int RP = NB * 16;
