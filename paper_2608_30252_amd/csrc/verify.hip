@@ -488,8 +488,10 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
 }
 
 // One workgroup (D threads) per (unit, query row): log-sum-exp merge of the
-// splits.  Threads first turn the splits' (max, sum) into weights in parallel,
-// then every thread sums its feature over the splits in batches of reads.
+// splits.  Every thread first issues the reads of its feature in the first MB
+// splits (they do not depend on the weights, so their round trip overlaps the
+// one of the (max, sum) pairs), the threads turn the splits' (max, sum) into
+// weights in parallel, then every thread sums its feature over the splits.
 template <int D>
 __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     const int R = a.T * a.G;
@@ -504,6 +506,11 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     const size_t so = (size_t)a.part_rows * D, sml = (size_t)a.part_rows * 2;
     __shared__ float s_w[kVerifyMaxSplits];
     __shared__ float s_red[2][NW];
+
+    constexpr int MB = 32;   // splits whose feature values are read ahead
+    float v[MB];
+    #pragma unroll
+    for (int e = 0; e < MB; ++e) v[e] = e < ns ? po[e * so] : 0.f;
 
     // split weights: thread i handles splits i and i + D (ns <= kVerifyMaxSplits <= 2 D)
     float m0 = -INFINITY, m1 = -INFINITY, l0 = 0.f, l1 = 0.f;
@@ -532,16 +539,20 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     if (tid + D < ns) s_w[tid + D] = w1 * inv;
     __syncthreads();
 
-    float acc = 0.f;
-    for (int s0 = 0; s0 < ns; s0 += 8) {
-        float v[8];
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+    for (int e = 0; e < MB; ++e)
+        if (e < ns) acc[e & 3] = fmaf(s_w[e], v[e], acc[e & 3]);
+    for (int s0 = MB; s0 < ns; s0 += 8) {
+        float x[8];
         #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = s0 + e < ns ? po[(s0 + e) * so] : 0.f;
+        for (int e = 0; e < 8; ++e) x[e] = s0 + e < ns ? po[(s0 + e) * so] : 0.f;
         #pragma unroll
-        for (int e = 0; e < 8; ++e) if (s0 + e < ns) acc = fmaf(s_w[s0 + e], v[e], acc);
+        for (int e = 0; e < 8; ++e) if (s0 + e < ns) acc[e & 3] = fmaf(s_w[s0 + e], x[e], acc[e & 3]);
     }
+    const float accs = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     const size_t head = ((size_t)b * a.T + t) * a.Hq + (size_t)c * a.G + g;
-    reinterpret_cast<bf16_t *>(a.out)[head * D + tid].bits = f32_to_bf16(acc);
+    reinterpret_cast<bf16_t *>(a.out)[head * D + tid].bits = f32_to_bf16(accs);
     if (a.lse && tid == 0) a.lse[head] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 
