@@ -25,9 +25,11 @@
 //     operand reads of S^T = K Q^T are conflict-free; the A rows are permuted
 //     so that each lane's S^T accumulators hold the 8 consecutive keys that
 //     the PV product's B operand needs (no shuffle of probabilities);
-//   * V is written transposed into LDS ([feature][key], 16-byte key chunks
-//     swizzled by feature), so the A operand of O^T = V^T P^T is one 16-byte
-//     read of 8 consecutive keys;
+//   * V rows are stored as they are (16-byte chunks XOR-swizzled by row), and
+//     the A operand of O^T = V^T P^T -- 8 consecutive keys of one feature --
+//     comes from two transposing LDS reads (ds_read_b64_tr_b16: lane 4e + a of
+//     a 16-lane group names features 4a .. 4a+3 of key row e, and lane 4a + b
+//     receives feature 4a + b of the four rows);
 //   * online softmax per query row (16 scores per lane per tile, two
 //     cross-lane steps); one barrier per tile.
 // Query blocks of every unit are dealt round-robin over the units (with a
@@ -52,16 +54,23 @@ struct PrefillCfg {
     static constexpr int RB = D * 2;                   // bytes per K row
     static constexpr int CPR = RB / 16;                // 16-byte chunks per K row
     static constexpr int KTILE = KT * RB;              // K tile bytes
-    static constexpr int VROW = KT * 2;                // bytes per V^T row (one feature, KT keys)
-    static constexpr int STAGE = 2 * KTILE;            // K tile + V^T tile (same size)
+    static constexpr int STAGE = 2 * KTILE;            // K tile + V tile (same size)
     static constexpr int SMEM = 2 * STAGE;
     static constexpr int KCH = KT * CPR / 256;         // K chunks per thread per tile
-    static constexpr int VCH = KT * (D / 8) / 256;     // V chunks per thread per tile
+    static constexpr int VCH = KCH;                    // V chunks per thread per tile
 };
 
 // swizzle of K row k's 16-byte chunks: distinct for the 8 rows one group of
 // eight lanes reads (k mod 4 and bit 3 of k vary across them)
 __device__ __forceinline__ int k_swz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+// swizzle of V row k's 16-byte chunks: a transposing read of 16 lanes covers
+// rows k0 .. k0+3 (k0 a multiple of 4) x two adjacent chunks; XOR with
+// 2 (k mod 4) spreads the eight (row, chunk) pairs over distinct banks
+__device__ __forceinline__ int v_swz(int k) { return (k & 3) << 1; }
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4s_t lds_read_tr16(const unsigned char *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s_t *)(p));
+}
 
 __device__ __forceinline__ float prefill_row_max(float v) {
     // lanes l, l^16, l^32, l^48 hold the same query row
@@ -181,7 +190,7 @@ __global__ __launch_bounds__(256, NB == 2 ? (D == 64 ? 3 : 2) : 1) void prefill_
         }
         #pragma unroll
         for (int i = 0; i < C::VCH; ++i) {
-            const int idx = tid + 256 * i, row = idx % C::KT, ch = idx / C::KT;
+            const int idx = tid + 256 * i, row = idx / C::CPR, ch = idx % C::CPR;
             const int key = min(base + row, end - 1);
             r.v[i] = *reinterpret_cast<const uint4 *>(vs + (size_t)key * D + ch * 8);
         }
@@ -196,14 +205,8 @@ __global__ __launch_bounds__(256, NB == 2 ? (D == 64 ? 3 : 2) : 1) void prefill_
         }
         #pragma unroll
         for (int i = 0; i < C::VCH; ++i) {
-            const int idx = tid + 256 * i, row = idx % C::KT, ch = idx / C::KT;
-            const uint32_t w[4] = {r.v[i].x, r.v[i].y, r.v[i].z, r.v[i].w};
-            // feature ch*8 + e, key `row`: V^T row (ch*8 + e), key chunk row/8 swizzled by e
-            #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint16_t h = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
-                *reinterpret_cast<uint16_t *>(sv + (ch * 8 + e) * C::VROW + ((((row >> 3) ^ e)) << 4) + (row & 7) * 2) = h;
-            }
+            const int idx = tid + 256 * i, row = idx / C::CPR, ch = idx % C::CPR;
+            *reinterpret_cast<uint4 *>(sv + row * C::RB + ((ch ^ v_swz(row)) << 4)) = r.v[i];
         }
     };
 
@@ -297,13 +300,18 @@ __global__ __launch_bounds__(256, NB == 2 ? (D == 64 ? 3 : 2) : 1) void prefill_
             #pragma unroll
             for (int db = 0; db < DB; ++db) o[db][i] *= alpha;
         }
-        // O^T += V^T P^T: A = V^T rows (features db*16 + lr), keys 32h + 8 lg .. +7
+        // O^T += V^T P^T: A = V^T rows (features db*16 + lr), keys 32h + 8 lg .. +7,
+        // from the transposing reads of key rows 32h + 8 lg + {0..3} and {4..7}
+        const int tr_row = 8 * lg + (lr >> 2), tr_byte = 8 * (lr & 3);
         #pragma unroll
         for (int h = 0; h < C::KH; ++h)
             #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                const int f = db * 16 + lr;
-                const bf16x8_v vf = *reinterpret_cast<const bf16x8_v *>(sv + f * C::VROW + (((4 * h + lg) ^ (f & 7)) << 4));
+                const int byte = db * 32 + tr_byte, chunk = byte >> 4, half = byte & 8;
+                const int r0 = 32 * h + tr_row, r1 = r0 + 4;
+                const v4s_t lo = lds_read_tr16(sv + r0 * C::RB + ((chunk ^ v_swz(r0)) << 4) + half);
+                const v4s_t hi = lds_read_tr16(sv + r1 * C::RB + ((chunk ^ v_swz(r1)) << 4) + half);
+                const bf16x8_v vf = __builtin_bit_cast(bf16x8_v, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
                 #pragma unroll
                 for (int i = 0; i < NB; ++i) o[db][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i][h], o[db][i], 0, 0, 0);
             }
