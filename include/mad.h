@@ -193,7 +193,7 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
  *   logits    device [B][T][V], dtype F32 or BF16
  *   draft_tok device int32 [B][T-1] (may be NULL when T == 1)
  *   n_accept, next_tok  device int32 [B]
- * V >= 1, T >= 1.
+ * V >= 1, 1 <= T <= 256.
  */
 int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok,
                       int B, int T, int V, int32_t *n_accept, int32_t *next_tok,

@@ -11,9 +11,11 @@
 // index in the low word.  The row argmax is then the maximum key: ties go to
 // the lowest index, the first NaN wins.
 //
-// One launch: workgroup (chunk, row) reduces a chunk of the vocabulary; the
-// last chunk of a row (arrival counter) reduces the row; the last row to
-// finish applies the accept rule for every sequence.
+// One launch: workgroup (chunk, row) reduces a chunk of the vocabulary and
+// folds its key into the row's key with a 64-bit atomic max; the last
+// workgroup of a sequence (arrival counter over its T rows and all chunks)
+// applies the accept rule to the sequence and clears the row keys for the
+// next call.
 //
 // Stochastic accept/reject (the rejection-sampling rule the target applies,
 // Sec. 2.1 and Sec. 3.3) with caller-supplied uniforms: drafted token x_i is
@@ -58,6 +60,9 @@ __device__ __forceinline__ void store_agent_u64(uint64_t *p, uint64_t v) {
 }
 __device__ __forceinline__ uint64_t load_agent_u64(const uint64_t *p) {
     return __hip_atomic_load(const_cast<uint64_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t max_agent_u64(uint64_t *p, uint64_t v) {
+    return __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename T>
@@ -108,67 +113,51 @@ __global__ __launch_bounds__(256) void accept_kernel(const AcceptArgs a) {
     if (tid == 0) {
         uint64_t m = s_w[0];
         for (int w = 1; w < 4; ++w) m = s_w[w] > m ? s_w[w] : m;
-        store_agent_u64(a.part + (size_t)row * a.n_chunks + chunk, m);
-    }
-    wait_vm_stores();
-    __syncthreads();
-    if (tid == 0) {
-        unsigned *cnt = a.counters + (size_t)row * kCounterStride;
-        const int last = arrive(cnt) == (unsigned)(a.n_chunks - 1);
+        // the returned value is awaited: the max is performed before the arrival
+        (void)max_agent_u64(a.row_best + row, m);
+        const int b = row / a.T;
+        unsigned *cnt = a.counters + (size_t)b * kCounterStride;
+        const int last = arrive(cnt) == (unsigned)(a.T * a.n_chunks - 1);
         if (last) reset_counter(cnt);
         s_flag = last;
     }
     __syncthreads();
     if (!s_flag) return;
 
-    // ---- last chunk of this row: reduce the row ----
-    uint64_t rb = 0;
-    for (int c = tid; c < a.n_chunks; c += 256) {
-        const uint64_t k = load_agent_u64(a.part + (size_t)row * a.n_chunks + c);
-        rb = k > rb ? k : rb;
+    // ---- last workgroup of sequence b: the accept rule, then clear its row keys ----
+    // thread t reads row t's key (all in one round trip); the first t < T-1
+    // whose drafted token differs from the row's argmax is the rejection
+    __shared__ int s_first;
+    __shared__ uint64_t s_keys[kAcceptMaxT];
+    const int b = row / a.T;
+    uint64_t *rbp = a.row_best + (size_t)b * a.T;
+    if (tid == 0) s_first = a.T - 1;
+    __syncthreads();
+    if (tid < a.T) {
+        const uint64_t k = load_agent_u64(rbp + tid);
+        s_keys[tid] = k;
+        if (tid < a.T - 1 && a.draft[(size_t)b * (a.T - 1) + tid] != key_index(k)) atomicMin(&s_first, tid);
+        store_agent_u64(rbp + tid, 0);   // the next call starts from zero keys
     }
-    rb = wave_max_u64(rb);
-    if (lane == 0) s_w[wave] = rb;
     __syncthreads();
     if (tid == 0) {
-        uint64_t m = s_w[0];
-        for (int w = 1; w < 4; ++w) m = s_w[w] > m ? s_w[w] : m;
-        store_agent_u64(a.row_best + row, m);
-    }
-    wait_vm_stores();
-    __syncthreads();
-    if (tid == 0) {
-        unsigned *cnt = a.counters + (size_t)rows * kCounterStride;
-        const int last = arrive(cnt) == (unsigned)(rows - 1);
-        if (last) reset_counter(cnt);
-        s_flag = last;
-    }
-    __syncthreads();
-    if (!s_flag) return;
-
-    // ---- last row overall: the accept rule for every sequence ----
-    for (int b = tid; b < a.B; b += 256) {
-        int acc = 0;
-        const uint64_t *rbp = a.row_best + (size_t)b * a.T;
-        while (acc < a.T - 1 && a.draft[(size_t)b * (a.T - 1) + acc] == key_index(load_agent_u64(rbp + acc))) ++acc;
+        const int acc = s_first;
         a.n_accept[b] = acc;
-        a.next_tok[b] = key_index(load_agent_u64(rbp + acc));
+        a.next_tok[b] = key_index(s_keys[acc]);
     }
 }
 
 // ------------------------------------------------------------------ host ----
 
+// Only the counter region: line b holds sequence b's arrivals, and the row
+// keys sit in the lines after line B-1.  That region is zero between calls
+// (every kernel of the library leaves it so), which the atomic maxima need;
+// the rest of a shared workspace holds other calls' partials.
 size_t accept_ws_bytes(int B, int T, int V) {
-    const size_t rows = (size_t)B * T;
-    const size_t chunks = ((size_t)V + kAcceptChunk - 1) / kAcceptChunk;
-    return kCounterRegionBytes + align256(rows * chunks * 8) + align256(rows * 8);
-}
-
-void accept_ws_layout(int B, int T, int V, size_t *off_part, size_t *off_rows) {
-    const size_t rows = (size_t)B * T;
-    const size_t chunks = ((size_t)V + kAcceptChunk - 1) / kAcceptChunk;
-    *off_part = kCounterRegionBytes;
-    *off_rows = kCounterRegionBytes + align256(rows * chunks * 8);
+    (void)B;
+    (void)T;
+    (void)V;
+    return kCounterRegionBytes;
 }
 
 // ---------------------------------------------------------- stochastic ----

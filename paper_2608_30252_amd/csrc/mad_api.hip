@@ -471,7 +471,7 @@ int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *
 int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, int B, int T, int V,
                       int32_t *n_accept, int32_t *next_tok, void *ws, size_t ws_bytes, void *stream) {
     if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
-    if (T < 1 || (size_t)B * T + 1 > (size_t)mad::kCounterLines) return fail(MAD_EINVAL, "T=%d", T);
+    if (T < 1 || T > mad::kAcceptMaxT) return fail(MAD_EINVAL, "T=%d outside [1, %d]", T, mad::kAcceptMaxT);
     if (V < 1) return fail(MAD_EINVAL, "V=%d", V);
     if (dtype != MAD_F32 && dtype != MAD_BF16) return fail(MAD_ENOTSUP, "dtype %d not supported", dtype);
     if (!logits || !n_accept || !next_tok) return fail(MAD_EINVAL, "null logits, n_accept or next_tok");
@@ -486,10 +486,7 @@ int mad_accept_greedy(const void *logits, int dtype, const int32_t *draft_tok, i
     a.draft = draft_tok;
     a.n_accept = n_accept;
     a.next_tok = next_tok;
-    size_t off_part, off_rows;
-    mad::accept_ws_layout(B, T, V, &off_part, &off_rows);
-    a.part = (uint64_t *)((char *)ws + off_part);
-    a.row_best = (uint64_t *)((char *)ws + off_rows);
+    a.row_best = (uint64_t *)((char *)ws + (size_t)B * mad::kCounterStride * 4);   // inside the counter region
     a.counters = (unsigned *)ws;
     a.B = B;
     a.T = T;

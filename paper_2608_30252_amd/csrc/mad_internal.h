@@ -150,20 +150,21 @@ hipError_t launch_verify(const VerifyArgs &a, hipStream_t st);
 
 // ---------------------------------------------------------------- accept ----
 constexpr int kAcceptChunk = 8192;   // vocabulary entries per workgroup
+constexpr int kAcceptMaxT = 256;     // rows per sequence of the greedy rule (one workgroup applies it)
+static_assert((size_t)kMaxB * kCounterStride * 4 + (size_t)kMaxB * kAcceptMaxT * 8 <= kCounterRegionBytes,
+              "greedy-accept counters and row keys fit the counter region");
 
 struct AcceptArgs {
     const void *logits;
     const int32_t *draft;      // [B][T-1] device
     int32_t *n_accept, *next_tok;
-    uint64_t *part;            // [rows][n_chunks] chunk argmax keys
-    uint64_t *row_best;        // [rows] row argmax keys
-    unsigned *counters;        // lines 0..rows-1: per row; line rows: all rows
+    uint64_t *row_best;        // [rows] row argmax keys, in the counter region after line B-1 (zero between calls)
+    unsigned *counters;        // line b: arrivals of sequence b's workgroups
     int B, T, V, n_chunks;
     int vec16;                 // rows 16-byte aligned and V a multiple of 16 / element size
 };
 
 size_t accept_ws_bytes(int B, int T, int V);
-void accept_ws_layout(int B, int T, int V, size_t *off_part, size_t *off_rows);
 hipError_t launch_accept(const AcceptArgs &a, int dtype, hipStream_t st);
 
 struct StochArgs {

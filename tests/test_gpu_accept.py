@@ -99,3 +99,30 @@ def test_small_vocab_and_repeated_calls_share_workspace():
         na_ref, nx_ref = oracle.accept_greedy(x, draft)
         np.testing.assert_array_equal(na, na_ref)
         np.testing.assert_array_equal(nx, nx_ref)
+
+
+def test_workspace_shared_with_decode_and_garbage_past_the_counters():
+    """The row keys live in the counter region, which every call leaves at
+    zero; whatever other calls left in the rest of a shared workspace (here: a
+    decode's split partials, then 0xFF bytes) must not leak into the argmax."""
+    import oracle
+    import paper_2608_30252_amd as mad
+    from paper_2608_30252_amd import synth
+    dev = torch.device("cuda")
+    ws = torch.zeros(4 << 20, dtype=torch.uint8, device=dev)
+    # a decode with many splits writes partials after the counter region
+    q = synth.normal((1, 32, 64), 901).to(dev)
+    kv = synth.normal((1, 8, 4096, 64), 902).to(dev)
+    mad.draft_decode_attn(q, None, mad.KV(kv, kv, [4096], [0]), ws=ws)
+    B, T, V = 3, 5, 30000
+    x = np.random.default_rng(9).standard_normal((B, T, V)).astype(np.float32)
+    draft, _ = _planted(x, seed=9)
+    for fill in (None, 0xFF):
+        if fill is not None:
+            ws[1 << 20:] = fill
+        na, nx = mad.accept_greedy(torch.from_numpy(x).to(dev), torch.from_numpy(draft).to(dev), ws=ws)
+        torch.cuda.synchronize()
+        na_ref, nx_ref = oracle.accept_greedy(x, draft)
+        np.testing.assert_array_equal(na.cpu().numpy(), na_ref)
+        np.testing.assert_array_equal(nx.cpu().numpy(), nx_ref)
+    assert int(ws[: 1 << 20].count_nonzero()) == 0   # counters and row keys left at zero
