@@ -98,7 +98,7 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
             if (B < 1 || B > MAD_MAX_BATCH || max_keys < 1) return 0;
             return mad::stoch_ws_bytes(B, max_keys);
         case MAD_OP_ACCEPT:   // B, T, max_keys = V
-            if (B < 1 || T < 1 || max_keys < 1) return 0;
+            if (B < 1 || B > MAD_MAX_BATCH || T < 1 || T > mad::kAcceptMaxT || max_keys < 1) return 0;
             return mad::accept_ws_bytes(B, T, max_keys);
         default:
             return 0;

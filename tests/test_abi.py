@@ -43,7 +43,8 @@ def test_workspace_sizes(mad):
     assert ws(mad.MAD_OP_DECODE, 16, 32, 8, 64) >= ws(mad.MAD_OP_DECODE, 1, 32, 8, 64)
     assert ws(mad.MAD_OP_UPDATE, 4, 2048, 8, 64) > (1 << 20)
     assert ws(mad.MAD_OP_VERIFY, 4, 32, 8, 128, 5) >= ws(mad.MAD_OP_VERIFY, 1, 32, 8, 128, 5) > (1 << 20)
-    assert ws(mad.MAD_OP_ACCEPT, 4, 1, 1, 64, 5, 128256) > (1 << 20)
+    assert ws(mad.MAD_OP_ACCEPT, 4, 1, 1, 64, 5, 128256) == (1 << 20)   # counters and row keys: the counter region
+    assert ws(mad.MAD_OP_ACCEPT, 1, 1, 1, 64, 257, 128256) == 0          # T above 256
     # invalid sizes give 0
     assert ws(mad.MAD_OP_DECODE, 0, 32, 8, 64) == 0
     assert ws(mad.MAD_OP_DECODE, 1, 30, 8, 64) == 0
@@ -135,6 +136,7 @@ def test_verify_and_accept_validation(mad):
         ctypes.c_void_p(1 << 22), ctypes.c_void_p(1 << 23), None, 0, None)
     assert acc(V=0) == mad.MAD_EINVAL
     assert acc(T=0) == mad.MAD_EINVAL
+    assert acc(T=257) == mad.MAD_EINVAL
     assert acc(draft=0) == mad.MAD_EINVAL
     assert acc(dtype=5) == mad.MAD_ENOTSUP
     assert acc() == mad.MAD_EWS
