@@ -87,6 +87,8 @@ UpdatePlan plan_update(int R, int D, int Hkv, int d);
 size_t update_part_stride(int R, int d, int KS);
 size_t update_ws_bytes(int R, int D, int Hkv, int d);
 hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st);
+constexpr int kUpdateGemvRows = 8;   // bf16 updates of at most this many rows stream W without a k-split
+bool update_uses_gemv(int R, int D, int dtype);
 
 // ---------------------------------------------------------------- verify ----
 #ifndef MAD_VERIFY_TARGET_WGS

@@ -17,6 +17,14 @@
 // with device-coherent stores; the last workgroup of a head block (arrival
 // counter) pulls them into LDS in one round trip, sums them, applies RoPE with
 // fp64 angles and writes bf16 rows.
+// BF16 with at most 8 rows (a single sequence's update, or a few): a weight
+// stream instead (update_gemv_kernel).  The projection is then a matrix-vector
+// product per row, bound by reading W once; a workgroup owns NC output
+// features -- rotate-half pairs (j, j + d/2) of one K or V head -- over the
+// whole input width, so no split partials and no merge: thread t holds the
+// 16-byte chunks t, t + 256, ... of every row and of the NC weight rows (all
+// loads issued together), products by v_dot2_f32_bf16, wave and workgroup
+// sums, then RoPE on the K pairs and the append.
 // F32: a vector-ALU kernel, one thread per (row, rotation pair).
 #include "mad_device.h"
 #include "mad_internal.h"
@@ -198,6 +206,75 @@ __global__ __launch_bounds__(256) void update_mfma_kernel(const UpdateArgs a) {
     }
 }
 
+template <int RR, int NC, int KD>
+__global__ __launch_bounds__(256) void update_gemv_kernel(const UpdateArgs a) {
+    constexpr int NP = NC / 2;   // rotation pairs per workgroup
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int R = a.R, D = a.D, d = a.d, hd = d / 2;
+    __shared__ float s_red[4][NC * RR];
+
+    // ---- rows and weights: chunk t + 256 j (8 inputs) of each ----
+    const bf16_t *x = reinterpret_cast<const bf16_t *>(a.x);
+    const bf16_t *w = reinterpret_cast<const bf16_t *>(a.w);
+    int wrow[NC];   // W row of feature c: pair q = blockIdx * NP + c % NP of head q / hd
+    #pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int q = blockIdx.x * NP + (c % NP);
+        wrow[c] = (q / hd) * d + (q % hd) + (c >= NP ? hd : 0);
+    }
+    uint4 wr[NC][KD], xr[RR][KD];
+    #pragma unroll
+    for (int j = 0; j < KD; ++j) {
+        const int e = (tid + 256 * j) * 8;
+        const bool in = e < D;
+        #pragma unroll
+        for (int c = 0; c < NC; ++c)
+            wr[c][j] = in ? *reinterpret_cast<const uint4 *>(w + (size_t)wrow[c] * D + e) : make_uint4(0u, 0u, 0u, 0u);
+        #pragma unroll
+        for (int r = 0; r < RR; ++r)
+            xr[r][j] = in && r < R ? *reinterpret_cast<const uint4 *>(x + (size_t)r * D + e) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    auto dot8 = [](const uint4 &u, const uint4 &v, float acc) {
+        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.x), __builtin_bit_cast(bf16x2_t, v.x), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.y), __builtin_bit_cast(bf16x2_t, v.y), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.z), __builtin_bit_cast(bf16x2_t, v.z), acc, false);
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u.w), __builtin_bit_cast(bf16x2_t, v.w), acc, false);
+    };
+    #pragma unroll
+    for (int c = 0; c < NC; ++c)
+        #pragma unroll
+        for (int r = 0; r < RR; ++r) {
+            float acc = 0.f;
+            #pragma unroll
+            for (int j = 0; j < KD; ++j) acc = dot8(wr[c][j], xr[r][j], acc);
+            acc = group_sum<64>(acc);
+            if (lane == 0) s_red[wave][c * RR + r] = acc;
+        }
+    __syncthreads();
+
+    // ---- thread (pair p, row r): sum the waves, rotate a K pair, append ----
+    if (tid < NP * RR) {
+        const int p = tid / RR, r = tid % RR;
+        if (r >= R) return;
+        const int b = r / a.n_new, i = r - b * a.n_new;
+        if (!a.fire[b]) return;
+        float y0 = 0.f, y1 = 0.f;
+        #pragma unroll
+        for (int wv = 0; wv < 4; ++wv) {
+            y0 += s_red[wv][p * RR + r];
+            y1 += s_red[wv][(p + NP) * RR + r];
+        }
+        const int q = blockIdx.x * NP + p, head = q / hd, jj = q % hd;
+        const bool is_k = head < a.Hkv;
+        if (is_k) rope_rotate(y0, y1, a.pos[r], rope_theta(jj, d, a.log2_base), &y0, &y1);
+        bf16_t *dst = reinterpret_cast<bf16_t *>(is_k ? a.mk : a.mv) + (size_t)(is_k ? head : head - a.Hkv) * a.m_head +
+                      (size_t)b * a.m_seq + (size_t)(a.mlen[b] + i) * d;
+        dst[jj].bits = f32_to_bf16(y0);
+        dst[jj + hd].bits = f32_to_bf16(y1);
+    }
+}
+
 // fp32: one thread per (row r, head h of K or V, feature pair j).
 __global__ __launch_bounds__(256) void update_f32_kernel(const UpdateArgs a) {
     const int d = a.d, half = d / 2;
@@ -278,7 +355,28 @@ size_t update_ws_bytes(int R, int D, int Hkv, int d) {
 
 size_t update_part_stride(int R, int d, int KS) { return ((size_t)KS * R * d + 63) / 64 * 64; }
 
+template <int RR, int KD>
+static hipError_t launch_gemv(const UpdateArgs &a, hipStream_t st) {
+    constexpr int NC = 4;
+    hipLaunchKernelGGL((update_gemv_kernel<RR, NC, KD>), dim3((unsigned)(2 * a.Hkv * a.d / NC)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+template <int RR>
+static hipError_t launch_gemv_kd(const UpdateArgs &a, hipStream_t st) {
+    const int kd = (a.D + 2047) / 2048;
+    if (kd == 1) return launch_gemv<RR, 1>(a, st);
+    if (kd == 2) return launch_gemv<RR, 2>(a, st);
+    return launch_gemv<RR, 4>(a, st);
+}
+
+bool update_uses_gemv(int R, int D, int dtype) { return dtype == MAD_BF16 && R <= kUpdateGemvRows && D <= 8192; }
+
 hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st) {
+    if (update_uses_gemv(a.R, a.D, dtype)) {
+        if (a.R == 1) return launch_gemv_kd<1>(a, st);
+        if (a.R <= 4) return launch_gemv_kd<4>(a, st);
+        return launch_gemv_kd<8>(a, st);
+    }
     if (dtype == MAD_BF16) {
         dim3 grid((unsigned)(2 * a.Hkv * a.KS)), block(256);
         const size_t lds = update_lds_bytes(a.R, a.d, a.KS, a.stages);

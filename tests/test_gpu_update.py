@@ -83,6 +83,14 @@ def test_head_dim_128_and_large_weights():
     _case(torch.bfloat16, 2, 3, 1024, 4, 128, 10, 40, [[5, 6, 7], [100000, 100001, 131072]], seed=7, wstd=0.05)
 
 
+@pytest.mark.parametrize("D", [2048, 3072, 6144])
+def test_few_rows_weight_stream_fire_and_widths(D):
+    # at most 8 rows take the weight-streaming kernel: two sequences x 4 slots,
+    # the first not firing; input widths that leave part of a thread's chunks empty
+    _case(torch.bfloat16, 2, 4, D, 8, 64, [700, 31], 800, [[16 * (60 + i) for i in range(4)], [9000, 9016, 9032, 9048]],
+          fire=[0, 1], seed=9 + D)
+
+
 def test_fp32_head_dim_128():
     _case(torch.float32, 2, 2, 128, 2, 128, 3, 8, [[0, 1], [2, 3]], seed=8)
 
