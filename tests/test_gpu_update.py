@@ -91,6 +91,16 @@ def test_few_rows_weight_stream_fire_and_widths(D):
           fire=[0, 1], seed=9 + D)
 
 
+@pytest.mark.parametrize("B,n_new,d", [(3, 4, 64), (5, 7, 64), (4, 8, 128)])
+def test_more_than_eight_rows_matrix_core_kernel(B, n_new, d):
+    # more than 8 rows take the matrix-core kernel: 12, 35 and 32 rows fill 1, 3 and 2 sixteen-row tiles
+    rng = np.random.default_rng(B * n_new)
+    pos = [[int(p) + 16 * i for i in range(n_new)] for p in rng.integers(1024, 30000, B)]
+    fire = [1] * B
+    fire[1] = 0
+    _case(torch.bfloat16, B, n_new, 2048, 8, d, rng.integers(0, 40, B).tolist(), 64, pos, fire=fire, seed=20 + B)
+
+
 def test_fp32_head_dim_128():
     _case(torch.float32, 2, 2, 128, 2, 128, 3, 8, [[0, 1], [2, 3]], seed=8)
 
