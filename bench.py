@@ -68,9 +68,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--summarize-trace", metavar="CSV",
                     help="print per-(kernel, grid) durations of a rocprofv3 kernel_trace.csv and exit")
-    ap.add_argument("--pmc-workload", choices=("decode", "copy"),
+    ap.add_argument("--pmc-workload", choices=("decode", "copy", "update", "verify", "prefill"),
                     help="run only a counter workload (under rocprofv3 --pmc): 'decode' = the headline's "
-                         "compact-memory decode launches, 'copy' = a streaming copy of known size")
+                         "compact-memory decode launches, 'copy' = a streaming copy of known size, "
+                         "'update' / 'verify' / 'prefill' = the matrix-core kernels at the benchmark's shapes")
     ap.add_argument("--summarize-counters", metavar="CSV",
                     help="print per-(kernel, grid) mean counter values of a rocprofv3 counter_collection.csv")
     return ap.parse_args()
@@ -92,6 +93,9 @@ def pmc_workload(kind):
         torch.cuda.synchronize()
         print(f"copy: 4 launches of {COPY_FLOATS * 4} B read + {COPY_FLOATS * 4} B written", flush=True)
         return
+    if kind in ("update", "verify", "prefill"):
+        mfma_workload(torch, mad, kind)
+        return
     model = DraftModel(torch, mad, 6)
     n = 0
     for k in range(4):
@@ -105,6 +109,51 @@ def pmc_workload(kind):
                 n += 1
     torch.cuda.synchronize()
     print(f"decode: {n} compact-memory launches, {kv_bytes(3073, model.Hkv, model.d)} B of K/V each", flush=True)
+
+
+def mfma_workload(torch, mad, kind):
+    """Launches of the matrix-core kernels at the benchmark's shapes, for the
+    MFMA counters: the memory update of 64 rows (16 sequences x 4 slots) and of
+    4 rows; verify at the 8B-layer (B4, 32/8) and 70B-layer (B1, 64/8) shapes;
+    the memory prefill over a 32K prefix at d 64 and d 128."""
+    bf = torch.bfloat16
+    rn = lambda *s_: torch.randn(*s_, device="cuda").to(bf)
+    if kind == "update":
+        Hkv, d, D = 8, 64, 2048
+        for B, n_new in ((16, 4), (1, 4)):
+            x, w = rn(B, n_new, D), (torch.randn(2 * Hkv * d, D, device="cuda") * 0.02).to(bf)
+            mk, mv = rn(B, Hkv, 1088, d), rn(B, Hkv, 1088, d)
+            ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_UPDATE, B * n_new, D, Hkv, d), dtype=torch.uint8,
+                             device="cuda")
+            pos = [[16 * (2048 + 4 * b + i) for i in range(n_new)] for b in range(B)]
+            for _ in range(8):
+                mad.memory_update(x, w, pos, mad.KV(mk, mv, [1024] * B), ws=ws)
+            torch.cuda.synchronize()
+            print(f"update: 8 launches of {B * n_new} rows, {2 * B * n_new * D * 2 * Hkv * d} flop each", flush=True)
+    elif kind == "verify":
+        Hkv, d, T = 8, 128, 5
+        L = 32768 + T
+        for B, Hq in ((4, 32), (1, 64)):
+            k, vt = rn(B, Hkv, 32776, d), rn(B, Hkv, d, 32776)
+            q = rn(B, T, Hq, d)
+            out, lse = torch.empty_like(q), torch.empty(B, T, Hq, device="cuda")
+            ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_VERIFY, B, Hq, Hkv, d, T), dtype=torch.uint8,
+                             device="cuda")
+            for _ in range(4):
+                mad.verify_attn(q, k, vt, [L] * B, out, lse, ws=ws)
+            torch.cuda.synchronize()
+            print(f"verify: 4 launches, B{B} {Hq}/{Hkv}, {4 * B * Hq * T * L * d} flop each", flush=True)
+    else:
+        P, S_, W_, r_, u_ = 32768, 0, 1024, 16, 4
+        M = mad.slots_after(P, S_, r_, u_)
+        for Hq, Hkv, d in ((32, 8, 64), (32, 8, 128)):
+            qr, qs_ = rn(1, P, Hq, d), rn(1, M, Hq, d)
+            rk, rv = rn(1, Hkv, P, d), rn(1, Hkv, P, d)
+            mk, mv = rn(1, Hkv, S_ + M, d), rn(1, Hkv, S_ + M, d)
+            for _ in range(2):
+                mad.memory_prefill_attn(qr, qs_, mad.KV(mk, mv, [S_ + M]), mad.KV(rk, rv, [P]), [P], S_, W_, r_, u_)
+            torch.cuda.synchronize()
+            print(f"prefill: 2 launches, d{d}, {prefill_flops(P, S_, W_, r_, u_, Hq, d)} flop each", flush=True)
 
 
 def summarize_counters(path):
@@ -553,6 +602,9 @@ def main():
     lay_res = draft_layer_bench(torch, mad, K)
     torch.cuda.empty_cache()
 
+    # --------------------------------------------------------- prefix sweep ----
+    sweep = prefix_sweep(torch, mad)
+
     # ------------------------------------------------------ memory prefill ----
     pre_res = {}
     P, S_, W_, r_, u_ = 32768, 0, 1024, 16, 4
@@ -601,6 +653,7 @@ def main():
         "cache_resident": cache_resident,
         "speedup_vs_full_kv": round(full_us_layer / us_per_layer, 3),
         "batched_decode": batched,
+        "prefix_sweep": sweep,
         "memory_update": upd_res,
         "verify": ver_res,
         "accept": acc_res,
@@ -678,6 +731,72 @@ def draft_layer_bench(torch, mad, K):
     out["speedup_vs_full_kv"] = round(out["full_kv"]["us_per_layer"] / out["compact"]["us_per_layer"], 3)
     log(f"draft layer linear maps: {t * 1e6 / L:.2f} us/layer, {wbytes * L / t / 1e12:.2f} TB/s")
     return out
+
+
+def decode_launch_cold(torch, mad, mem_len, win_len, Hq=32, Hkv=8, d=64, cold_bytes=640 << 20):
+    """Mean duration of one batch-1 draft decode launch over mem_len memory rows,
+    win_len ring rows and the new token, the launches rotating through enough
+    independent buffers (>= 640 MB, over twice the L2 and Infinity Cache) that
+    every launch reads its K/V from HBM.  Returns (seconds, algorithmic bytes)."""
+    keys = mem_len + win_len + 1
+    nbytes = kv_bytes(keys, Hkv, d)
+    n = max(2, min(256, -(-cold_bytes // nbytes)))
+    mcap, rcap = max(mem_len, 1), (win_len + 1 + 63) // 64 * 64
+    bf = torch.bfloat16
+    mem = torch.randn(n, 2, Hkv, mcap, d, device="cuda").to(bf) if mem_len else None
+    ring = torch.randn(n, 2, Hkv, rcap, d, device="cuda").to(bf)
+    q = torch.randn(1, Hq, d, device="cuda").to(bf)
+    kn, vn = torch.randn(1, Hkv, d, device="cuda").to(bf), torch.randn(1, Hkv, d, device="cuda").to(bf)
+    out, lse = torch.empty_like(q), torch.empty(1, Hq, device="cuda")
+    ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_DECODE, 1, Hq, Hkv, d), dtype=torch.uint8, device="cuda")
+
+    def launch(j):
+        m = mad.KV(mem[j, 0:1], mem[j, 1:2], [mem_len]) if mem_len else None
+        mad.draft_decode_attn(q, m, mad.KV(ring[j, 0:1], ring[j, 1:2], [win_len], [0]), kn, vn, out, lse, ws=ws)
+
+    t = mean_launch_seconds(torch, [lambda j=j: launch(j) for j in range(n)])
+    del mem, ring
+    return t, nbytes
+
+
+def prefix_sweep(torch, mad):
+    """Draft decode latency against the prefix length L (8K..32K), compact memory
+    beside the full KV, with the least-squares fit t = alpha + beta * L of the
+    per-layer cost model (Eq. 2); and the paper's own memory shapes at 32K
+    (S = 128 sinks, W = 128, slot interval r = 4 and 8)."""
+    import numpy as np
+    from paper_2608_30252_amd.state import MemoryLayout
+    pts = []
+    for P in (8192, 16384, 24576, 32768):
+        lay = MemoryLayout(0, 1024, 16, ring_cap=1024 + 128, mem_cap=P // 16 + 64, slots_per_update=4)
+        v = lay.decode_view(P)
+        tc, bc = decode_launch_cold(torch, mad, v.mem_len, v.win_len)
+        tf, bf_ = decode_launch_cold(torch, mad, 0, P)
+        pts.append({"prefix": P, "compact_keys": v.mem_len + v.win_len + 1, "compact_us": round(tc * 1e6, 3),
+                    "compact_tbps": round(bc / tc / 1e12, 3), "full_keys": P + 1, "full_us": round(tf * 1e6, 3),
+                    "full_tbps": round(bf_ / tf / 1e12, 3), "speedup": round(tf / tc, 2)})
+        log(f"prefix {P}: compact {tc * 1e6:.2f} us ({bc / tc / 1e12:.2f} TB/s), full {tf * 1e6:.2f} us "
+            f"({bf_ / tf / 1e12:.2f} TB/s)")
+    Ls = np.array([p["prefix"] for p in pts], dtype=np.float64)
+
+    def fit(key):
+        beta, alpha = np.polyfit(Ls, np.array([p[key] for p in pts]), 1)
+        return {"alpha_us": round(float(alpha), 3), "beta_ns_per_token": round(float(beta) * 1e3, 4)}
+    full_fit, compact_fit = fit("full_us"), fit("compact_us")
+    # one token of the full KV costs 8 KV heads x 64 x 2 (K, V) x 2 B = 2048 B
+    full_fit["beta_tbps"] = round(2048 / (full_fit["beta_ns_per_token"] * 1e-9) / 1e12, 3)
+    paper = []
+    for r in (4, 8):
+        lay = MemoryLayout(128, 128, r, ring_cap=256, mem_cap=128 + 32768 // r, slots_per_update=4)
+        v = lay.decode_view(32768)
+        t, b = decode_launch_cold(torch, mad, v.mem_len, v.win_len)
+        paper.append({"sinks": 128, "window": 128, "slot_interval": r, "keys": v.mem_len + v.win_len + 1,
+                      "us": round(t * 1e6, 3), "tbps": round(b / t / 1e12, 3)})
+        log(f"paper-shaped S = W = 128, r = {r}: {v.mem_len + v.win_len + 1} keys, {t * 1e6:.2f} us")
+    torch.cuda.empty_cache()
+    return {"workload": "batch-1 draft decode launch, 32/8 heads, d64, bf16, cold (buffers rotated over >= 640 MB); "
+                        "compact = L/16 slots + 1024-token window, full = L + 1 keys",
+            "points": pts, "full_fit": full_fit, "compact_fit": compact_fit, "paper_shaped_32k": paper}
 
 
 def prefill_flops(P, S, W, r, u, Hq, d):

@@ -106,6 +106,13 @@ def test_draft_32k_full_kv_layer_bf16():
     _case(torch.bfloat16, 1, 32, 8, 64, 0, 32768, 32768 + 64, 0, seed=5, mem=False)
 
 
+@pytest.mark.parametrize("r,mlen", [(4, 8288), (8, 4208)])
+def test_paper_shaped_memory_32k_bf16(r, mlen):
+    # 32K prefix, 128 sinks + (32768 - 128) / r slots (materialised 4 at a time), a 128-token window:
+    # 8416 keys at r = 4, 4336 at r = 8 (the ring wraps: 127 rows from row 200 of a 256-row ring)
+    _case(torch.bfloat16, 1, 32, 8, 64, mlen, 127, 256, 200, seed=13 + r)
+
+
 def test_peaky_queries_bf16():
     _case(torch.bfloat16, 1, 32, 8, 64, 2048, 1023, 1056, 50, seed=6, peaky=0.6)
 
