@@ -123,11 +123,9 @@ def mfma_workload(torch, mad, kind):
         for B, n_new in ((16, 4), (1, 4)):
             x, w = rn(B, n_new, D), (torch.randn(2 * Hkv * d, D, device="cuda") * 0.02).to(bf)
             mk, mv = rn(B, Hkv, 1088, d), rn(B, Hkv, 1088, d)
-            ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_UPDATE, B * n_new, D, Hkv, d), dtype=torch.uint8,
-                             device="cuda")
             pos = [[16 * (2048 + 4 * b + i) for i in range(n_new)] for b in range(B)]
             for _ in range(8):
-                mad.memory_update(x, w, pos, mad.KV(mk, mv, [1024] * B), ws=ws)
+                mad.memory_update(x, w, pos, mad.KV(mk, mv, [1024] * B))
             torch.cuda.synchronize()
             print(f"update: 8 launches of {B * n_new} rows, {2 * B * n_new * D * 2 * Hkv * d} flop each", flush=True)
     elif kind == "verify":
@@ -254,8 +252,7 @@ class DraftModel:
             self.vnf = [self.vn[l].expand(1 + u, Hkv, d).contiguous() for l in range(L)]
             self.outf = [torch.empty(1 + u, Hq, d, device=dev, dtype=bf) for _ in range(L)]
             self.lsef = [torch.empty(1 + u, Hq, device=dev, dtype=torch.float32) for _ in range(L)]
-        self.ws = torch.zeros(max(mad.workspace_bytes(mad.MAD_OP_DECODE, 1 + u if not full_kv else 1, Hq, Hkv, d),
-                                  mad.workspace_bytes(mad.MAD_OP_UPDATE, u if not full_kv else 1, self.D, Hkv, d)),
+        self.ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_DECODE, 1 + u if not full_kv else 1, Hq, Hkv, d),
                               dtype=torch.uint8, device=dev)
         self.decode_calls = []   # keys the raw query attends, per layer-step (slot-scope rows not counted)
         self.n_updates = 0
@@ -278,7 +275,7 @@ class DraftModel:
                 self.decode_calls.append(view.mem_len + view.win_len + 1)
                 continue
             mk, mv = self.mem_k[set_idx][l], self.mem_v[set_idx][l]
-            mad.memory_update(self.x[l], self.w_g[l], [upd.positions], mad.KV(mk, mv, [upd.mem_row]), ws=self.ws)
+            mad.memory_update(self.x[l], self.w_g[l], [upd.positions], mad.KV(mk, mv, [upd.mem_row]))
             views, modes = fused
             mad.draft_step_attn(self.qf[l], mad.KV(mk, mv, [v.mem_len for v in views]),
                                 mad.KV(rk, rv, [v.win_len for v in views], [v.win_start for v in views]),
@@ -521,10 +518,8 @@ def main():
         ws_ = [(torch.randn(2 * Hkv * d, D, device="cuda") * 0.02).to(torch.bfloat16) for _ in range(sets)]
         mks = [torch.randn(B, Hkv, 1088, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
         mvs = [torch.randn(B, Hkv, 1088, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
-        wsb = torch.zeros(mad.workspace_bytes(mad.MAD_OP_UPDATE, B * n_new, D, Hkv, d), dtype=torch.uint8,
-                          device="cuda")
         posl = [[16 * (2048 + 4 * b + i) for i in range(n_new)] for b in range(B)]
-        fns = [lambda j=j: mad.memory_update(xs[j], ws_[j], posl, mad.KV(mks[j], mvs[j], [1024] * B), ws=wsb)
+        fns = [lambda j=j: mad.memory_update(xs[j], ws_[j], posl, mad.KV(mks[j], mvs[j], [1024] * B))
                for j in range(sets)]
         g = graph_of(torch, lambda: [f() for f in fns])
         g.replay()
@@ -535,7 +530,7 @@ def main():
                          "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "tflops": round(flops / t / 1e12, 3),
                          "mfma_frac_of_bf16_peak": round(flops / t / PEAK_BF16, 6), "bytes": nbytes}
         log(f"memory update {name}: {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
-        del xs, ws_, mks, mvs, wsb, fns, g
+        del xs, ws_, mks, mvs, fns, g
     torch.cuda.empty_cache()
 
     # -------------------------------------------------------------- verify ----

@@ -59,7 +59,7 @@ extern "C" {
 #define MAD_MAX_LAYER_ROWS 8   /* rows (raw token + slot tokens) per draft-layer linear map */
 
 #define MAD_OP_DECODE 0
-#define MAD_OP_UPDATE 1
+#define MAD_OP_UPDATE 1 /* takes no workspace: 0 bytes */
 #define MAD_OP_VERIFY 2
 #define MAD_OP_ACCEPT 3
 #define MAD_OP_ACCEPT_STOCH 4
@@ -157,11 +157,15 @@ int mad_draft_step_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype,
  *          untouched (the per-sequence mask of heterogeneous batches, Sec. 4.1)
  *   mem    linear view to append to; requires mem.len[b] + n_new <= mem.cap
  * B * n_new <= MAD_MAX_UPDATE_ROWS; D a multiple of 64; d in {64, 128}.
- * BF16 runs the projection on the matrix cores; F32 on the vector ALUs.
+ * BF16 runs the projection as a weight stream (at most 8 rows) or on the
+ * matrix cores; F32 on the vector ALUs.  No workspace: every output element is
+ * produced by one workgroup.
+ * Errors: MAD_EINVAL (null pointers, B, n_new, D, Hkv, rope_base <= 1 or not
+ * finite, a firing sequence's len + n_new above cap), MAD_ENOTSUP (d, dtype).
  */
 int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const uint8_t *fire,
                       int B, int n_new, int D, int Hkv, int d, int dtype, double rope_base,
-                      const mad_kv_view *mem, void *ws, size_t ws_bytes, void *stream);
+                      const mad_kv_view *mem, void *stream);
 
 /*
  * Target verify attention (Sec. 2.1: the target scores the drafted block in
@@ -306,11 +310,11 @@ int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *
 /*
  * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:
  *   DECODE: B, Hq, Hkv, d                       (T, max_keys ignored)
- *   UPDATE: B = rows (B * n_new), Hq = D, Hkv, d (T, max_keys ignored)
  *   VERIFY: B, Hq, Hkv, d, T                    (max_keys ignored)
  *   ACCEPT: B, T, max_keys = V                  (Hq, Hkv, d ignored)
  *   ACCEPT_STOCH: B, max_keys = V               (Hq, Hkv, d, T ignored)
- * Returns 0 for an unknown op or invalid sizes.
+ * Returns 0 for an unknown op or invalid sizes.  The memory update and the
+ * draft-layer maps take no workspace (MAD_OP_UPDATE is 0 bytes).
  */
 size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max_keys);
 

@@ -52,7 +52,7 @@ def _load_library():
     vp, i, f, d, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double, ctypes.c_size_t
     kvp = ctypes.POINTER(_KVView)
     lib.mad_draft_decode_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, vp, vp, vp, sz, vp]
-    lib.mad_memory_update.argtypes = [vp, vp, _i32p, _u8p, i, i, i, i, i, i, d, kvp, vp, sz, vp]
+    lib.mad_memory_update.argtypes = [vp, vp, _i32p, _u8p, i, i, i, i, i, i, d, kvp, vp]
     lib.mad_verify_attn.argtypes = [vp, i, i, i, i, i, i, f, vp, vp, ctypes.c_int64, ctypes.c_int64,
                                     ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
@@ -230,8 +230,7 @@ def draft_step_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV], k_new
     return out, lse
 
 
-def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None,
-                  rope_base: float = 500000.0, ws: Optional[torch.Tensor] = None):
+def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None, rope_base: float = 500000.0):
     """x [B, n_new, D] slot hidden states, w_kv [2*Hkv*d, D]; pos host [B][n_new].
 
     Appends the slots' K (rotated at pos) and V at mem rows len[b]..len[b]+n_new-1
@@ -244,11 +243,8 @@ def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None,
     fire_arr = None
     if fire is not None:
         fire_arr = (ctypes.c_uint8 * B)(*[1 if f else 0 for f in fire])
-    nbytes = workspace_bytes(MAD_OP_UPDATE, B * n_new, D, Hkv, d)
-    w = _ws_for(x.device, nbytes, ws)
     rc = _load_library().mad_memory_update(_ptr(x), _ptr(w_kv), pos_arr, fire_arr, B, n_new, D, Hkv, d,
-                               _dtype_code(x), float(rope_base), ctypes.byref(mv),
-                               _ptr(w), w.numel(), _stream(x.device))
+                               _dtype_code(x), float(rope_base), ctypes.byref(mv), _stream(x.device))
     _check(rc)
 
 

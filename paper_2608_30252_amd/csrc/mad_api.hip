@@ -88,9 +88,6 @@ size_t mad_workspace_bytes(int op, int B, int Hq, int Hkv, int d, int T, int max
         case MAD_OP_DECODE:
             if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128)) return 0;
             return mad::decode_ws_bytes(B, Hq, Hkv, d);
-        case MAD_OP_UPDATE:   // B = rows (B * n_new), Hq = D
-            if (B < 1 || B > MAD_MAX_UPDATE_ROWS || Hq < 64 || Hq % 64 || Hkv < 1 || (d != 64 && d != 128)) return 0;
-            return mad::update_ws_bytes(B, Hq, Hkv, d);
         case MAD_OP_VERIFY:
             if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128) || T < 1) return 0;
             return mad::verify_ws_bytes(B, Hq, Hkv, d, T);
@@ -210,8 +207,7 @@ int mad_draft_step_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype,
 }
 
 int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const uint8_t *fire, int B, int n_new,
-                      int D, int Hkv, int d, int dtype, double rope_base, const mad_kv_view *mem, void *ws,
-                      size_t ws_bytes, void *stream) {
+                      int D, int Hkv, int d, int dtype, double rope_base, const mad_kv_view *mem, void *stream) {
     if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
     if (n_new < 1 || B * n_new > MAD_MAX_UPDATE_ROWS)
         return fail(MAD_EINVAL, "B*n_new=%d outside [1, %d]", B * n_new, MAD_MAX_UPDATE_ROWS);
@@ -250,19 +246,6 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
         a.fire[b] = (unsigned char)(fire ? (fire[b] != 0) : 1);
     }
     for (int r = 0; r < R; ++r) a.pos[r] = pos[r];
-    if (dtype == MAD_BF16) {
-        mad::UpdatePlan p = mad::plan_update(R, D, Hkv, d);
-        const size_t need = mad::update_ws_bytes(R, D, Hkv, d);
-        if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
-        if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
-        if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
-        a.KS = p.KS;
-        a.kc = p.kc;
-        a.stages = p.stages;
-        a.counters = (unsigned *)ws;
-        a.part = (float *)((char *)ws + mad::kCounterRegionBytes);
-        a.part_stride = (int64_t)mad::update_part_stride(R, d, p.KS);
-    }
     return hip_status(mad::launch_update(a, dtype, (hipStream_t)stream), "memory update launch");
 }
 

@@ -59,35 +59,19 @@ size_t decode_ws_bytes(int B, int Hq, int Hkv, int d);
 hipError_t launch_decode(const DecodeArgs &a, int dtype, int d, int G, hipStream_t st);
 
 // ---------------------------------------------------------------- update ----
-constexpr size_t kUpdateMaxLds = 160 * 1024 - 512;   // LDS a workgroup may use (staging ring or split merge)
-#ifndef MAD_UPDATE_TARGET_WGS
-#define MAD_UPDATE_TARGET_WGS 256
-#endif
-constexpr int kUpdateTargetWGs = MAD_UPDATE_TARGET_WGS;   // the k-split aims at this many workgroups
-
 struct UpdateArgs {
     const void *x, *w;    // [R][D] slot rows, [2*Hkv*d][D] mirrored projections
     void *mk, *mv;        // memory segment to append to
     int64_t m_seq, m_head;
-    float *part;          // split partials: one block of part_stride floats per head block
-    int64_t part_stride;
-    unsigned *counters;   // counter region: head block hb on line hb
     double log2_base;     // log2 of the RoPE base
-    int R, n_new, D, Hkv, d, KS, kc, stages;
+    int R, n_new, D, Hkv, d;
     int mlen[kMaxB];
     int pos[MAD_MAX_UPDATE_ROWS];
     unsigned char fire[kMaxB];
 };
 
-struct UpdatePlan {
-    int KS, kc, stages;   // k-splits, the input-width chunk of each, LDS ring stages
-};
-
-UpdatePlan plan_update(int R, int D, int Hkv, int d);
-size_t update_part_stride(int R, int d, int KS);
-size_t update_ws_bytes(int R, int D, int Hkv, int d);
 hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st);
-constexpr int kUpdateGemvRows = 8;   // bf16 updates of at most this many rows stream W without a k-split
+constexpr int kUpdateGemvRows = 8;   // bf16 updates of at most this many rows take the weight stream
 bool update_uses_gemv(int R, int D, int dtype);
 
 // ---------------------------------------------------------------- verify ----

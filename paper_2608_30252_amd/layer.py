@@ -88,7 +88,7 @@ class DraftLayer:
                               self.lse[:R], ws=ws)
         else:
             memory_update(xn[1:].unsqueeze(0), w.w_kv_g, [upd.positions], KV(mem_k, mem_v, [upd.mem_row]),
-                          rope_base=self.rope_base, ws=ws)
+                          rope_base=self.rope_base)
             views, modes = lay.step_views(p)
             draft_step_attn(q, KV(mem_k, mem_v, [vw.mem_len for vw in views]),
                             KV(ring_k, ring_v, [vw.win_len for vw in views], [vw.win_start for vw in views]),

@@ -41,14 +41,13 @@ def test_workspace_sizes(mad):
     ws = mad.workspace_bytes
     assert ws(mad.MAD_OP_DECODE, 1, 32, 8, 64) > (1 << 20)          # counter region + partials
     assert ws(mad.MAD_OP_DECODE, 16, 32, 8, 64) >= ws(mad.MAD_OP_DECODE, 1, 32, 8, 64)
-    assert ws(mad.MAD_OP_UPDATE, 4, 2048, 8, 64) > (1 << 20)
+    assert ws(mad.MAD_OP_UPDATE, 4, 2048, 8, 64) == 0                 # the update takes no workspace
     assert ws(mad.MAD_OP_VERIFY, 4, 32, 8, 128, 5) >= ws(mad.MAD_OP_VERIFY, 1, 32, 8, 128, 5) > (1 << 20)
     assert ws(mad.MAD_OP_ACCEPT, 4, 1, 1, 64, 5, 128256) == (1 << 20)   # counters and row keys: the counter region
     assert ws(mad.MAD_OP_ACCEPT, 1, 1, 1, 64, 257, 128256) == 0          # T above 256
     # invalid sizes give 0
     assert ws(mad.MAD_OP_DECODE, 0, 32, 8, 64) == 0
     assert ws(mad.MAD_OP_DECODE, 1, 30, 8, 64) == 0
-    assert ws(mad.MAD_OP_UPDATE, 65, 2048, 8, 64) == 0
     assert ws(99, 1, 1, 1, 64) == 0
 
 
@@ -104,9 +103,8 @@ def test_update_validation(mad):
     mem = mad._KVView(1 << 24, 1 << 25, 0, 16 * 64, 16, None, ln)
     def call(B=1, n_new=4, D=2048, Hkv=8, d=64, dtype=mad.MAD_BF16, base=500000.0, x=1 << 20, memp=True):
         return lib.mad_memory_update(ctypes.c_void_p(x), ctypes.c_void_p(1 << 21), pos, None, B, n_new, D, Hkv, d,
-                                     dtype, base, ctypes.byref(mem) if memp else None, None, 0, None)
+                                     dtype, base, ctypes.byref(mem) if memp else None, None)
     assert call(n_new=8) == mad.MAD_EINVAL and "exceeds cap" in _last_error(mad)   # 10 + 8 > 16
-    assert call(n_new=4) == mad.MAD_EWS                                             # valid, but no workspace
     assert call(n_new=0) == mad.MAD_EINVAL
     assert call(B=65) == mad.MAD_EINVAL
     assert call(D=100) == mad.MAD_EINVAL

@@ -120,3 +120,12 @@ def test_duplicate_position_gives_identical_keys():
     torch.cuda.synchronize()
     assert torch.equal(mk[0, :, 0].view(torch.int16), mk[0, :, 1].view(torch.int16))
     assert torch.equal(mv[0, :, 0].view(torch.int16), mv[0, :, 1].view(torch.int16))
+
+
+@pytest.mark.parametrize("D,Hkv,d", [(192, 2, 64), (4096, 8, 64), (6144, 4, 128)])
+def test_matrix_core_kernel_input_widths(D, Hkv, d):
+    # the matrix-core kernel's k loop: an odd number of 32-wide steps (D 192: waves 0-1 take two, 2-3 one),
+    # two and three batches of steps per wave; 18 rows leave a 2-row second tile
+    rng = np.random.default_rng(D)
+    pos = [[int(p) + 16 * i for i in range(6)] for p in rng.integers(100, 60000, 3)]
+    _case(torch.bfloat16, 3, 6, D, Hkv, d, [5, 0, 17], 32, pos, fire=[1, 1, 0], seed=30 + D // 64)
