@@ -31,7 +31,10 @@
 //     a 16-lane group names features 4a .. 4a+3 of key row e, and lane 4a + b
 //     receives feature 4a + b of the four rows);
 //   * online softmax per query row (16 scores per lane per tile, two
-//     cross-lane steps); one barrier per tile.
+//     cross-lane lane swaps), masks applied in place on edge tiles only, and
+//     a lazy rescale: the reference maximum of a row block moves only when a
+//     row gains more than 2^8, so most tiles skip the exponential of the
+//     correction and the rescale of o; one barrier per tile.
 // Query blocks of every unit are dealt round-robin over the units (with a
 // multiple of 8 units all blocks of one KV head share an XCD and its L2), the
 // heaviest blocks first.
@@ -72,17 +75,23 @@ __device__ __forceinline__ v4s_t lds_read_tr16(const unsigned char *p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s_t *)(p));
 }
 
+// Lanes l, l^16, l^32, l^48 hold the same query row.  v_permlane16_swap and
+// v_permlane32_swap (VALU lane swaps, no LDS round trip) give every lane the
+// values of lanes l & ~16 and l | 16 (resp. 32), so two swaps reduce over the four.
 __device__ __forceinline__ float prefill_row_max(float v) {
-    // lanes l, l^16, l^32, l^48 hold the same query row
-    v = fmaxf(v, xor_lane<16>(v));
-    v = fmaxf(v, xor_lane<32>(v));
-    return v;
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float prefill_row_sum(float v) {
-    v += xor_lane<16>(v);
-    v += xor_lane<32>(v);
-    return v;
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
+
+constexpr float kLazyLog2 = 8.f;   // rescale threshold of the online softmax, log2 units
 
 __device__ __forceinline__ int prefill_slots_after(int t, int S, int ru, int u) {
     return t <= S ? 0 : (t - S) / ru * u;
@@ -256,49 +265,51 @@ __global__ __launch_bounds__(256, NB == 2 ? (D == 64 ? 3 : 2) : 1) void prefill_
         for (int i = 0; i < NB; ++i) {
             const int lo = is_mem ? 0 : r_lo[i];
             const int hi = min(end, is_mem ? m_lim[i] : r_hi[i]);
-            const bool full = __all(base >= lo && base + C::KT <= hi);
-            float sv16[C::KH][8];
-            float mt = -INFINITY;
-            if (full) {   // wave-uniform: no masks
+            if (!__all(base >= lo && base + C::KT <= hi)) {
+                // edge tile: element e of half h is key base + 32h + 8lg + e; mask in place
+                const int k0 = base + 8 * lg, a0 = lo - k0, b0 = hi - k0;
                 #pragma unroll
                 for (int h = 0; h < C::KH; ++h)
                     #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        sv16[h][e] = sacc[h][e >> 2][i][e & 3];
-                        mt = fmaxf(mt, sv16[h][e]);
-                    }
-            } else {
-                #pragma unroll
-                for (int h = 0; h < C::KH; ++h)
-                    #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int key = base + 32 * h + 8 * lg + e;
-                        const bool ok = (key >= lo) & (key < hi);   // no short circuit: straight-line selects
-                        sv16[h][e] = ok ? sacc[h][e >> 2][i][e & 3] : -INFINITY;
-                        mt = fmaxf(mt, sv16[h][e]);
+                        const int kk = 32 * h + e;
+                        const bool ok = (kk >= a0) & (kk < b0);   // no short circuit: straight-line selects
+                        sacc[h][e >> 2][i][e & 3] = ok ? sacc[h][e >> 2][i][e & 3] : -INFINITY;
                     }
             }
+            float mt = -INFINITY;
+            #pragma unroll
+            for (int h = 0; h < C::KH; ++h)
+                #pragma unroll
+                for (int e = 0; e < 8; ++e) mt = fmaxf(mt, sacc[h][e >> 2][i][e & 3]);
             mt = prefill_row_max(mt);
-            const float mn = fmaxf(m_run[i], mt);
-            const float ms = (mn == -INFINITY) ? 0.f : mn * cs;
-            const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run[i], cs, -ms));
-            m_run[i] = mn;
+            // lazy rescale: the reference maximum moves only when some row of the
+            // block gains more than kLazyLog2 (in log2 units); until then the
+            // probabilities stay below 2^kLazyLog2, and o and l share one reference
+            const bool grow = mt > m_run[i] && (m_run[i] == -INFINITY || (mt - m_run[i]) * cs > kLazyLog2);
+            if (__any(grow)) {
+                const float mn = fmaxf(m_run[i], mt);
+                const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run[i], cs, mn == -INFINITY ? 0.f : -mn * cs));
+                m_run[i] = mn;
+                l_run[i] *= alpha;
+                #pragma unroll
+                for (int db = 0; db < DB; ++db) o[db][i] *= alpha;
+            }
+            const float ms = m_run[i] == -INFINITY ? 0.f : m_run[i] * cs;
             float ps = 0.f;
             #pragma unroll
             for (int h = 0; h < C::KH; ++h) {
                 uint32_t pk[4];
                 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = __builtin_amdgcn_exp2f(fmaf(sv16[h][2 * e], cs, -ms));
-                    const float p1 = __builtin_amdgcn_exp2f(fmaf(sv16[h][2 * e + 1], cs, -ms));
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[h][(2 * e) >> 2][i][(2 * e) & 3], cs, -ms));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[h][(2 * e + 1) >> 2][i][(2 * e + 1) & 3], cs, -ms));
                     ps += p0 + p1;
                     pk[e] = cvt_pk_bf16(p0, p1);
                 }
                 pf[i][h] = __builtin_bit_cast(bf16x8_v, u32x4_v{pk[0], pk[1], pk[2], pk[3]});
             }
-            l_run[i] = fmaf(l_run[i], alpha, ps);
-            #pragma unroll
-            for (int db = 0; db < DB; ++db) o[db][i] *= alpha;
+            l_run[i] += ps;
         }
         // O^T += V^T P^T: A = V^T rows (features db*16 + lr), keys 32h + 8 lg .. +7,
         // from the transposing reads of key rows 32h + 8 lg + {0..3} and {4..7}

@@ -16,7 +16,7 @@ from parity import check, check_out, to_np, F32_ATOL
 pytestmark = pytest.mark.gpu
 
 
-def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_idx=None):
+def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_idx=None, ramp=0.0):
     import oracle
     import paper_2608_30252_amd as mad
     from paper_2608_30252_amd import synth
@@ -33,6 +33,11 @@ def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_id
     raw_v = synth.normal((B, Hkv, q_cap, d), 100 * seed + 4)
     mem_k = synth.normal((B, Hkv, mem_cap, d), 100 * seed + 5)
     mem_v = synth.normal((B, Hkv, mem_cap, d), 100 * seed + 6)
+    if ramp:
+        # keys grow along the sequence: each row's running maximum keeps jumping by far more than
+        # 2^8 from tile to tile, so the online softmax must rebase it many times
+        raw_k = (raw_k.float() * (1 + ramp * torch.arange(q_cap).float() / q_cap)[None, None, :, None]).to(raw_k.dtype)
+        mem_k = (mem_k.float() * (1 + ramp * torch.arange(mem_cap).float() / mem_cap)[None, None, :, None]).to(mem_k.dtype)
     s = min(S, q_cap)
     mem_k[:, :, :s], mem_v[:, :, :s] = raw_k[:, :, :s], raw_v[:, :, :s]   # the sinks are raw tokens 0..S-1
 
@@ -103,3 +108,11 @@ def test_32k_prefix_full_size_sampled():
                          rng.integers(0, 32768, 12).tolist()))
     slot_idx = sorted(set([1, 2, 4, 5, 64, 65, 1024, 2047, 2048] + rng.integers(1, 2049, 6).tolist()))
     _run(32, 8, 64, S=0, W=1024, r=16, u=4, P_list=[32768], seed=11, raw_idx=raw_idx, slot_idx=slot_idx)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_growing_scores_rebase_the_running_maximum(d):
+    # keys scaled by 1 .. 5 along the prefix: the late tiles' scores exceed the early ones' by more than
+    # 2^8, so the lazily rebased maximum moves within a pass (larger scores would put the lse below the
+    # 1e-5 bar's reach: fp32 spacing at |lse| ~ 50 is 4e-6)
+    _run(8, 2, d, S=4, W=300, r=8, u=2, P_list=[2500, 1700], seed=23, ramp=4.0)
