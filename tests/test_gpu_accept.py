@@ -34,12 +34,13 @@ def _run(logits_t, draft):
     return na.cpu().numpy(), nx.cpu().numpy()
 
 
-@pytest.mark.parametrize("B,T", [(4, 5), (1, 5), (16, 6), (3, 1)])
-def test_planted_acceptance_fp32(B, T):
+@pytest.mark.parametrize("B,T,V", [(4, 5, 128256), (1, 5, 128256), (16, 6, 128256), (3, 1, 128256),
+                                   (2, 256, 1001), (64, 3, 4099)])
+def test_planted_acceptance_fp32(B, T, V):
+    # the last two: the largest T (256 rows of a sequence) and the largest batch, unaligned vocabularies
     import oracle
     from paper_2608_30252_amd import synth
-    V = 128256
-    logits = synth.normal((B, T, V), 500 + B * 10 + T, dtype=torch.float32)
+    logits = synth.normal((B, T, V), 500 + B * 10 + T + V, dtype=torch.float32)
     x = logits.numpy()
     draft, ks = _planted(x, seed=B + T) if T > 1 else (np.zeros((B, 0), np.int32), np.zeros(B, int))
     na, nx = _run(logits, draft)

@@ -44,7 +44,7 @@ def _check(q, k, v, length, out, lse, bs=None):
 
 
 @pytest.mark.parametrize("Hq,Hkv,d,T", [(32, 8, 128, 5), (64, 8, 128, 5), (32, 8, 64, 6), (16, 1, 128, 4),
-                                        (8, 8, 128, 1), (16, 16, 64, 2)])
+                                        (8, 8, 128, 1), (16, 16, 64, 2), (64, 4, 64, 4), (32, 2, 128, 4)])
 def test_small_shapes(Hq, Hkv, d, T):
     B, cap = 2, 520
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=Hq + d + T)
