@@ -42,18 +42,50 @@ __device__ __forceinline__ uint64_t argmax_key(float x, int idx) {
 }
 __device__ __forceinline__ int key_index(uint64_t k) { return (int)(0xffffffffu - (uint32_t)k); }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    const int lo = __shfl_xor((int)(uint32_t)v, m, 64);
-    const int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, 64);
-    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+// Cross-lane exchanges of 64-bit values (two 32-bit halves) on the vector ALU,
+// without an LDS round trip: DPP within rows of 16 lanes, then the gfx950
+// lane swaps between rows.  dpp_u64<CTRL, ROWS>: the DPP move CTRL into the
+// rows of ROWS; lanes without a source, and rows outside ROWS, read 0.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROWS, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROWS, 0xF, false);
+    return ((uint64_t)hi << 32) | lo;
+}
+// the values of lanes l & ~W and l | W (W = 16 or 32), in that order
+template <int W>
+__device__ __forceinline__ void lane_pair_u64(uint64_t v, uint64_t &a, uint64_t &b) {
+    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    if constexpr (W == 16) {
+        const auto l = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto h = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        a = ((uint64_t)h[0] << 32) | l[0];
+        b = ((uint64_t)h[1] << 32) | l[1];
+    } else {
+        const auto l = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto h = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        a = ((uint64_t)h[0] << 32) | l[0];
+        b = ((uint64_t)h[1] << 32) | l[1];
+    }
+}
+// f folded over the 64 lanes, the same value in every lane: pairs within a
+// quad, then the two quads of 8 lanes (half mirror), the two 8s of a row
+// (mirror), the two 16s of 32 lanes, the two 32s.  Every lane combines the same
+// operands in the same order, so a floating-point sum is bitwise uniform.
+template <typename F>
+__device__ __forceinline__ uint64_t wave_fold_u64(uint64_t v, F f) {
+    v = f(v, dpp_u64<0xB1>(v));    // quad_perm [1, 0, 3, 2]
+    v = f(v, dpp_u64<0x4E>(v));    // quad_perm [2, 3, 0, 1]
+    v = f(v, dpp_u64<0x141>(v));   // row_half_mirror
+    v = f(v, dpp_u64<0x140>(v));   // row_mirror
+    uint64_t a, b;
+    lane_pair_u64<16>(v, a, b);
+    v = f(a, b);
+    lane_pair_u64<32>(v, a, b);
+    return f(a, b);
 }
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-    #pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-        const uint64_t o = shfl_xor_u64(v, m);
-        v = o > v ? o : v;
-    }
-    return v;
+    return wave_fold_u64(v, [](uint64_t x, uint64_t y) { return x > y ? x : y; });
 }
 __device__ __forceinline__ void store_agent_u64(uint64_t *p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -162,26 +194,21 @@ size_t accept_ws_bytes(int B, int T, int V) {
 
 // ---------------------------------------------------------- stochastic ----
 
-__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
-    const uint64_t u = __double_as_longlong(v);
-    const int lo = __shfl_xor((int)(uint32_t)u, m, 64);
-    const int hi = __shfl_xor((int)(uint32_t)(u >> 32), m, 64);
-    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+__device__ __forceinline__ uint64_t add_f64_bits(uint64_t x, uint64_t y) {
+    return (uint64_t)__double_as_longlong(__longlong_as_double((long long)x) + __longlong_as_double((long long)y));
 }
-__device__ __forceinline__ double shfl_up_f64(double v, int d) {
-    const uint64_t u = __double_as_longlong(v);
-    const int lo = __shfl_up((int)(uint32_t)u, d, 64);
-    const int hi = __shfl_up((int)(uint32_t)(u >> 32), d, 64);
-    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
-}
-// inclusive prefix sum over the 64 lanes of a wave (lane order)
-__device__ __forceinline__ double wave_scan_f64(double v, int lane) {
-    #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const double y = shfl_up_f64(v, d);
-        if (lane >= d) v += y;
-    }
-    return v;
+// inclusive prefix sum over the 64 lanes of a wave (lane order): shifts by 1,
+// 2, 4, 8 within each row of 16, then row 0's total into row 1 and row 2's
+// into row 3 (row_bcast:15), then rows 0-1's total into rows 2-3 (row_bcast:31)
+__device__ __forceinline__ double wave_scan_f64(double v) {
+    uint64_t u = (uint64_t)__double_as_longlong(v);
+    u = add_f64_bits(u, dpp_u64<0x111>(u));
+    u = add_f64_bits(u, dpp_u64<0x112>(u));
+    u = add_f64_bits(u, dpp_u64<0x114>(u));
+    u = add_f64_bits(u, dpp_u64<0x118>(u));
+    u = add_f64_bits(u, dpp_u64<0x142, 0xA>(u));
+    u = add_f64_bits(u, dpp_u64<0x143, 0xC>(u));
+    return __longlong_as_double((long long)u);
 }
 __device__ __forceinline__ double read_lane_f64(double v, int l) {
     const uint64_t u = __double_as_longlong(v);
@@ -190,9 +217,7 @@ __device__ __forceinline__ double read_lane_f64(double v, int l) {
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 __device__ __forceinline__ double wave_sum_f64(double v) {
-    #pragma unroll
-    for (int m = 1; m < 64; m <<= 1) v += shfl_xor_f64(v, m);
-    return v;
+    return __longlong_as_double((long long)wave_fold_u64((uint64_t)__double_as_longlong(v), add_f64_bits));
 }
 // weight of entry v in the draw: max(0, p - q) (q given) or max(0, p)
 __device__ __forceinline__ double draw_weight(float p, float q, bool resid) {
@@ -305,7 +330,7 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
         int cs = -1, clast = -1;
         for (int c0 = 0; c0 < nc; c0 += 64) {
             const double w = c0 + lane < nc ? chunk_sum(c0 + lane, use_p) : 0.0;
-            const double incl = wave_scan_f64(w, lane);
+            const double incl = wave_scan_f64(w);
             const unsigned long long pos = __ballot(w > 0.0);
             const unsigned long long hit = __ballot(w > 0.0 && carry + incl > t);
             if (pos) clast = c0 + 63 - __clzll((long long)pos);
@@ -337,16 +362,31 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     double w[RUN];
     double mine = 0.0;
     int lastpos = -1;
+    if (a.vec16 && r0 + RUN <= cend) {
+        #pragma unroll
+        for (int k = 0; k < RUN / 4; ++k) {
+            const float4 pv = *reinterpret_cast<const float4 *>(pr + r0 + 4 * k);
+            const float4 qv = wres ? *reinterpret_cast<const float4 *>(qr + r0 + 4 * k) : make_float4(0.f, 0.f, 0.f, 0.f);
+            w[4 * k + 0] = draw_weight(pv.x, qv.x, wres);
+            w[4 * k + 1] = draw_weight(pv.y, qv.y, wres);
+            w[4 * k + 2] = draw_weight(pv.z, qv.z, wres);
+            w[4 * k + 3] = draw_weight(pv.w, qv.w, wres);
+        }
+    } else {
+        #pragma unroll
+        for (int i = 0; i < RUN; ++i) {
+            const int v = r0 + i;
+            w[i] = v < cend ? draw_weight(pr[v], wres ? qr[v] : 0.f, wres) : 0.0;
+        }
+    }
     #pragma unroll
     for (int i = 0; i < RUN; ++i) {
-        const int v = r0 + i;
-        w[i] = v < cend ? draw_weight(pr[v], wres ? qr[v] : 0.f, wres) : 0.0;
         mine += w[i];
-        if (w[i] > 0.0) lastpos = v;
+        if (w[i] > 0.0) lastpos = r0 + i;
     }
     __shared__ double s_wt[4];
     __shared__ int s_first[4], s_last[4];
-    const double incl = wave_scan_f64(mine, lane);
+    const double incl = wave_scan_f64(mine);
     if (lane == 63) s_wt[wave] = incl;
     __syncthreads();
     double excl = incl - mine;
@@ -354,9 +394,7 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     const double tt = s_t;
     const bool hit = !s_fb && mine > 0.0 && excl + mine > tt;
     const unsigned long long hm = __ballot(hit);
-    int lp = lastpos;
-    #pragma unroll
-    for (int m = 1; m < 64; m <<= 1) lp = max(lp, __shfl_xor(lp, m, 64));
+    const int lp = (int)wave_max_u64((uint64_t)(lastpos + 1)) - 1;   // lastpos >= -1
     if (lane == 0) {
         s_first[wave] = hm ? wave * 64 + __ffsll((long long)hm) - 1 : 0x7fffffff;
         s_last[wave] = lp;
