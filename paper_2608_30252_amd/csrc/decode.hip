@@ -503,8 +503,8 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
         #pragma unroll
         for (int hi = 0; hi < C::HW; ++hi) {
             if constexpr (C::KSW == 2) {
-                o_acc[hi][0] += __shfl_xor(o_acc[hi][0], 32, 64);
-                o_acc[hi][1] += __shfl_xor(o_acc[hi][1], 32, 64);
+                o_acc[hi][0] = pair_sum<32>(o_acc[hi][0]);
+                o_acc[hi][1] = pair_sum<32>(o_acc[hi][1]);
             }
         }
         #pragma unroll

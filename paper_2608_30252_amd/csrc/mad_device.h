@@ -60,9 +60,11 @@ __device__ __forceinline__ void unpack16(const uint4 &u, float (&f)[8], bf16_t) 
     f[4] = bf16_lo(u.z); f[5] = bf16_hi(u.z); f[6] = bf16_lo(u.w); f[7] = bf16_hi(u.w);
 }
 
-// Cross-lane exchange inside a wave64.  Patterns 1 and 2 use DPP quad
-// permutes, 4 and 8 use DPP row mirrors (valid for sum/max reductions over
-// aligned groups), 16 and 32 use ds_swizzle / permute through the LDS crossbar.
+// Cross-lane exchange inside a wave64, all on the vector ALU (no LDS
+// crossbar).  Patterns 1 and 2 use DPP quad permutes, 4 and 8 use DPP row
+// mirrors (valid for sum/max reductions over aligned groups); across 16 and
+// 32 lanes the gfx950 lane swaps v_permlane16_swap / v_permlane32_swap give
+// every lane the values of lanes l & ~X and l | X (pair_sum, pair_max).
 template <int X> __device__ __forceinline__ float xor_lane(float v);
 template <> __device__ __forceinline__ float xor_lane<1>(float v) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));
@@ -80,12 +82,25 @@ template <> __device__ __forceinline__ float xor_lane<4>(float v) {
 template <> __device__ __forceinline__ float xor_lane<8>(float v) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, true));
 }
-template <> __device__ __forceinline__ float xor_lane<16>(float v) {
-    // ds_swizzle bitmask mode inside 32-lane halves: and 0x1f, or 0, xor 0x10.
-    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
+// v + v[l ^ X] for X = 16 or 32, the operands in the same order in both lanes
+// of a pair (the two lanes' results are bitwise equal)
+template <int X> __device__ __forceinline__ float pair_sum(float v) {
+    if constexpr (X == 16) {
+        const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+    } else {
+        const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+    }
 }
-template <> __device__ __forceinline__ float xor_lane<32>(float v) {
-    return __shfl_xor(v, 32, 64);
+template <int X> __device__ __forceinline__ float pair_max(float v) {
+    if constexpr (X == 16) {
+        const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+    } else {
+        const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+    }
 }
 
 // Reduce over aligned groups of N consecutive lanes (N a power of two <= 64).
@@ -96,24 +111,17 @@ template <int N> __device__ __forceinline__ float group_sum(float v) {
     if constexpr (N >= 4) v += xor_lane<2>(v);
     if constexpr (N >= 8) v += xor_lane<4>(v);
     if constexpr (N >= 16) v += xor_lane<8>(v);
-    if constexpr (N >= 32) v += xor_lane<16>(v);
-    if constexpr (N >= 64) v += xor_lane<32>(v);
+    if constexpr (N >= 32) v = pair_sum<16>(v);
+    if constexpr (N >= 64) v = pair_sum<32>(v);
     return v;
 }
-
-// Reduce over lanes that share (lane % STRIDE), i.e. across the 64/STRIDE
-// groups of STRIDE lanes.  Uses exchanges with partners lane ^ k for k >=
-// STRIDE; every pattern here is a true xor for k >= 16 and a mirror for
-// k in {4, 8}.  Mirrors do not preserve (lane % STRIDE), so for STRIDE < 16
-// the generic permute is used instead.
-template <int STRIDE> __device__ __forceinline__ float strided_max(float v) {
-    #pragma unroll
-    for (int k = STRIDE; k < 64; k <<= 1) v = fmaxf(v, __shfl_xor(v, k, 64));
-    return v;
-}
-template <int STRIDE> __device__ __forceinline__ float strided_sum(float v) {
-    #pragma unroll
-    for (int k = STRIDE; k < 64; k <<= 1) v += __shfl_xor(v, k, 64);
+template <int N> __device__ __forceinline__ float group_max(float v) {
+    if constexpr (N >= 2) v = fmaxf(v, xor_lane<1>(v));
+    if constexpr (N >= 4) v = fmaxf(v, xor_lane<2>(v));
+    if constexpr (N >= 8) v = fmaxf(v, xor_lane<4>(v));
+    if constexpr (N >= 16) v = fmaxf(v, xor_lane<8>(v));
+    if constexpr (N >= 32) v = pair_max<16>(v);
+    if constexpr (N >= 64) v = pair_max<32>(v);
     return v;
 }
 

@@ -516,9 +516,7 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     float m0 = -INFINITY, m1 = -INFINITY, l0 = 0.f, l1 = 0.f;
     if (tid < ns) { m0 = pml[tid * sml]; l0 = pml[tid * sml + 1]; }
     if (tid + D < ns) { m1 = pml[(tid + D) * sml]; l1 = pml[(tid + D) * sml + 1]; }
-    float m = fmaxf(m0, m1);
-    #pragma unroll
-    for (int x = 1; x < 64; x <<= 1) m = fmaxf(m, __shfl_xor(m, x, 64));
+    const float m = group_max<64>(fmaxf(m0, m1));
     if (lane == 0) s_red[0][wave] = m;
     __syncthreads();
     float M = s_red[0][0];
@@ -526,9 +524,7 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
     for (int w = 1; w < NW; ++w) M = fmaxf(M, s_red[0][w]);
     const float w0 = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
     const float w1 = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-    float lsum = w0 * l0 + w1 * l1;
-    #pragma unroll
-    for (int x = 1; x < 64; x <<= 1) lsum += __shfl_xor(lsum, x, 64);
+    const float lsum = group_sum<64>(w0 * l0 + w1 * l1);
     if (lane == 0) s_red[1][wave] = lsum;
     __syncthreads();
     float L = 0.f;
