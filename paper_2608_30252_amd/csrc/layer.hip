@@ -80,6 +80,14 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinearArgs a) {
         for (int j = 0; j < KD; ++j)
             wr[c][j] = *reinterpret_cast<const uint4 *>(w + (size_t)col[c] * D + (tid + 256 * j) * 8);
 
+    // the norm weights, loaded with everything else rather than after the barrier
+    uint4 gr[KD];
+    if constexpr (NORM) {
+        const bf16_t *gm = reinterpret_cast<const bf16_t *>(a.gamma);
+        #pragma unroll
+        for (int j = 0; j < KD; ++j) gr[j] = *reinterpret_cast<const uint4 *>(gm + (tid + 256 * j) * 8);
+    }
+
     // ---- RMSNorm of the input rows (fp32), rounded to bf16 for the product ----
     if constexpr (NORM) {
         float ss[RR];
@@ -99,10 +107,6 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinearArgs a) {
             if (lane == 0) s_sq[wave][r] = ss[r];
         }
         __syncthreads();
-        const bf16_t *gm = reinterpret_cast<const bf16_t *>(a.gamma);
-        uint4 gr[KD];
-        #pragma unroll
-        for (int j = 0; j < KD; ++j) gr[j] = *reinterpret_cast<const uint4 *>(gm + (tid + 256 * j) * 8);
         #pragma unroll
         for (int r = 0; r < RR; ++r) {
             const float tot = s_sq[0][r] + s_sq[1][r] + s_sq[2][r] + s_sq[3][r];
