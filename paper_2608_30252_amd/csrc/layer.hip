@@ -227,13 +227,14 @@ static hipError_t launch_kd(const LinearArgs &a, int grid, hipStream_t st) {
 
 // Features per workgroup (measured): 2 for Q/K/V (one rotation pair each,
 // 1536 workgroups; 5% faster than two pairs), 8 for the output projection (one
-// workgroup per CU; 2 and 4 measure the same), 4 for the wide down projection,
-// 8 (4 gate + 4 up) for the SwiGLU map.
+// workgroup per CU; 2 and 4 measure the same), 2 for the wide down projection
+// (1024 workgroups; 3% faster than 4), 8 (4 gate + 4 up) for the SwiGLU map (4
+// and 16 are slower).
 hipError_t launch_linear(const LinearArgs &a, int mode, hipStream_t st) {
     if (mode == kLinQKV) return launch_kd<kLinQKV, 2>(a, a.N / 2, st);
     if (mode == kLinSwiglu) return launch_kd<kLinSwiglu, 8>(a, a.N / 4, st);
     if (mode == kLinRes) {
-        if (a.D / 2048 == 4) return launch_rr<kLinRes, 4, 4>(a, a.N / 4, st);
+        if (a.D / 2048 == 4) return launch_rr<kLinRes, 2, 4>(a, a.N / 2, st);
         if (a.N % 8 == 0) return launch_kd<kLinRes, 8>(a, a.N / 8, st);
         return launch_kd<kLinRes, 4>(a, a.N / 4, st);
     }
