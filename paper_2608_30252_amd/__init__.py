@@ -122,16 +122,48 @@ class KV:
     length: Sequence[int]
     start: Optional[Sequence[int]] = None
 
-    def view(self, B):
+    def view(self, B, Hkv=None, d=None, dtype=None, device=None, name="kv"):
+        """The C view of this pair for a call over B rows.  The batch dimension
+        must be B, or 1 (every row then aliases sequence 0: seq_stride 0); the
+        KV heads, head_dim, dtype and device must match the call's."""
         k, v = self.k, self.v
         if k.dim() != 4 or k.shape != v.shape or k.stride() != v.stride():
-            raise ValueError("K and V must be [B, Hkv, cap, d] tensors with identical strides")
+            raise ValueError(f"{name}: K and V must be [B, Hkv, cap, d] tensors with identical strides")
         if k.stride(3) != 1 or k.stride(2) != k.shape[3]:
-            raise ValueError("K/V rows must be contiguous")
+            raise ValueError(f"{name}: K/V rows must be contiguous")
+        if k.shape[0] not in (1, B):
+            raise ValueError(f"{name}: batch dimension {k.shape[0]} must be 1 or B={B}")
+        if Hkv is not None and k.shape[1] != Hkv:
+            raise ValueError(f"{name}: {k.shape[1]} KV heads, the call has {Hkv}")
+        if d is not None and k.shape[3] != d:
+            raise ValueError(f"{name}: head_dim {k.shape[3]}, the call has {d}")
+        if dtype is not None and (k.dtype != dtype or v.dtype != dtype):
+            raise ValueError(f"{name}: dtype {k.dtype}, the call has {dtype}")
+        if device is not None and (k.device != device or v.device != device):
+            raise ValueError(f"{name}: tensors on {k.device}, the call is on {device}")
+        if len(self.length) < B or (self.start is not None and len(self.start) < B):
+            raise ValueError(f"{name}: lengths/starts need one entry per row ({B})")
         self._len = _host_i32(self.length, B)
         self._start = _host_i32(self.start, B) if self.start is not None else None
         return _KVView(k.data_ptr(), v.data_ptr(), k.stride(0) if k.shape[0] > 1 else 0, k.stride(1),
                        k.shape[2], self._start, self._len)
+
+
+def _need(cond, msg):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _contiguous(**tensors):
+    for name, t in tensors.items():
+        if t is not None and not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+
+def _same_device(dev, **tensors):
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, the call is on {dev}")
 
 
 class Workspace:
@@ -154,19 +186,51 @@ _default_ws = {}
 
 
 def _ws_for(device, nbytes, ws):
+    """The caller's workspace, or one kept per (device, stream): calls issued
+    in order on one stream may share a workspace, calls on different streams
+    must not (their arrival counters and partials would overlap)."""
     if ws is not None:
         if ws.numel() < nbytes:
             raise ValueError(f"workspace of {ws.numel()} bytes < {nbytes} needed")
         return ws
-    key = torch.device(device).index
+    dev = torch.device(device)
+    key = (dev.index, torch.cuda.current_stream(dev).cuda_stream)
     w = _default_ws.get(key)
     if w is None:
-        w = _default_ws[key] = Workspace(device)
+        w = _default_ws[key] = Workspace(dev)
     return w.get(nbytes)
 
 
 def workspace_bytes(op, B=1, Hq=1, Hkv=1, d=64, T=1, max_keys=0) -> int:
     return int(_load_library().mad_workspace_bytes(op, B, Hq, Hkv, d, T, max_keys))
+
+
+def _decode_args(q, mem, win, k_new, v_new, out, lse, scale):
+    """Checks shared by the two decode entry points; returns the marshalled
+    arguments (B, Hq, Hkv, d, out, lse, scale, mem view, window view)."""
+    _need(q.dim() == 3, "q must be [B, Hq, d]")
+    B, Hq, d = q.shape
+    _need(mem is not None or win is not None, "mem and win cannot both be None")
+    Hkv = (mem.k if mem is not None else win.k).shape[1]
+    _need(Hkv >= 1 and Hq % Hkv == 0, f"Hq={Hq} must be a multiple of the KV heads {Hkv}")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    _need(out.shape == q.shape and out.dtype == q.dtype, "out must match q's shape and dtype")
+    _need(lse.shape == (B, Hq) and lse.dtype == torch.float32, "lse must be float32 [B, Hq]")
+    _need((k_new is None) == (v_new is None), "k_new and v_new go together")
+    if k_new is not None:
+        for name, t in (("k_new", k_new), ("v_new", v_new)):
+            _need(t.shape == (B, Hkv, d) and t.dtype == q.dtype, f"{name} must be [B, Hkv, d] = {(B, Hkv, d)} "
+                  f"of {q.dtype}")
+    _contiguous(q=q, out=out, lse=lse, k_new=k_new, v_new=v_new)
+    _same_device(q.device, out=out, lse=lse, k_new=k_new, v_new=v_new)
+    if scale is None:
+        scale = d ** -0.5
+    mv = mem.view(B, Hkv, d, q.dtype, q.device, "mem") if mem is not None else None
+    wv = win.view(B, Hkv, d, q.dtype, q.device, "win") if win is not None else None
+    return B, Hq, Hkv, d, out, lse, scale, mv, wv
 
 
 def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
@@ -178,16 +242,7 @@ def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
     Attends over mem rows [0, len) then the window ring rows start..start+len-1
     (mod cap) then the new token (k_new/v_new [B, Hkv, d], which is also
     written into the ring at row (start + len) % cap)."""
-    B, Hq, d = q.shape
-    Hkv = (mem.k if mem is not None else win.k).shape[1]
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
-    if scale is None:
-        scale = d ** -0.5
-    mv = mem.view(B) if mem is not None else None
-    wv = win.view(B) if win is not None else None
+    B, Hq, Hkv, d, out, lse, scale, mv, wv = _decode_args(q, mem, win, k_new, v_new, out, lse, scale)
     nbytes = workspace_bytes(MAD_OP_DECODE, B, Hq, Hkv, d)
     w = _ws_for(q.device, nbytes, ws)
     rc = _load_library().mad_draft_decode_attn(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
@@ -206,18 +261,8 @@ def draft_step_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV], k_new
     """draft_decode_attn with a per-row new-token mode (host list of B values):
     0 = no new token, 1 = attend k_new/v_new[b] only, 2 = attend and append it
     to the row's ring.  Rows may alias one sequence's buffers (batch dim 1)."""
-    B, Hq, d = q.shape
-    Hkv = (mem.k if mem is not None else win.k).shape[1]
-    if len(new_mode) != B:
-        raise ValueError("new_mode needs one entry per row")
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
-    if scale is None:
-        scale = d ** -0.5
-    mv = mem.view(B) if mem is not None else None
-    wv = win.view(B) if win is not None else None
+    B, Hq, Hkv, d, out, lse, scale, mv, wv = _decode_args(q, mem, win, k_new, v_new, out, lse, scale)
+    _need(len(new_mode) == B, "new_mode needs one entry per row")
     modes = (ctypes.c_uint8 * B)(*[int(m) for m in new_mode])
     nbytes = workspace_bytes(MAD_OP_DECODE, B, Hq, Hkv, d)
     w = _ws_for(q.device, nbytes, ws)
@@ -235,9 +280,16 @@ def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None, 
 
     Appends the slots' K (rotated at pos) and V at mem rows len[b]..len[b]+n_new-1
     of every firing sequence.  The caller then raises its lengths."""
+    _need(x.dim() == 3, "x must be [B, n_new, D]")
     B, n_new, D = x.shape
     Hkv, d = mem.k.shape[1], mem.k.shape[3]
-    mv = mem.view(B)
+    _need(w_kv.shape == (2 * Hkv * d, D) and w_kv.dtype == x.dtype,
+          f"w_kv must be [2*Hkv*d, D] = {(2 * Hkv * d, D)} of {x.dtype}")
+    _need(len(pos) == B and all(len(row) == n_new for row in pos), "pos must be [B][n_new]")
+    _need(fire is None or len(fire) == B, "fire needs one flag per sequence")
+    _contiguous(x=x, w_kv=w_kv)
+    _same_device(x.device, w_kv=w_kv)
+    mv = mem.view(B, Hkv, d, x.dtype, x.device, "mem")
     flat = [int(p) for row in pos for p in row]
     pos_arr = _host_i32(flat, B * n_new)
     fire_arr = None
@@ -286,6 +338,12 @@ def accept_greedy(logits: torch.Tensor, draft_tok: Optional[torch.Tensor], n_acc
         n_accept = torch.empty(B, dtype=torch.int32, device=dev)
     if next_tok is None:
         next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+    _need(T == 1 or (draft_tok is not None and draft_tok.shape == (B, T - 1) and draft_tok.dtype == torch.int32),
+          "draft_tok must be int32 [B, T-1]")
+    _need(n_accept.shape == (B,) and next_tok.shape == (B,) and n_accept.dtype == torch.int32
+          and next_tok.dtype == torch.int32, "n_accept and next_tok must be int32 [B]")
+    _contiguous(logits=logits, draft_tok=draft_tok, n_accept=n_accept, next_tok=next_tok)
+    _same_device(dev, draft_tok=draft_tok, n_accept=n_accept, next_tok=next_tok)
     nbytes = workspace_bytes(MAD_OP_ACCEPT, B, 1, 1, 64, T, V)
     w = _ws_for(dev, nbytes, ws)
     rc = _load_library().mad_accept_greedy(_ptr(logits), _dtype_code(logits), _ptr(draft_tok), B, T, V,
@@ -305,6 +363,14 @@ def accept_stochastic(p: torch.Tensor, q: Optional[torch.Tensor], draft_tok: Opt
         n_accept = torch.empty(B, dtype=torch.int32, device=dev)
     if next_tok is None:
         next_tok = torch.empty(B, dtype=torch.int32, device=dev)
+    _need(p.dtype == torch.float32 and u.shape == (B, T) and u.dtype == torch.float32, "p float32, u float32 [B, T]")
+    _need(T == 1 or (q is not None and q.shape == (B, T - 1, V) and q.dtype == torch.float32
+                     and draft_tok is not None and draft_tok.shape == (B, T - 1) and draft_tok.dtype == torch.int32),
+          "q float32 [B, T-1, V] and draft_tok int32 [B, T-1]")
+    _need(n_accept.shape == (B,) and next_tok.shape == (B,) and n_accept.dtype == torch.int32
+          and next_tok.dtype == torch.int32, "n_accept and next_tok must be int32 [B]")
+    _contiguous(p=p, q=q, draft_tok=draft_tok, u=u, n_accept=n_accept, next_tok=next_tok)
+    _same_device(dev, q=q, draft_tok=draft_tok, u=u, n_accept=n_accept, next_tok=next_tok)
     nbytes = workspace_bytes(MAD_OP_ACCEPT_STOCH, B, 1, 1, 64, T, V)
     w = _ws_for(dev, nbytes, ws)
     lib = _load_library()
@@ -340,9 +406,19 @@ def memory_prefill_attn(q_raw: torch.Tensor, q_slot: Optional[torch.Tensor], mem
             out_slot = torch.empty_like(q_slot)
         if lse_slot is None:
             lse_slot = torch.empty((B, slot_cap, Hq), dtype=torch.float32, device=q_raw.device)
+    _need(q_slot is None or (q_slot.dim() == 4 and q_slot.shape[0] == B and q_slot.shape[2:] == q_raw.shape[2:]
+                             and q_slot.dtype == q_raw.dtype), "q_slot must be [B, slot_cap, Hq, d] like q_raw")
+    _contiguous(q_raw=q_raw, q_slot=q_slot, out_raw=out_raw, lse_raw=lse_raw, out_slot=out_slot, lse_slot=lse_slot)
+    _same_device(q_raw.device, q_slot=q_slot, out_raw=out_raw, lse_raw=lse_raw, out_slot=out_slot,
+                 lse_slot=lse_slot)
+    _need(out_raw.shape == q_raw.shape and lse_raw.shape == (B, q_cap, Hq), "out_raw/lse_raw shapes")
+    _need(q_slot is None or (out_slot.shape == q_slot.shape and lse_slot.shape == (B, slot_cap, Hq)),
+          "out_slot/lse_slot shapes")
+    _need(len(P) == B, "P needs one entry per sequence")
     if scale is None:
         scale = d ** -0.5
-    mv, rv = mem.view(B), raw.view(B)
+    mv = mem.view(B, Hkv, d, q_raw.dtype, q_raw.device, "mem")
+    rv = raw.view(B, Hkv, d, q_raw.dtype, q_raw.device, "raw")
     plen = _host_i32(P, B)
     rc = _load_library().mad_memory_prefill_attn(
         _ptr(q_raw), _ptr(q_slot), B, Hq, Hkv, d, _dtype_code(q_raw), float(scale), plen, q_cap, slot_cap,
@@ -366,6 +442,13 @@ def rmsnorm_qkv_rope(x: torch.Tensor, gamma: torch.Tensor, w_qkv: torch.Tensor, 
         k = torch.empty((R, Hkv, d), dtype=x.dtype, device=x.device)
     if v is None:
         v = torch.empty((R, Hkv, d), dtype=x.dtype, device=x.device)
+    _need(x.dtype == torch.bfloat16, "the draft-layer maps run in bf16")
+    _need(gamma.shape == (D,) and w_qkv.shape == ((Hq + 2 * Hkv) * d, D), "gamma [D], w_qkv [(Hq+2Hkv)d, D]")
+    _need(q.shape == (R, Hq, d) and k.shape == (R, Hkv, d) and v.shape == (R, Hkv, d), "q/k/v output shapes")
+    _need(xn is None or xn.shape == (R, D), "xn must be [R, D]")
+    _need(len(pos) == R, "pos needs one entry per row")
+    _contiguous(x=x, gamma=gamma, w_qkv=w_qkv, q=q, k=k, v=v, xn=xn)
+    _same_device(x.device, gamma=gamma, w_qkv=w_qkv, q=q, k=k, v=v, xn=xn)
     rc = _load_library().mad_rmsnorm_qkv_rope(_ptr(x), _ptr(gamma), float(eps), _ptr(w_qkv), _host_i32(pos, R), R,
                                               D, Hq, Hkv, d, float(rope_base), 1 if kv_from_row0 else 0, _ptr(q),
                                               _ptr(k), _ptr(v), _ptr(xn), _stream(x.device))
@@ -379,6 +462,10 @@ def linear_residual(x: torch.Tensor, w: torch.Tensor, res: torch.Tensor, out: Op
     N = w.shape[0]
     if out is None:
         out = torch.empty((R, N), dtype=x.dtype, device=x.device)
+    _need(x.dtype == torch.bfloat16 and w.shape == (N, D) and res.shape == (R, N) and out.shape == (R, N),
+          "x [R, D], w [N, D], res and out [R, N], bf16")
+    _contiguous(x=x, w=w, res=res, out=out)
+    _same_device(x.device, w=w, res=res, out=out)
     _check(_load_library().mad_linear_residual(_ptr(x), _ptr(w), _ptr(res), R, D, N, _ptr(out), _stream(x.device)))
     return out
 
@@ -390,6 +477,10 @@ def rmsnorm_swiglu(x: torch.Tensor, gamma: torch.Tensor, w_gate_up: torch.Tensor
     Fd = w_gate_up.shape[0] // 2
     if out is None:
         out = torch.empty((R, Fd), dtype=x.dtype, device=x.device)
+    _need(x.dtype == torch.bfloat16 and gamma.shape == (D,) and w_gate_up.shape == (2 * Fd, D)
+          and out.shape == (R, Fd), "x [R, D], gamma [D], w_gate_up [2F, D], out [R, F], bf16")
+    _contiguous(x=x, gamma=gamma, w_gate_up=w_gate_up, out=out)
+    _same_device(x.device, gamma=gamma, w_gate_up=w_gate_up, out=out)
     _check(_load_library().mad_rmsnorm_swiglu(_ptr(x), _ptr(gamma), float(eps), _ptr(w_gate_up), R, D, Fd,
                                               _ptr(out), _stream(x.device)))
     return out

@@ -32,12 +32,11 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def build(verbose: bool = False, extra_defines=(), out: str = LIB, build_dir: str = BUILD_DIR) -> str:
+def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR) -> str:
     os.makedirs(build_dir, exist_ok=True)
     cc = hipcc()
     common = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
               "-Wno-unused-function", "-I", os.path.join(HERE, "..", "include")] + DEVICE_FLAGS
-    common += [f"-D{d}" for d in extra_defines]
 
     def compile_one(src):
         obj = os.path.join(build_dir, os.path.basename(src) + ".o")

@@ -145,8 +145,11 @@ __global__ __launch_bounds__(256) void accept_kernel(const AcceptArgs a) {
     if (tid == 0) {
         uint64_t m = s_w[0];
         for (int w = 1; w < 4; ++w) m = s_w[w] > m ? s_w[w] : m;
-        // the returned value is awaited: the max is performed before the arrival
+        // the maximum must have been performed at device scope before the
+        // arrival is counted: the atomic's result is not used, so the compiler
+        // may issue its no-return form; vmcnt(0) waits for it either way
         (void)max_agent_u64(a.row_best + row, m);
+        wait_vm_stores();
         const int b = row / a.T;
         unsigned *cnt = a.counters + (size_t)b * kCounterStride;
         const int last = arrive(cnt) == (unsigned)(a.T * a.n_chunks - 1);

@@ -86,17 +86,6 @@ struct DecodeCfg {
     static_assert(NSUB * G * (D + 2) * 4 <= SZ_ST, "group merge buffer fits the stages");
 };
 
-// vmcnt(n) for n in {0, 4, 8, 12} (the tile loads are the only vector memory
-// operations in flight inside the pipeline; 4 per super-tile and thread).
-__device__ __forceinline__ void wait_vmcnt(int n) {
-    switch (n) {
-        case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-        case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
-        case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
-        default: __builtin_amdgcn_s_waitcnt(0x0F7C); break;   // 12
-    }
-}
-
 typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, a), __builtin_bit_cast(bf16x2_v, b), c,
@@ -162,7 +151,7 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
         if (off + lane * 16 < nbytes)
             lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, lds + off);
     }
-    wait_vmcnt(0);
+    wait_vm(0);
     __syncthreads();
     const float *lo = reinterpret_cast<const float *>(lds);                               // [n_splits][G][D]
     const float2 *lml = reinterpret_cast<const float2 *>(lo + (size_t)n_splits * G * D);  // [n_splits][G]
@@ -352,7 +341,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     for (; issued < nst && issued < C::STAGES - 1; ++issued) issue(k0 + issued * C::SUPER, issued);
 
     for (int t = 0; t < nst; ++t) {
-        wait_vmcnt(4 * (issued - t - 1));
+        wait_vm(4 * (issued - t - 1));
         __syncthreads();   // super-tile t is in LDS for every wave; stage (t-1) % STAGES is free
         if (issued < nst) {
             issue(k0 + issued * C::SUPER, issued % C::STAGES);
@@ -590,9 +579,6 @@ static int decode_tile(int dtype, int d) { return 8192 / (d * (dtype == MAD_BF16
 // possible.
 static int decode_nsub(int units, int n_max, int G, int d, int dtype) {
     if (!(dtype == MAD_BF16 && d == 64 && G <= 4)) return 1;
-#ifdef MAD_DECODE_FORCE_NSUB
-    return MAD_DECODE_FORCE_NSUB;
-#endif
     const bool wide = (int64_t)units * n_max >= kDecodeWideKeys;
     return wide ? 2 : 1;
 }
@@ -609,7 +595,7 @@ DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_key
     // two per CU when there is enough work to need the loads in flight of both
     const int64_t total = (int64_t)p.units * p.n_max;
     const int per_cu = p.nsub == 2 ? 2 : (total >= kDecodeWideKeys ? 2 : 1);
-    const int target = per_cu * kDecodeCUs / kDecodeTargetDiv;
+    const int target = per_cu * kDecodeCUs;
     int ns = (target + p.units - 1) / p.units;
     const int cap = decode_max_splits(d, G);
     if (ns > cap) ns = cap;

@@ -132,10 +132,17 @@ template <int N> __device__ __forceinline__ float group_max(float v) {
 __device__ __forceinline__ double rope_theta(int j, int d, double log2_base) {
     return exp2(-2.0 * (double)j / (double)d * log2_base);
 }
-__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
-    const double a = (double)pos * theta;
+// a - n * 2 pi with n = rint(a / (2 pi)): 2 pi split as hi + lo, hi the double
+// nearest 2 pi and lo the double nearest 2 pi - hi.  The inner fma forms
+// a - n * hi with a single rounding (its product is exact inside the fma), the
+// outer one subtracts n * lo, so the reduced angle is within a few ulps of the
+// exact a - n * 2 pi for every angle a position id reaches.
+__host__ __device__ inline double rope_reduce(double a) {
     const double n = rint(a * 0.15915494309189535);            // 1 / (2 pi)
-    const double r = fma(-n, 1.2246467991473532e-16, fma(-n, 6.283185307179586, a));   // 2 pi = hi + lo
+    return fma(-n, 2.4492935982947064e-16, fma(-n, 6.283185307179586, a));
+}
+__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
+    const double r = rope_reduce((double)pos * theta);
     float s, c;
     sincosf((float)r, &s, &c);
     *k0 = y0 * c - y1 * s;

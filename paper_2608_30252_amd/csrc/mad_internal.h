@@ -16,10 +16,6 @@ constexpr int kMaxB = MAD_MAX_BATCH;
 // are whole super-tiles (see plan_decode).
 constexpr int kDecodeCUs = 256;        // compute units of the device the split plan is sized for
 constexpr int kDecodeWideKeys = 65536;      // 8-wave workgroups: launches holding at least this many keys
-#ifndef MAD_DECODE_TARGET_DIV
-#define MAD_DECODE_TARGET_DIV 1
-#endif
-constexpr int kDecodeTargetDiv = MAD_DECODE_TARGET_DIV;   // fewer, longer splits (tuning)
 constexpr int kDecodeMaxSplits = 256;
 // Every workspace starts with a fixed counter region that holds nothing but
 // arrival counters (one per 256-byte line) and that every kernel leaves at
@@ -75,10 +71,7 @@ constexpr int kUpdateGemvRows = 8;   // bf16 updates of at most this many rows t
 bool update_uses_gemv(int R, int D, int dtype);
 
 // ---------------------------------------------------------------- verify ----
-#ifndef MAD_VERIFY_TARGET_WGS
-#define MAD_VERIFY_TARGET_WGS 256
-#endif
-constexpr int kVerifyTargetWGs = MAD_VERIFY_TARGET_WGS;
+constexpr int kVerifyTargetWGs = 256;   // workgroups the split count aims at (one per CU)
 constexpr int kVerifyMaxSplits = 128;
 
 struct VerifyArgs {

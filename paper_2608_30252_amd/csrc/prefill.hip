@@ -47,12 +47,9 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_v;
 
-#ifndef MAD_PREFILL_KT64
-#define MAD_PREFILL_KT64 64
-#endif
 template <int D>
 struct PrefillCfg {
-    static constexpr int KT = D == 64 ? MAD_PREFILL_KT64 : 64;   // keys per tile (128 spills registers at d 64)
+    static constexpr int KT = 64;                     // keys per tile (128 spills registers at d 64)
     static constexpr int KH = KT / 32;                 // 32-key halves of a tile
     static constexpr int RB = D * 2;                   // bytes per K row
     static constexpr int CPR = RB / 16;                // 16-byte chunks per K row
@@ -366,11 +363,8 @@ __global__ __launch_bounds__(256, NB == 2 ? (D == 64 ? 3 : 2) : 1) void prefill_
 
 // ------------------------------------------------------------------ host ----
 
-#ifndef MAD_PREFILL_NB64
-#define MAD_PREFILL_NB64 2
-#endif
-// 16-row blocks per wave: 2 (two workgroups per CU) unless tuned otherwise
-static constexpr int prefill_nb(int d) { return d == 64 ? MAD_PREFILL_NB64 : 2; }
+// 16-row blocks per wave (two workgroups per CU)
+static constexpr int prefill_nb(int) { return 2; }
 
 int prefill_tokens_per_block(int d, int G) { return 16 * 4 * prefill_nb(d) / G; }
 

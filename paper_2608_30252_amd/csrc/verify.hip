@@ -27,12 +27,7 @@
 
 namespace mad {
 
-#ifndef MAD_VERIFY_REGS
-#define MAD_VERIFY_REGS 0   // 1: the register-resident split kernel for every shape
-#endif
-#ifndef MAD_VERIFY_LDS_MIN_NB
-#define MAD_VERIFY_LDS_MIN_NB 2   // query row blocks from which the LDS-staged kernel is used
-#endif
+constexpr int kVerifyLdsMinNb = 2;   // query row blocks from which the LDS-staged kernel is used
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
@@ -564,7 +559,7 @@ VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len) {
     if (ns < 1) ns = 1;
     int chunk = (n_max + ns - 1) / ns;
     // whole slabs: 4 x 32 keys for the register-resident kernel, 64 for the LDS-staged one
-    const int gran = (!MAD_VERIFY_REGS && (T * G + 15) / 16 >= MAD_VERIFY_LDS_MIN_NB) ? 64 : 128;
+    const int gran = ((T * G + 15) / 16 >= kVerifyLdsMinNb) ? 64 : 128;
     chunk = (chunk + gran - 1) / gran * gran;
     if (chunk < gran) chunk = gran;
     p.chunk = chunk;
@@ -595,7 +590,7 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
-    if (!MAD_VERIFY_REGS && NB >= MAD_VERIFY_LDS_MIN_NB) {
+    if (NB >= kVerifyLdsMinNb) {
         hipLaunchKernelGGL((verify_lds_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)),
                            dim3(64 * VerifyLdsCfg<D>::NWV), VerifyLdsCfg<D>::SMEM, st, a);
         return hipGetLastError();

@@ -253,3 +253,44 @@ def test_layer_linear_validation(mad):
         vp(1 << 20), vp(1 << 21), 1e-5, vp(1 << 22), R, D, F, vp(out), None)
     assert swi(F=6) == mad.MAD_EINVAL and swi(D=8192) == mad.MAD_ENOTSUP and swi(R=0) == mad.MAD_EINVAL
     assert swi(out=(1 << 20) + 16) == mad.MAD_EINVAL
+
+
+def test_python_binding_rejects_mismatched_tensors(mad):
+    """The binding refuses, before any launch, tensors whose shapes would make a
+    kernel read or write past them: a batch dimension other than 1 or B, KV
+    heads or head_dim that differ between q, the memory, the ring and the new
+    token, non-contiguous q/out/x, adaptor weights of the wrong shape."""
+    import torch
+    bf = torch.bfloat16
+    B, Hq, Hkv, d = 2, 8, 2, 64
+    q = torch.zeros(B, Hq, d, dtype=bf)
+    mk = torch.zeros(B, Hkv, 16, d, dtype=bf)
+    rk = torch.zeros(B, Hkv, 32, d, dtype=bf)
+    kn = torch.zeros(B, Hkv, d, dtype=bf)
+    mem = mad.KV(mk, mk.clone(), [4] * B)
+    win = mad.KV(rk, rk.clone(), [3] * B, [0] * B)
+    with pytest.raises(ValueError, match="batch dimension"):
+        mad.draft_decode_attn(q, mad.KV(torch.zeros(3, Hkv, 16, d, dtype=bf), torch.zeros(3, Hkv, 16, d, dtype=bf),
+                                        [4] * B), win)
+    with pytest.raises(ValueError, match="KV heads"):
+        mad.draft_decode_attn(q, mem, mad.KV(torch.zeros(B, 1, 32, d, dtype=bf), torch.zeros(B, 1, 32, d, dtype=bf),
+                                             [3] * B, [0] * B), kn, kn.clone())
+    with pytest.raises(ValueError, match="head_dim"):
+        mad.draft_decode_attn(q, mem, mad.KV(torch.zeros(B, Hkv, 32, 128, dtype=bf),
+                                             torch.zeros(B, Hkv, 32, 128, dtype=bf), [3] * B, [0] * B))
+    with pytest.raises(ValueError, match="k_new"):
+        mad.draft_decode_attn(q, mem, win, torch.zeros(B, 1, d, dtype=bf), torch.zeros(B, 1, d, dtype=bf))
+    with pytest.raises(ValueError, match="contiguous"):
+        mad.draft_decode_attn(torch.zeros(B, d, Hq, dtype=bf).transpose(1, 2), mem, win)
+    with pytest.raises(ValueError, match="dtype"):
+        mad.draft_decode_attn(q.float(), mem, win)
+    with pytest.raises(ValueError, match="one entry per row"):
+        mad.draft_decode_attn(q, mad.KV(mk, mk.clone(), [4]), win)
+    x = torch.zeros(B, 4, Hq * d, dtype=bf)
+    with pytest.raises(ValueError, match="w_kv"):
+        mad.memory_update(x, torch.zeros(2 * Hkv * d, Hq * d - 64, dtype=bf), [[0] * 4] * B, mem)
+    with pytest.raises(ValueError, match="contiguous"):
+        mad.memory_update(torch.zeros(B, Hq * d, 4, dtype=bf).transpose(1, 2),
+                          torch.zeros(2 * Hkv * d, Hq * d, dtype=bf), [[0] * 4] * B, mem)
+    with pytest.raises(ValueError, match="pos"):
+        mad.memory_update(x, torch.zeros(2 * Hkv * d, Hq * d, dtype=bf), [[0] * 3] * B, mem)
