@@ -20,7 +20,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score_batched, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -70,7 +70,8 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
             rows.append(new)
         K = np.stack([k for k, _ in rows], axis=1)[None]   # [1, Hkv, n, d]
         V = np.stack([v for _, v in rows], axis=1)[None]
-        return oracle.attend_batched(qrows[None], K, V, np.array([K.shape[2]]), scale)
+        o, lse = oracle.attend_batched(qrows[None], K, V, np.array([K.shape[2]]), scale)
+        return o, lse, abs_score_batched(qrows[None], K, [K.shape[2]], scale)
 
     # ---- eager run, oracle at every step ----
     for i, p in schedule:
@@ -85,7 +86,7 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
         out, lse = (model.out, model.lse) if upd is None else (model.outf, model.lsef)
         for l in range(L):
             check_out(to_np(out[l][0]), refs[l][0][0], True, f"set {i} pos {p} layer {l} out")
-            check(to_np(lse[l][0]), refs[l][1][0], F32_ATOL, None, f"set {i} pos {p} layer {l} lse")
+            check_lse(to_np(lse[l][0]), refs[l][1][0], refs[l][2][0], d, f"set {i} pos {p} layer {l} lse")
         for l in range(L):
             st = h[i, l]
             st["rk"][:, lay.ring_row(p)] = kn[l]
@@ -98,9 +99,9 @@ def test_bench_draft_step_eager_oracle_and_graph_replays():
                 st["mv"][:, upd.mem_row + r] = _bf16(v_ref[r])
             for r in range(len(upd.positions)):
                 sview = lay.slot_scope_view(upd.first_slot + r)
-                o_ref, l_ref = attend(qf[l][1 + r], st, sview, None)
+                o_ref, l_ref, a_ref = attend(qf[l][1 + r], st, sview, None)
                 check_out(to_np(model.outf[l][1 + r]), o_ref[0], True, f"set {i} slot {upd.first_slot + r} layer {l}")
-                check(to_np(model.lsef[l][1 + r]), l_ref[0], F32_ATOL, None, f"set {i} slot {upd.first_slot + r} lse")
+                check_lse(to_np(model.lsef[l][1 + r]), l_ref[0], a_ref[0], d, f"set {i} slot {upd.first_slot + r} lse")
     eager = [(model.out[l].clone(), model.lse[l].clone(), model.outf[l].clone(), model.lsef[l].clone())
              for l in range(L)]
 

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score_batched, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -33,18 +33,23 @@ def _case(dtype, B, Hq, Hkv, d, mlen, wlen, wcap, wstart, new=True, seed=0, mcap
     kn = synth.normal((B, Hkv, d), s + 6, dtype=dtype)
     vn = synth.normal((B, Hkv, d), s + 7, dtype=dtype)
     G = Hq // Hkv
+    targets = {}
     if peaky:
-        # each query points at one visible key: softmax close to one-hot
+        # each query is peaky * one visible key: with peaky >= 2 the softmax is close to one-hot
+        # (the target key's weight is checked below) and o is close to that key's value row
         for b in range(B):
             for h in range(Hq):
                 c = h // G
                 if wlen[b] > 0:
-                    r = (wstart[b] + (h * 7) % wlen[b]) % wcap
-                    q[b, h] = (peaky * wk[b, c, r].float()).to(dtype)
+                    kt = wk[b, c, (wstart[b] + (h * 7) % wlen[b]) % wcap]
                 elif mlen[b] > 0:
-                    q[b, h] = (peaky * mk[b, c, (h * 5) % mlen[b]].float()).to(dtype)
+                    kt = mk[b, c, (h * 5) % mlen[b]]
+                else:
+                    continue
+                q[b, h] = (peaky * kt.float()).to(dtype)
+                targets[(b, h)] = kt.double().numpy()
     g = {n: t.to(dev) for n, t in dict(q=q, mk=mk, mv=mv, wk=wk, wv=wv, kn=kn, vn=vn).items()}
-    wk_before = g["wk"].clone()
+    wk_before, wv_before = g["wk"].clone(), g["wv"].clone()
     memkv = mad.KV(g["mk"], g["mv"], mlen) if mem else None
     win = mad.KV(g["wk"], g["wv"], wlen, wstart)
     out, lse = mad.draft_decode_attn(g["q"], memkv, win, g["kn"] if new else None, g["vn"] if new else None)
@@ -71,16 +76,22 @@ def _case(dtype, B, Hq, Hkv, d, mlen, wlen, wcap, wstart, new=True, seed=0, mcap
             V[b, :, : n[b]] = np.concatenate(rows_v, axis=1)
     o_ref, lse_ref = oracle.attend_batched(q.double().numpy(), K, V, np.array(n), d ** -0.5)
     bf = dtype == torch.bfloat16
+    q64 = q.double().numpy()
+    for (b, h), kt in targets.items():
+        w = np.exp(d ** -0.5 * float(q64[b, h] @ kt) - lse_ref[b, h])
+        assert w >= 0.9 if peaky >= 2 else w > 0, f"peaky query ({b}, {h}): target weight {w:.3f}"
     check_out(to_np(out), o_ref, bf)
-    check(to_np(lse), lse_ref, F32_ATOL, None, "lse")
+    check_lse(to_np(lse), lse_ref, abs_score_batched(q64, K, n, d ** -0.5), d)
 
-    # the new token was appended at ring row (start + len) % cap; nothing else moved
-    wk_after = g["wk"].cpu()
-    expect = wk_before.cpu().clone()
-    if new:
-        for b in range(B):
-            expect[b, :, (wstart[b] + wlen[b]) % wcap] = kn[b]
-    assert torch.equal(wk_after.view(torch.int16) if bf else wk_after, expect.view(torch.int16) if bf else expect)
+    # the new token's K and V rows were appended at ring row (start + len) % cap; no other bit moved
+    for before, new_rows, name in ((wk_before, kn, "wk"), (wv_before, vn, "wv")):
+        after = g[name].cpu()
+        expect = before.cpu().clone()
+        if new:
+            for b in range(B):
+                expect[b, :, (wstart[b] + wlen[b]) % wcap] = new_rows[b]
+        assert torch.equal(after.view(torch.int16) if bf else after.view(torch.int32),
+                           expect.view(torch.int16) if bf else expect.view(torch.int32)), f"{name} ring bits"
     return out, lse
 
 
@@ -90,7 +101,7 @@ def test_tiny_fp32_shape():
 
 
 def test_tiny_fp32_ring_wrap_and_peaky():
-    _case(torch.float32, 1, 4, 1, 64, 64, 127, 144, 140, seed=2, peaky=0.5)
+    _case(torch.float32, 1, 4, 1, 64, 64, 127, 144, 140, seed=2, peaky=2.0)
 
 
 def test_draft_8k_layer_bf16():
@@ -113,8 +124,17 @@ def test_paper_shaped_memory_32k_bf16(r, mlen):
     _case(torch.bfloat16, 1, 32, 8, 64, mlen, 127, 256, 200, seed=13 + r)
 
 
-def test_peaky_queries_bf16():
-    _case(torch.bfloat16, 1, 32, 8, 64, 2048, 1023, 1056, 50, seed=6, peaky=0.6)
+@pytest.mark.parametrize("c", [3.0, 4.0])
+def test_peaky_queries_bf16(c):
+    # the 32K compact layer (2048 slots + 1023 window + new token) with q = c k_j: the target key holds
+    # at least 0.9 of the softmax weight (asserted; at c = 2 a short key among 3072 can hold only ~0.8),
+    # lse ~ 8 c
+    _case(torch.bfloat16, 1, 32, 8, 64, 2048, 1023, 1056, 50, seed=6, peaky=c)
+
+
+def test_peaky_queries_on_memory_rows_bf16():
+    # no window: every query points at a memory row
+    _case(torch.bfloat16, 2, 32, 8, 64, 2048, 0, 16, 0, seed=14, peaky=3.0, new=False)
 
 
 def test_ragged_batch_bf16():
@@ -182,4 +202,4 @@ def _case_ws(ws, B, Hq, Hkv, d, seed):
     o_ref, lse_ref = oracle.attend_batched(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                            np.full(B, n), d ** -0.5)
     check_out(to_np(out), o_ref, True, f"out B{B} Hq{Hq} Hkv{Hkv} d{d}")
-    check(to_np(lse), lse_ref, F32_ATOL, None, "lse")
+    check_lse(to_np(lse), lse_ref, abs_score_batched(q.double().numpy(), k.double().numpy(), [n] * B, d ** -0.5), d)

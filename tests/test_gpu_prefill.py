@@ -5,25 +5,43 @@ Each query of the prefill pass attends the set it would attend while decoding
 write scope).  The oracle builds every key list from the visible-set
 simulator; the inputs are seeded bf16 tensors that both sides read.  Rows of
 the outputs past each sequence's prefix (or slot count) must stay untouched.
-Tolerances: bf16 outputs max-abs 2e-2 and relative L2 1e-2, lse 1e-5.
+Slot counts come from the oracle's set simulator.  Tolerances: bf16 outputs
+max-abs 2e-2 and relative L2 1e-2; lse per row within the bound derived from
+the fp32 arithmetic (parity.lse_tol).
 """
 import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
 
-def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_idx=None, ramp=0.0):
+def _row_scores(qrow, view, mem_k, raw_k, S, scale):
+    """A (per query head) over the keys of one prefill row: its sinks and slots
+    (memory rows) and its raw window."""
+    Hq, d = qrow.shape
+    Hkv = mem_k.shape[0]
+    G = Hq // Hkv
+    mrows = list(view.sink) + [S + m - 1 for m in view.slots]
+    A = np.zeros(Hq)
+    for c in range(Hkv):
+        K = np.concatenate([mem_k[c][mrows].reshape(-1, d), raw_k[c][list(view.window)].reshape(-1, d)])
+        A[c * G:(c + 1) * G] = abs_score(qrow[c * G:(c + 1) * G], K, scale)
+    return A
+
+
+def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_idx=None, ramp=0.0, peaky=0.0):
     import oracle
     import paper_2608_30252_amd as mad
+    from oracle.masw_sets import MaswSets
     from paper_2608_30252_amd import synth
 
     dev = torch.device("cuda")
     B = len(P_list)
-    M_list = [mad.slots_after(P, S, r, u) for P in P_list]
+    sets = MaswSets(S, W, r, u)
+    M_list = [sets.slots_after(P) for P in P_list]
     q_cap = max(P_list) + 5
     slot_cap = max(max(M_list), 1) + 2
     mem_cap = S + slot_cap + 3
@@ -40,6 +58,23 @@ def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_id
         mem_k = (mem_k.float() * (1 + ramp * torch.arange(mem_cap).float() / mem_cap)[None, None, :, None]).to(mem_k.dtype)
     s = min(S, q_cap)
     mem_k[:, :, :s], mem_v[:, :, :s] = raw_k[:, :, :s], raw_v[:, :, :s]   # the sinks are raw tokens 0..S-1
+    G = Hq // Hkv
+    targets = []
+    if peaky:
+        # sampled raw queries point at a raw key of their window, sampled slot queries at their own
+        # slot row (a slot's write scope holds itself): q = peaky * that key
+        for b, (P, M) in enumerate(zip(P_list, M_list)):
+            for p in (raw_idx or []):
+                if S <= p < P:
+                    for h in range(Hq):
+                        j = p - (h * 13) % min(W, p - S + 1)
+                        q_raw[b, p, h] = (peaky * raw_k[b, h // G, j].float()).to(q_raw.dtype)
+                        targets.append(("raw", b, p, h, raw_k[b, h // G, j].double().numpy()))
+            for m in (slot_idx or []):
+                if 1 <= m <= M:
+                    for h in range(Hq):
+                        q_slot[b, m - 1, h] = (peaky * mem_k[b, h // G, S + m - 1].float()).to(q_slot.dtype)
+                        targets.append(("slot", b, m, h, mem_k[b, h // G, S + m - 1].double().numpy()))
 
     g = [t.to(dev) for t in (q_raw, q_slot, raw_k, raw_v, mem_k, mem_v)]
     out_raw = torch.full((B, q_cap, Hq, d), float("nan"), dtype=torch.bfloat16, device=dev)
@@ -59,15 +94,24 @@ def _run(Hq, Hkv, d, S, W, r, u, P_list, seed, slots=True, raw_idx=None, slot_id
         ref_raw, ref_slot = oracle.memory_prefill(
             to_np(q_raw[b]), to_np(q_slot[b]) if slots else None, to_np(mem_k[b]), to_np(mem_v[b]),
             to_np(raw_k[b]), to_np(raw_v[b]), P, S, W, r, u, scale, raw_idx=ridx, slot_idx=sidx)
+        mk_b, rk_b = to_np(mem_k[b]), to_np(raw_k[b])
+        for kind, bb, i, h, kt in targets:
+            if bb == b:
+                qv, lref = (q_raw[b, i, h], ref_raw[i][1][h]) if kind == "raw" else (q_slot[b, i - 1, h], ref_slot[i][1][h])
+                w = np.exp(scale * float(qv.double().numpy() @ kt) - lref)
+                assert w >= 0.9, f"seq {b} {kind} {i} head {h}: target weight {w:.3f}"
         if ridx:
             check_out(o_raw[b, ridx], np.stack([ref_raw[p][0] for p in ridx]), True, f"seq {b} raw out")
-            check(l_raw[b, ridx], np.stack([ref_raw[p][1] for p in ridx]), F32_ATOL, None, f"seq {b} raw lse")
+            A = np.stack([_row_scores(to_np(q_raw[b, p]), sets.raw_view(p), mk_b, rk_b, S, scale) for p in ridx])
+            check_lse(l_raw[b, ridx], np.stack([ref_raw[p][1] for p in ridx]), A, d, f"seq {b} raw lse")
         assert np.isnan(o_raw[b, P:]).all() and np.isnan(l_raw[b, P:]).all(), f"seq {b}: rows past the prefix written"
         if slots:
             if sidx:
                 rows = [m - 1 for m in sidx]
                 check_out(o_slot[b, rows], np.stack([ref_slot[m][0] for m in sidx]), True, f"seq {b} slot out")
-                check(l_slot[b, rows], np.stack([ref_slot[m][1] for m in sidx]), F32_ATOL, None, f"seq {b} slot lse")
+                A = np.stack([_row_scores(to_np(q_slot[b, m - 1]), sets.slot_scope(m), mk_b, rk_b, S, scale)
+                              for m in sidx])
+                check_lse(l_slot[b, rows], np.stack([ref_slot[m][1] for m in sidx]), A, d, f"seq {b} slot lse")
             assert np.isnan(o_slot[b, M:]).all(), f"seq {b}: slot rows past the slot count written"
         else:
             assert np.isnan(o_slot).all()
@@ -100,19 +144,31 @@ def test_window_shorter_than_the_slot_interval():
     _run(32, 8, 64, S=0, W=8, r=16, u=1, P_list=[513], seed=10)
 
 
-def test_32k_prefix_full_size_sampled():
-    # the 32K draft layer: 2048 slots (four per update), 1024-token window;
-    # the GPU computes every query, the oracle a sample spanning block edges
+def _sample_32k():
     rng = np.random.default_rng(0)
     raw_idx = sorted(set([0, 1, 15, 16, 63, 64, 1023, 1024, 1025, 16383, 16384, 32703, 32704, 32767] +
                          rng.integers(0, 32768, 12).tolist()))
     slot_idx = sorted(set([1, 2, 4, 5, 64, 65, 1024, 2047, 2048] + rng.integers(1, 2049, 6).tolist()))
+    return raw_idx, slot_idx
+
+
+def test_32k_prefix_full_size_sampled():
+    # the 32K draft layer: 2048 slots (four per update), 1024-token window;
+    # the GPU computes every query, the oracle a sample spanning block edges
+    raw_idx, slot_idx = _sample_32k()
     _run(32, 8, 64, S=0, W=1024, r=16, u=4, P_list=[32768], seed=11, raw_idx=raw_idx, slot_idx=slot_idx)
 
 
-@pytest.mark.parametrize("d", [64, 128])
-def test_growing_scores_rebase_the_running_maximum(d):
-    # keys scaled by 1 .. 5 along the prefix: the late tiles' scores exceed the early ones' by more than
-    # 2^8, so the lazily rebased maximum moves within a pass (larger scores would put the lse below the
-    # 1e-5 bar's reach: fp32 spacing at |lse| ~ 50 is 4e-6)
-    _run(8, 2, d, S=4, W=300, r=8, u=2, P_list=[2500, 1700], seed=23, ramp=4.0)
+def test_32k_prefix_peaky_queries_sampled():
+    # the same layer with the sampled queries set to 3 x a key they attend: the target key holds
+    # at least 0.9 of the softmax weight (asserted), lse ~ 24
+    raw_idx, slot_idx = _sample_32k()
+    _run(32, 8, 64, S=0, W=1024, r=16, u=4, P_list=[32768], seed=12, raw_idx=raw_idx, slot_idx=slot_idx,
+         peaky=3.0)
+
+
+@pytest.mark.parametrize("d,ramp", [(64, 4.0), (128, 4.0), (64, 11.0), (128, 11.0)])
+def test_growing_scores_rebase_the_running_maximum(d, ramp):
+    # keys scaled by 1 .. 1 + ramp along the prefix: the late tiles' scores exceed the early ones' by
+    # more than 2^8, so the lazily rebased maximum moves within a pass; at ramp 11 scores reach ~50
+    _run(8, 2, d, S=4, W=300, r=8, u=2, P_list=[2500, 1700], seed=23, ramp=ramp)

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score_batched, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -70,7 +70,8 @@ def _run_sequence(dtype, Hq, Hkv, d, S, W, r, prefix, steps, seed):
         vs = [o_sink[i][1] for i in sink_ids] + [o_slot[m][1] for m in slot_ids] + [o_raw[x][1] for x in raw_ids]
         K = np.stack(ks, axis=1)[None]   # [1, Hkv, n, d]
         V = np.stack(vs, axis=1)[None]
-        return oracle.attend_batched(q.double().numpy(), K, V, np.array([K.shape[2]]), scale)
+        o, lse = oracle.attend_batched(q.double().numpy(), K, V, np.array([K.shape[2]]), scale)
+        return o, lse, abs_score_batched(q.double().numpy(), K, [K.shape[2]], scale)
 
     n_updates = 0
     for p in range(prefix, prefix + steps):
@@ -82,9 +83,9 @@ def _run_sequence(dtype, Hq, Hkv, d, S, W, r, prefix, steps, seed):
                                          mad.KV(g_rk, g_rv, [view.win_len], [view.win_start]),
                                          k_new[None].to(dev), v_new[None].to(dev), scale=scale)
         sv = sets.raw_view(p)
-        o_ref, lse_ref = oracle_attend(q, sv.sink, sv.slots, sv.window)
+        o_ref, lse_ref, a_ref = oracle_attend(q, sv.sink, sv.slots, sv.window)
         check_out(to_np(out), o_ref, bf, f"step {p} out")
-        check(to_np(lse), lse_ref, F32_ATOL, None, f"step {p} lse")
+        check_lse(to_np(lse), lse_ref, a_ref, d, f"step {p} lse")
 
         upd = lay.update_in_pass_of(p)
         if upd is None:
@@ -111,9 +112,9 @@ def _run_sequence(dtype, Hq, Hkv, d, S, W, r, prefix, steps, seed):
             out, lse = mad.draft_decode_attn(qg.to(dev), mad.KV(g_mk, g_mv, [sview.mem_len]),
                                              mad.KV(g_rk, g_rv, [sview.win_len], [sview.win_start]), scale=scale)
             sc = sets.slot_scope(m)
-            o_ref, lse_ref = oracle_attend(qg, sc.sink, sc.slots, sc.window)
+            o_ref, lse_ref, a_ref = oracle_attend(qg, sc.sink, sc.slots, sc.window)
             check_out(to_np(out), o_ref, bf, f"slot {m} scope out")
-            check(to_np(lse), lse_ref, F32_ATOL, None, f"slot {m} scope lse")
+            check_lse(to_np(lse), lse_ref, a_ref, d, f"slot {m} scope lse")
     torch.cuda.synchronize()
     return n_updates
 
@@ -212,9 +213,10 @@ def test_batched_sixteen_ragged_sequences_staggered_updates():
                 K[j, :, ns:ns + len(win)], V[j, :, ns:ns + len(win)] = o_raw_k[b][:, win], o_raw_v[b][:, win]
                 n[j] = ns + len(win)
             o_ref, lse_ref = oracle.attend_batched(q[rows].double().numpy(), K, V, n, scale)
+            a_ref = abs_score_batched(q[rows].double().numpy(), K, n, scale)
             for j, b in enumerate(rows):
                 check_out(to_np(out[b:b + 1]), o_ref[j:j + 1], True, f"token {t} seq {b} out")
-                check(to_np(lse[b:b + 1]), lse_ref[j:j + 1], F32_ATOL, None, f"token {t} seq {b} lse")
+                check_lse(to_np(lse[b:b + 1]), lse_ref[j:j + 1], a_ref[j:j + 1], d, f"token {t} seq {b} lse")
             checked_after += len(after_update)
 
         # one update launch for the batch: the sequences whose 64-token block ends at this token

@@ -15,7 +15,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score_batched, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -94,13 +94,14 @@ def _fused_boundary(dtype, Hq, Hkv, d, S, W, r, u, prefix, seed):
         ids = [("sink", i) for i in sv.sink] + [("slot", m) for m in sv.slots] + [("raw", x) for x in sv.window]
         K = np.stack([keys[k][0] for k in ids], axis=1)[None]
         V = np.stack([keys[k][1] for k in ids], axis=1)[None]
-        return oracle.attend_batched(qrows.double().numpy()[None], K, V, np.array([K.shape[2]]), scale)
+        o, lse = oracle.attend_batched(qrows.double().numpy()[None], K, V, np.array([K.shape[2]]), scale)
+        return o, lse, abs_score_batched(qrows.double().numpy()[None], K, [K.shape[2]], scale)
 
     scopes = [sets.raw_view(p)] + [sets.slot_scope(upd.first_slot + i) for i in range(n_new)]
     for row, sv in enumerate(scopes):
-        o_ref, l_ref = oracle_attend(q[row], sv)
+        o_ref, l_ref, a_ref = oracle_attend(q[row], sv)
         check_out(to_np(out[row]), o_ref[0], bf, f"row {row} out")
-        check(to_np(lse[row]), l_ref[0], F32_ATOL, None, f"row {row} lse")
+        check_lse(to_np(lse[row]), l_ref[0], a_ref[0], d, f"row {row} lse")
     # the ring gained exactly the current token, once
     changed = (g_rk != ring_before).any(dim=-1).any(dim=1)[0].nonzero().flatten().tolist()
     assert changed == [lay.ring_row(p)], changed

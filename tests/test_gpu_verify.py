@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import check, check_out, to_np, F32_ATOL
+from parity import abs_score_verify, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -32,15 +32,36 @@ def _run(q, k, v, length):
     return out.cpu(), lse.cpu()
 
 
-def _check(q, k, v, length, out, lse, bs=None):
+def _check(q, k, v, length, out, lse, targets=None):
+    """Every sequence against the oracle; with targets (b, t, h) -> key row, also the
+    target key's softmax weight (>= 0.9 for a peaky query)."""
     import oracle
     B, T, Hq, d = q.shape
-    bs = range(B) if bs is None else bs
-    for b in bs:
-        o_ref, lse_ref = oracle.verify(q[b:b + 1].double().numpy(), k[b:b + 1].double().numpy(),
-                                       v[b:b + 1].double().numpy(), np.array([length[b]]), d ** -0.5)
+    for b in range(B):
+        qb, kb = q[b:b + 1].double().numpy(), k[b:b + 1].double().numpy()
+        o_ref, lse_ref = oracle.verify(qb, kb, v[b:b + 1].double().numpy(), np.array([length[b]]), d ** -0.5)
+        if targets:
+            for (bb, t, h), j in targets.items():
+                if bb == b:
+                    w = np.exp(d ** -0.5 * float(qb[0, t, h] @ kb[0, h // (Hq // k.shape[1]), j]) - lse_ref[0, t, h])
+                    assert w >= 0.9, f"peaky query ({b}, {t}, {h}): target weight {w:.3f}"
         check_out(to_np(out[b:b + 1]), o_ref, True, f"out b{b}")
-        check(to_np(lse[b:b + 1]), lse_ref, F32_ATOL, None, f"lse b{b}")
+        check_lse(to_np(lse[b:b + 1]), lse_ref, abs_score_verify(qb, kb, [length[b]], d ** -0.5), d, f"lse b{b}")
+
+
+def _make_peaky(q, k, length, c):
+    """q[b, t, h] = c * a key row that query t sees (rows 0 .. len-T+t of KV head h // G)."""
+    B, T, Hq, d = q.shape
+    G = Hq // k.shape[1]
+    targets = {}
+    for b in range(B):
+        for t in range(T):
+            n = length[b] - T + t + 1
+            for h in range(Hq):
+                j = (h * 131 + t * 17 + b * 7) % n
+                q[b, t, h] = (c * k[b, h // G, j].float()).to(q.dtype)
+                targets[(b, t, h)] = j
+    return targets
 
 
 @pytest.mark.parametrize("Hq,Hkv,d,T", [(32, 8, 128, 5), (64, 8, 128, 5), (32, 8, 64, 6), (16, 1, 128, 4),
@@ -97,12 +118,23 @@ def test_70b_shaped_layer_full_size():
     _check(q, k, v, length, out, lse)
 
 
-def test_8b_shaped_layer_full_size_sampled():
-    # 32 query / 8 KV heads, d 128, batch 4, 32768-token prefix + 5 new tokens;
-    # the oracle checks two of the four sequences
+def test_8b_shaped_layer_full_size():
+    # 32 query / 8 KV heads, d 128, batch 4, 32768-token prefix + 5 new tokens; every sequence checked
     B, T, Hq, Hkv, d = 4, 5, 32, 8, 128
     length = [32768 + T] * B
     cap = 32776
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=44)
     out, lse = _run(q, k, v, length)
-    _check(q, k, v, length, out, lse, bs=[1, 3])
+    _check(q, k, v, length, out, lse)
+
+
+@pytest.mark.parametrize("B,Hq,c", [(4, 32, 2.0), (1, 64, 2.0), (1, 64, 3.0)])
+def test_peaky_queries_full_size(B, Hq, c):
+    # both target shapes at the 32K prefix with q = c k_j (j visible to the query): the target key holds
+    # at least 0.9 of the softmax weight (asserted), o is close to its value row, lse ~ 11 c
+    T, Hkv, d = 5, 8, 128
+    length = [32768 + T] * B
+    q, k, v = _inputs(B, T, Hq, Hkv, d, 32776, seed=45 + Hq)
+    targets = _make_peaky(q, k, length, c)
+    out, lse = _run(q, k, v, length)
+    _check(q, k, v, length, out, lse, targets)
