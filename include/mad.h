@@ -119,6 +119,33 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
                           void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * The draft decode attention of mad_draft_decode_attn without a workspace and
+ * without any allocation, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Arguments, results, layouts and errors are those of
+ * mad_draft_decode_attn (the same kernels run); the split partials and
+ * arrival counters live in a library-owned device array of
+ * MAD_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends.
+ *   - The first call on a device looks up the array's address and clears its
+ *     counter region with a small kernel on `stream`; every call leaves the
+ *     counters at zero again.
+ *   - Calls whose workspace need, mad_workspace_bytes(MAD_OP_DECODE, B, Hq,
+ *     Hkv, d, ...), exceeds MAD_NOALLOC_SCRATCH_BYTES return MAD_EINVAL before
+ *     anything is launched (16 MiB holds B * Hkv up to 240 units at d 64 and
+ *     G 4; the 16-sequence, 8-KV-head launch needs 9 MiB).
+ *   - Every call on one GPU shares its array: calls ordered on one stream are
+ *     safe; calls that overlap in time on one GPU (other streams, threads)
+ *     race and must not be issued.
+ *   - Errors: as mad_draft_decode_attn, plus MAD_EHIP if the array's address
+ *     cannot be obtained on the current device.
+ */
+#define MAD_NOALLOC_SCRATCH_BYTES (16u << 20)
+int mad_draft_decode_attn_noalloc(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                                  const mad_kv_view *mem, const mad_kv_view *win,
+                                  const void *k_new, const void *v_new,
+                                  void *out, float *lse, void *stream);
+
+/*
  * The same attention with a per-row choice for the new token, so that one
  * launch serves the raw query of a step and the write-scope queries of the
  * memory slots materialised in that step (Sec. 3.2: a slot is an extra

@@ -58,6 +58,7 @@ def _load_library():
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_accept_stochastic.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_draft_step_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, _u8p, vp, vp, vp, sz, vp]
+    lib.mad_draft_decode_attn_noalloc.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, vp, vp, vp]
     lib.mad_memory_prefill_attn.argtypes = [vp, vp, i, i, i, i, i, f, _i32p, i, i, i, i, i, i, kvp, kvp,
                                             vp, vp, vp, vp, vp]
     lib.mad_rmsnorm_qkv_rope.argtypes = [vp, vp, f, vp, _i32p, i, i, i, i, i, d, i, vp, vp, vp, vp, vp]
@@ -68,7 +69,8 @@ def _load_library():
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
-               "mad_accept_stochastic", "mad_draft_step_attn", "mad_memory_prefill_attn",
+               "mad_accept_stochastic", "mad_draft_step_attn", "mad_draft_decode_attn_noalloc",
+               "mad_memory_prefill_attn",
                "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
@@ -250,6 +252,23 @@ def draft_decode_attn(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
                                    ctypes.byref(wv) if wv is not None else None,
                                    _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(lse),
                                    _ptr(w), w.numel(), _stream(q.device))
+    _check(rc)
+    return out, lse
+
+
+def draft_decode_attn_noalloc(q: torch.Tensor, mem: Optional[KV], win: Optional[KV],
+                              k_new: Optional[torch.Tensor] = None, v_new: Optional[torch.Tensor] = None,
+                              out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                              scale: Optional[float] = None):
+    """draft_decode_attn without a workspace: the library's own per-GPU scratch
+    holds the split partials (no allocation by the library; out and lse are
+    allocated here only when not given).  Calls on one GPU must not overlap."""
+    B, Hq, Hkv, d, out, lse, scale, mv, wv = _decode_args(q, mem, win, k_new, v_new, out, lse, scale)
+    rc = _load_library().mad_draft_decode_attn_noalloc(_ptr(q), B, Hq, Hkv, d, _dtype_code(q), float(scale),
+                                                       ctypes.byref(mv) if mv is not None else None,
+                                                       ctypes.byref(wv) if wv is not None else None,
+                                                       _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(lse),
+                                                       _stream(q.device))
     _check(rc)
     return out, lse
 

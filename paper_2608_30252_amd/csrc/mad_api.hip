@@ -6,6 +6,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "mad_internal.h"
 
 namespace {
@@ -195,6 +197,75 @@ int mad_draft_decode_attn(const void *q, int B, int Hq, int Hkv, int d, int dtyp
     for (int b = 0; b < B; ++b) mode[b] = k_new ? 2 : 0;
     return decode_impl(q, B, Hq, Hkv, d, dtype, scale, mem, win, k_new, v_new, mode, out, lse, ws, ws_bytes,
                        stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// ---- the no-allocation decode entry point's scratch -----------------------
+// One library-owned device array per GPU (every device that runs the library
+// holds its own copy until the process ends): the counter region followed by
+// split partials, the same layout as a caller workspace.  In host code the
+// array's name only names the symbol; its device address on the current GPU
+// comes from hipGetSymbolAddress, looked up once per device and kept.
+constexpr size_t kNoallocScratchBytes = (size_t)MAD_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+__global__ void zero_words(unsigned *p, unsigned n) {
+    for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+// The current device's scratch address; on the first call on a device, look it
+// up and clear the counter region with a kernel on `stream` (the kernels leave
+// it at zero after every call, so this happens once).
+int scratch_of_current_device(hipStream_t stream, void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(MAD_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return fail(MAD_EHIP, "device ordinal %d outside [0, %d)", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(MAD_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        hipLaunchKernelGGL(zero_words, dim3(256), dim3(256), 0, stream, (unsigned *)p,
+                           (unsigned)(mad::kCounterRegionBytes / 4));
+        e = hipGetLastError();
+        if (e != hipSuccess) return fail(MAD_EHIP, "scratch clear launch: %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MAD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mad_draft_decode_attn_noalloc(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
+                                  const mad_kv_view *mem, const mad_kv_view *win, const void *k_new,
+                                  const void *v_new, void *out, float *lse, void *stream) {
+    if (B < 1 || B > MAD_MAX_BATCH) return fail(MAD_EINVAL, "B=%d outside [1, %d]", B, MAD_MAX_BATCH);
+    int rc = check_heads(B, Hq, Hkv, d, dtype);
+    if (rc) return rc;
+    const size_t need = mad::decode_ws_bytes(B, Hq, Hkv, d);
+    if (need > kNoallocScratchBytes)
+        return fail(MAD_EINVAL, "B=%d, Hkv=%d, d=%d need %zu bytes of scratch, above the %zu-byte limit of the "
+                    "no-allocation entry point (use mad_draft_decode_attn with a workspace)", B, Hkv, d, need,
+                    kNoallocScratchBytes);
+    if (k_new && !win) return fail(MAD_EINVAL, "k_new needs a window ring to append to");
+    void *ws = nullptr;
+    if ((rc = scratch_of_current_device((hipStream_t)stream, &ws))) return rc;
+    unsigned char mode[MAD_MAX_BATCH];
+    for (int b = 0; b < B; ++b) mode[b] = k_new ? 2 : 0;
+    return decode_impl(q, B, Hq, Hkv, d, dtype, scale, mem, win, k_new, v_new, mode, out, lse, ws,
+                       kNoallocScratchBytes, stream);
 }
 
 int mad_draft_step_attn(const void *q, int B, int Hq, int Hkv, int d, int dtype, float scale,
