@@ -33,9 +33,20 @@ Reported in the same run (sub-objects of the JSON line):
   memory_prefill the draft's masked prefill attention over a 32K prefix (32768
                  raw tokens + 2048 slots, 32/8 heads, d 64 and d 128), TFLOP/s
                  against the bf16 matrix-core peak
+  draft_8k       the 8K-prefix draft: 512 slots + 512-token window, 64 steps
+                 per sequence with its memory update, beside the full 8K KV
+  batched_drafting  16 ragged sequences drafting 4 tokens per iteration for
+                 128 iterations with staggered memory updates (one graph)
+  probes         the device's own figures: streaming read bandwidth (the
+                 measured peak the fractions are also reported against), the
+                 empty-launch floor, hand-off primitive latencies
   roofline       the dominant kernel (draft decode attention): algorithmic
-                 bytes per launch / mean launch duration from HIP events
-  cpu_baseline   the fp64 oracle on the host cores (a bounded sample)
+                 bytes per launch / mean launch duration from HIP events, its
+                 fraction of 8 TB/s and of the streaming probe, and the
+                 per-launch p10 / median / p90
+  cpu_baseline   the fp64 oracle on the host cores (a bounded sample), with
+                 the full-KV layer, both verify layers and a memory update
+                 on all threads and on one
 Inputs are synthetic N(0, 1) activations and N(0, 0.02^2) adaptor weights.
 """
 import argparse
@@ -65,7 +76,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--sets", type=int, default=6, help="sequences decoded round-robin (cold HBM reads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0)
     ap.add_argument("--summarize-trace", metavar="CSV",
                     help="print per-(kernel, grid) durations of a rocprofv3 kernel_trace.csv and exit")
     ap.add_argument("--pmc-workload", choices=("decode", "copy", "update", "verify", "prefill"),
@@ -369,6 +380,10 @@ def main():
     n_sets = max(args.sets, 1)
     log(f"device {torch.cuda.get_device_name(0)}; {mad.version()}")
 
+    # -------------------------------------------------------------- probes ----
+    probes, stream_peak = device_probes(torch, mad)
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------------------ headline ----
     model = DraftModel(torch, mad, n_sets)
     # positions: every sequence starts at the 32K prefix; sequence 0 starts a few
@@ -416,10 +431,14 @@ def main():
     achieved = bytes_launch / t_launch
     log(f"decode launch: {t_launch * 1e6:.2f} us mean over {len(launches)}, {bytes_launch:,.0f} B -> "
         f"{achieved / 1e12:.2f} TB/s")
+    dist = launch_distribution(torch, mad, [f for f, _ in launches])
+    log(f"decode launch distribution: {dist}")
     roofline = {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM, 4), "traffic": traffic_from_profile(DECODE_SOURCES),
                 "kernel": "mad::decode_kernel<bf16_t, 64, 4, 1>", "bytes_per_launch": int(bytes_launch),
-                "mean_launch_us": round(t_launch * 1e6, 3)}
+                "mean_launch_us": round(t_launch * 1e6, 3),
+                "frac_of_stream_probe": round(achieved / stream_peak, 4),
+                "stream_probe_gbps": round(stream_peak / 1e9, 1), "launch_distribution": dist}
     del model
     torch.cuda.empty_cache()
 
@@ -509,6 +528,10 @@ def main():
     log(f"batched decode B16: {t * 1e6:.2f} us/launch, {nb / t / 1e12:.2f} TB/s")
     del mkb, rkb, fns, g
     torch.cuda.empty_cache()
+
+    # ------------------------------------------- 8K-prefix draft, and C4 loop ----
+    c2 = c2_leg(torch, mad)
+    c4 = c4_loop(torch, mad)
 
     # ------------------------------------------------------- memory update ----
     upd_res = {}
@@ -648,6 +671,9 @@ def main():
         "cache_resident": cache_resident,
         "speedup_vs_full_kv": round(full_us_layer / us_per_layer, 3),
         "batched_decode": batched,
+        "draft_8k": c2,
+        "batched_drafting": c4,
+        "probes": probes,
         "prefix_sweep": sweep,
         "memory_update": upd_res,
         "verify": ver_res,
@@ -794,6 +820,183 @@ def prefix_sweep(torch, mad):
             "points": pts, "full_fit": full_fit, "compact_fit": compact_fit, "paper_shaped_32k": paper}
 
 
+def device_probes(torch, mad):
+    """What the device itself delivers, measured in the same run: the read
+    bandwidth of a plain streaming kernel over 256 MiB buffers rotated through
+    1 GiB (cold: four times the Infinity Cache), the cost of an empty launch in a
+    replayed graph, and the latency of the hand-off primitives (one thread)."""
+    import numpy as np
+    size, nbuf = 256 << 20, 4
+    bufs = [torch.empty(size, dtype=torch.uint8, device="cuda") for _ in range(nbuf)]
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = {}
+    for nwg in (1024, 2048):
+        g = graph_of(torch, lambda: [mad.probe_stream_read(bufs[j % nbuf], sink, nwg) for j in range(8)])
+        g.replay()
+        t = time_graph(torch, g, reps=3) / 8
+        stream[nwg] = size / t
+        log(f"stream probe ({nwg} workgroups): {size / t / 1e12:.3f} TB/s")
+    del bufs
+    g = graph_of(torch, lambda: [mad.probe_empty(256, 256) for _ in range(64)])
+    g.replay()
+    t_empty = time_graph(torch, g, reps=3) / 64
+    reps = 64
+    hb = torch.zeros(reps * 256 + 4096, dtype=torch.uint8, device="cuda")
+    cyc = torch.zeros(8, reps, dtype=torch.int64, device="cuda")
+    mad.probe_handoff_latency(hb, cyc, reps)
+    torch.cuda.synchronize()
+    c = cyc.cpu().numpy().astype(np.float64)
+    ghz = (c[7, -1] - c[7, 1]) / ((c[6, -1] - c[6, 1]) * 10.0)
+    names = ["plain_store_ack", "device_store_ack", "device_atomic", "device_load_written", "load_l2_hit",
+             "load_miss"]
+    lat = {n: round(float(np.median(c[k, 8:]) / ghz), 1) for k, n in enumerate(names)}
+    log(f"empty launch {t_empty * 1e6:.2f} us; hand-off latencies (ns) {lat}")
+    peak = max(stream.values())
+    return {"stream_read_tbps": round(peak / 1e12, 3),
+            "stream_read_by_workgroups": {str(k): round(v / 1e12, 3) for k, v in stream.items()},
+            "stream_workload": "nontemporal 16-byte loads, 8 in flight per thread, 256 threads per workgroup, "
+                               "256 MiB per launch over four buffers (1 GiB)",
+            "empty_launch_us": round(t_empty * 1e6, 3), "handoff_latency_ns": lat,
+            "shader_clock_ghz": round(float(ghz), 3)}, peak
+
+
+def launch_distribution(torch, mad, fns, n=256):
+    """Per-launch device time from a pair of HIP events around each launch:
+    p10 / median / p90 in us.  A streaming read of ~1 GiB per launch keeps the
+    device busy while the host enqueues every (event, launch, event) triple, so
+    the launches run back to back and each interval is the kernel plus the
+    two event packets, not the host's submission time."""
+    import numpy as np
+    busy = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(8):
+        fns[i % len(fns)]()
+    torch.cuda.synchronize()
+    for _ in range(60):                    # ~12 ms of device work ahead of the timed launches
+        mad.probe_stream_read(busy, None, 1024)
+    for i in range(n):
+        evs[i][0].record()
+        fns[i % len(fns)]()
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    del busy
+    t = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    return {"p10_us": round(float(np.percentile(t, 10)), 3), "median_us": round(float(np.median(t)), 3),
+            "p90_us": round(float(np.percentile(t, 90)), 3), "launches": n,
+            "method": "HIP events around each launch, enqueued behind ~12 ms of device work (kernel + event packets)"}
+
+
+def c2_leg(torch, mad, K=64):
+    """The 8K-prefix draft: 16 layers, 512 slots + a 512-token window, every
+    sequence decoding 64 steps (its memory update fires at the 64th, when its
+    64-token block ends); ten sequences round-robin keep the reads in HBM
+    (16 layers x 2 MB x 10 > 256 MB).  Beside it the same steps over the full
+    8192-token KV."""
+    n_sets = 10
+    model = DraftModel(torch, mad, n_sets, prefix=8192, W=512)
+    sched = [(i, model.prefix + s) for s in range(K) for i in range(n_sets)]
+    g = graph_of(torch, lambda: [model.step(i, p) for i, p in sched])
+    calls = list(model.decode_calls)
+    n_upd = model.n_updates
+    g.replay()
+    t = time_graph(torch, g)
+    steps = len(sched)
+    us_layer = t * 1e6 / (steps * model.layers)
+    nbytes = sum(kv_bytes(k, model.Hkv, model.d) for k in calls)
+    del model, g
+    torch.cuda.empty_cache()
+    full = DraftModel(torch, mad, 2, prefix=8192, full_kv=True)
+    fs = [(i, full.prefix + s) for s in range(16) for i in range(2)]
+    gf = graph_of(torch, lambda: [full.step(i, p) for i, p in fs])
+    fcalls = list(full.decode_calls)
+    gf.replay()
+    tf = time_graph(torch, gf)
+    f_us = tf * 1e6 / (len(fs) * full.layers)
+    fbytes = sum(kv_bytes(k, full.Hkv, full.d) for k in fcalls)
+    del full, gf
+    torch.cuda.empty_cache()
+    log(f"8K draft: {us_layer:.2f} us/layer ({nbytes / t / 1e12:.2f} TB/s), {n_upd} updates; full KV "
+        f"{f_us:.2f} us/layer")
+    return {"workload": "draft decode at an 8K prefix: B1, 16 layers, 32/8 heads, d64, bf16, 512 slots + 512-token "
+                        "window (1024 keys), 64 steps per sequence with the memory update at the 64th, 10 sequences "
+                        "round-robin",
+            "us_per_layer": round(us_layer, 3), "ms_per_step": round(t * 1e3 / steps, 4),
+            "tbps": round(nbytes / t / 1e12, 3), "bytes_per_layer": kv_bytes(1024, 8, 64), "steps": steps,
+            "updates": n_upd, "full_kv_us_per_layer": round(f_us, 3),
+            "full_kv_tbps": round(fbytes / tf / 1e12, 3), "speedup_vs_full_kv": round(f_us / us_layer, 3)}
+
+
+def c4_loop(torch, mad, layers=16, gamma=4, iters=128, seed=44):
+    """Batched drafting with continuous memory updates: 16 sequences with
+    prefixes drawn uniformly in [8192, 32768), 1024 memory slots and a 512-token
+    window each, 32/8 heads, d 64, bf16, `layers` layers; gamma = 4 tokens per
+    iteration for 128 iterations (512 tokens).  Per token and layer one decode
+    launch for the 16 sequences; a sequence's update fires when its own 64-token
+    block ends (slot interval 16, 4 slots per update), all firing sequences of a
+    token in one update launch with per-sequence fire flags.  Whole run captured
+    in one graph."""
+    import numpy as np
+    from paper_2608_30252_amd.state import MemoryLayout
+    B, Hq, Hkv, d, W, r, u, base_slots = 16, 32, 8, 64, 512, 16, 4, 1024
+    D = Hq * d
+    N = gamma * iters
+    rng = np.random.default_rng(seed)
+    P = rng.integers(8192, 32768, B).tolist()
+    ring_cap = (W + r * u + gamma + ROLLBACK + 7) // 8 * 8
+    lays = [MemoryLayout(0, W, r, ring_cap=ring_cap, mem_cap=1 << 20, slots_per_update=u) for _ in range(B)]
+    made0 = [lays[b].slots_materialised(P[b]) for b in range(B)]
+    mem_cap = base_slots + (N // (r * u) + 2) * u
+    bf = torch.bfloat16
+    mk = lambda *sh: torch.randn(*sh, device="cuda").to(bf)
+    mem_k = [mk(B, Hkv, mem_cap, d) for _ in range(layers)]
+    mem_v = [mk(B, Hkv, mem_cap, d) for _ in range(layers)]
+    ring_k = [mk(B, Hkv, ring_cap, d) for _ in range(layers)]
+    ring_v = [mk(B, Hkv, ring_cap, d) for _ in range(layers)]
+    q, kn, vn = mk(B, Hq, d), mk(B, Hkv, d), mk(B, Hkv, d)
+    out, lse = torch.empty_like(q), torch.empty(B, Hq, device="cuda")
+    x = mk(B, u, D)
+    w_g = [(torch.randn(2 * Hkv * d, D, device="cuda") * 0.02).to(bf) for _ in range(layers)]
+    ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_DECODE, B, Hq, Hkv, d), dtype=torch.uint8, device="cuda")
+    keys, n_upd_launch, n_fired = [], 0, 0
+
+    def run():
+        nonlocal n_upd_launch, n_fired
+        for t in range(N):
+            pos = [P[b] + t for b in range(B)]
+            views = [lays[b].decode_view(pos[b]) for b in range(B)]
+            mlen = [base_slots + views[b].mem_len - made0[b] for b in range(B)]
+            upds = [lays[b].update_in_pass_of(pos[b]) for b in range(B)]
+            fire = [1 if x_ is not None else 0 for x_ in upds]
+            for l in range(layers):
+                mad.draft_decode_attn(q, mad.KV(mem_k[l], mem_v[l], mlen),
+                                      mad.KV(ring_k[l], ring_v[l], [v.win_len for v in views],
+                                             [v.win_start for v in views]), kn, vn, out, lse, ws=ws)
+                keys.append(sum(mlen) + sum(v.win_len for v in views) + B)
+                if any(fire):
+                    posl = [x_.positions if x_ is not None else [0] * u for x_ in upds]
+                    rows = [base_slots + x_.mem_row - made0[b] if x_ is not None else mlen[b]
+                            for b, x_ in enumerate(upds)]
+                    mad.memory_update(x, w_g[l], posl, mad.KV(mem_k[l], mem_v[l], rows), fire=fire)
+                    n_upd_launch += 1
+            n_fired += sum(fire)
+
+    g = graph_of(torch, run)
+    g.replay()
+    t = time_graph(torch, g)
+    nbytes = sum(kv_bytes(k, Hkv, d) for k in keys)
+    del mem_k, mem_v, ring_k, ring_v, g
+    torch.cuda.empty_cache()
+    log(f"batched drafting B16: {t * 1e3 / iters:.3f} ms per gamma-{gamma} iteration, {nbytes / t / 1e12:.2f} TB/s, "
+        f"{n_upd_launch} update launches")
+    return {"workload": f"16 ragged sequences (prefixes U[8192, 32768), seed {seed}), 1024 slots + 512-token window, "
+                        f"32/8 heads, d64, bf16, {layers} layers, gamma {gamma} x {iters} iterations ({N} tokens), "
+                        "staggered memory updates (4 slots per 64-token block, per-sequence fire flags)",
+            "ms_per_iteration": round(t * 1e3 / iters, 4), "us_per_token_layer": round(t * 1e6 / (N * layers), 3),
+            "tokens_per_s": round(B * N / t, 1), "tbps_decode_bytes": round(nbytes / t / 1e12, 3),
+            "update_launches": n_upd_launch // max(layers, 1), "slot_updates_per_layer": n_fired,
+            "prefixes": P}
+
+
 def prefill_flops(P, S, W, r, u, Hq, d):
     """Multiply-adds x 2 of both attention products over every query's visible
     keys in the memory-prefill pass: a raw token at p sees min(S, p+1) sinks,
@@ -811,10 +1014,39 @@ def prefill_flops(P, S, W, r, u, Hq, d):
     return int((raw.sum() + slot.sum()) * Hq * d * 4)
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _time_calls(fn, seconds, min_calls=1, warm=True):
+    """Mean wall time of fn() over about `seconds` (at least min_calls calls, after one warm call)."""
+    if warm:
+        fn()
+    t0 = time.perf_counter()
+    calls = 0
+    while calls < min_calls or time.perf_counter() - t0 < seconds:
+        fn()
+        calls += 1
+    return (time.perf_counter() - t0) / calls, calls
+
+
 def cpu_baseline(seconds):
-    """The fp64 oracle on the host: the 32K compact-memory layer attention
-    (8 KV heads x 3072 keys x 4 query heads, head_dim 64), repeated for about
-    `seconds` of wall time."""
+    """The fp64 oracle on the host, a bounded sample of the workloads.
+
+    value: the 32K compact-memory layer attention (8 KV heads x 3072 keys x 4
+    query heads, head_dim 64) on every host thread OpenMP uses, repeated for
+    about `seconds`.  breadth: the same layer over the full 32769-token KV, the
+    verify attention of both target layers (B4 32/8 heads and B1 64/8 heads,
+    d 128, 32768 + 5 keys, 5 queries) and one memory update of 4 slot rows
+    (D 2048 -> 8 KV heads x 64), each timed on all threads and on one thread
+    (one or a few calls each; the verify layers dominate the few seconds)."""
     import numpy as np
     import oracle
     from paper_2608_30252_amd import synth
@@ -823,18 +1055,44 @@ def cpu_baseline(seconds):
     k = synth.normal((1, Hkv, n, d), 2).double().numpy()
     v = synth.normal((1, Hkv, n, d), 3).double().numpy()
     nn = np.array([n])
-    oracle.attend_batched(q, k, v, nn, d ** -0.5)
-    t0 = time.perf_counter()
-    calls = 0
-    while True:
-        oracle.attend_batched(q, k, v, nn, d ** -0.5)
-        calls += 1
-        if time.perf_counter() - t0 > seconds:
-            break
-    t = (time.perf_counter() - t0) / calls
-    return {"value": round(t * 1e6, 1), "unit": "us/layer", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{calls} calls of one 32K compact-memory layer attention (8 KV heads x 3072 keys x 4 "
-                      f"query heads, d 64, fp64)"}
+    threads = oracle.num_threads()
+    t, calls = _time_calls(lambda: oracle.attend_batched(q, k, v, nn, d ** -0.5), seconds)
+    res = {"value": round(t * 1e6, 1), "unit": "us/layer", "cores": threads, "kind": "oracle",
+           "cpu_model": _cpu_model(),
+           "sample": f"{calls} calls of one 32K compact-memory layer attention (8 KV heads x 3072 keys x 4 "
+                     f"query heads, d 64, fp64)"}
+    # breadth: full KV, verify (both target layers), one memory update; all threads and one thread
+    nf = 32769
+    kf = synth.normal((1, Hkv, nf, d), 4).double().numpy()
+    vf = synth.normal((1, Hkv, nf, d), 5).double().numpy()
+    items = [("32k_full_kv_layer", lambda: oracle.attend_batched(q, kf, vf, np.array([nf]), d ** -0.5), 1.0)]
+    T, L = 5, 32768 + 5
+    for name, B, Hq_v in (("verify_8b_layer_b4", 4, 32), ("verify_70b_layer_b1", 1, 64)):
+        qv = synth.normal((B, T, Hq_v, 128), 6).double().numpy()
+        kv_ = synth.normal((B, 8, L, 128), 7).double().numpy()
+        vv_ = synth.normal((B, 8, L, 128), 8).double().numpy()
+        items.append((name, lambda qv=qv, kv_=kv_, vv_=vv_, B=B: oracle.verify(qv, kv_, vv_, np.array([L] * B),
+                                                                               128 ** -0.5), 0.5))
+    x = synth.normal((4, 2048), 9).double().numpy()
+    w = synth.normal((2 * 8 * 64, 2048), 10, std=0.02).double().numpy()
+    items.append(("memory_update_4_rows", lambda: oracle.memory_update(x, w, np.array([32768, 32784, 32800, 32816]),
+                                                                       8, 64, 500000.0), 1.0))
+    breadth = {}
+    for name, fn, secs in items:
+        heavy = name.startswith("verify")   # seconds per call: one call each, no warm call
+        tm, cm = _time_calls(fn, secs, warm=not heavy)
+        oracle.set_threads(1)
+        t1, c1 = _time_calls(fn, secs / 4, warm=not heavy)
+        oracle.set_threads(threads)
+        breadth[name] = {"us_all_threads": round(tm * 1e6, 1), "us_one_thread": round(t1 * 1e6, 1),
+                         "calls": [cm, c1]}
+        log(f"cpu baseline {name}: {tm * 1e6:.0f} us on {threads} threads, {t1 * 1e6:.0f} us on one")
+    oracle.set_threads(1)
+    t1, c1 = _time_calls(lambda: oracle.attend_batched(q, k, v, nn, d ** -0.5), seconds / 6)
+    oracle.set_threads(threads)
+    breadth["32k_compact_layer_one_thread"] = {"us": round(t1 * 1e6, 1), "calls": c1}
+    res["breadth"] = breadth
+    return res
 
 
 if __name__ == "__main__":

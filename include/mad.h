@@ -335,6 +335,29 @@ int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *
                        void *out, void *stream);
 
 /*
+ * Measurement aids (not part of the attention path), used by the benchmark to
+ * put the kernels' times next to what the device itself delivers:
+ * mad_probe_stream_read: reads `bytes` (a multiple of 16; src 16-byte
+ *   aligned) with n_workgroups x 256 threads, each workgroup a contiguous
+ *   range, 8 nontemporal 16-byte loads in flight per thread; the HBM read
+ *   bandwidth a plain streaming kernel reaches.  sink: device unsigned, written only if an xor of the data
+ *   hits one particular value (keeps the loads), may be NULL.
+ * mad_probe_empty: an empty kernel of n_workgroups x threads (the launch floor).
+ * mad_probe_handoff_latency: one thread times, in shader-clock cycles, `reps`
+ *   repetitions (reps >= 2) of: row 0 a plain store until acknowledged; 1 a
+ *   device-scope store until acknowledged; 2 a device-scope atomic add (value
+ *   returned); 3 a device-scope load of the word row 1 stored; 4 a plain load
+ *   of the word row 0 stored; 5 a plain load of an untouched line; rows 6 and 7
+ *   the 100 MHz real-time counter and the shader clock at the end of each
+ *   repetition (their ratio gives the clock rate).  buf: device, at least
+ *   reps * 256 + 256 bytes, fresh lines; cycles: device uint64 [8][reps].
+ * Errors: MAD_EINVAL for bad arguments, MAD_EHIP for a failed launch.
+ */
+int mad_probe_stream_read(const void *src, size_t bytes, unsigned *sink, int n_workgroups, void *stream);
+int mad_probe_empty(int n_workgroups, int threads, void *stream);
+int mad_probe_handoff_latency(void *buf, size_t buf_bytes, unsigned long long *cycles, int reps, void *stream);
+
+/*
  * Workspace bytes needed by op (MAD_OP_*) for calls with at most these sizes:
  *   DECODE: B, Hq, Hkv, d                       (T, max_keys ignored)
  *   VERIFY: B, Hq, Hkv, d, T                    (max_keys ignored)

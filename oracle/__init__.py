@@ -68,6 +68,8 @@ def _load():
     lib.oracle_accept_stochastic.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
     for f in ("oracle_attend", "oracle_attend_batched", "oracle_verify", "oracle_project",
               "oracle_rope", "oracle_argmax", "oracle_accept_greedy"):
         getattr(lib, f).restype = None
@@ -90,6 +92,11 @@ def _ptr(a, t):
 def num_threads():
     """OpenMP threads the batched oracle routines run on."""
     return int(_load().oracle_num_threads())
+
+
+def set_threads(n):
+    """OpenMP threads of the batched oracle routines from now on (timing only)."""
+    _load().oracle_set_threads(int(n))
 
 
 def attend(q, k, v, scale, with_wsum=False):

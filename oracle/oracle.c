@@ -285,6 +285,9 @@ void oracle_accept_stochastic(int B, int T, int V, const float *p, const float *
 #ifdef _OPENMP
 #include <omp.h>
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+/* threads of the parallel loops from now on (timing of the oracle itself only) */
+void oracle_set_threads(int n) { if (n > 0) omp_set_num_threads(n); }
 #else
 int oracle_num_threads(void) { return 1; }
+void oracle_set_threads(int n) { (void)n; }
 #endif

@@ -64,6 +64,9 @@ def _load_library():
     lib.mad_rmsnorm_qkv_rope.argtypes = [vp, vp, f, vp, _i32p, i, i, i, i, i, d, i, vp, vp, vp, vp, vp]
     lib.mad_linear_residual.argtypes = [vp, vp, vp, i, i, i, vp, vp]
     lib.mad_rmsnorm_swiglu.argtypes = [vp, vp, f, vp, i, i, i, vp, vp]
+    lib.mad_probe_stream_read.argtypes = [vp, sz, vp, i, vp]
+    lib.mad_probe_empty.argtypes = [i, i, vp]
+    lib.mad_probe_handoff_latency.argtypes = [vp, sz, vp, i, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
@@ -71,7 +74,8 @@ def _load_library():
     for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
                "mad_accept_stochastic", "mad_draft_step_attn", "mad_draft_decode_attn_noalloc",
                "mad_memory_prefill_attn",
-               "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu"):
+               "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu", "mad_probe_stream_read",
+               "mad_probe_empty", "mad_probe_handoff_latency"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -503,3 +507,26 @@ def rmsnorm_swiglu(x: torch.Tensor, gamma: torch.Tensor, w_gate_up: torch.Tensor
     _check(_load_library().mad_rmsnorm_swiglu(_ptr(x), _ptr(gamma), float(eps), _ptr(w_gate_up), R, D, Fd,
                                               _ptr(out), _stream(x.device)))
     return out
+
+
+# ---- measurement aids (the benchmark's probes; not part of the attention path) ----
+
+def probe_stream_read(src: torch.Tensor, sink: Optional[torch.Tensor] = None, n_workgroups: int = 1024):
+    """Stream-read the bytes of a contiguous device tensor (a contiguous range per workgroup,
+    nontemporal 16-byte loads)."""
+    _need(src.is_contiguous() and src.numel() * src.element_size() % 16 == 0, "src: contiguous, bytes % 16 == 0")
+    _check(_load_library().mad_probe_stream_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink),
+                                                 n_workgroups, _stream(src.device)))
+
+
+def probe_empty(n_workgroups: int = 256, threads: int = 256, device=None):
+    """Launch an empty kernel (the launch floor)."""
+    dev = torch.device(device or "cuda")
+    _check(_load_library().mad_probe_empty(n_workgroups, threads, _stream(dev)))
+
+
+def probe_handoff_latency(buf: torch.Tensor, cycles: torch.Tensor, reps: int):
+    """Time the hand-off primitives (see include/mad.h); cycles: int64 [8, reps] on the device."""
+    _need(cycles.dtype == torch.int64 and cycles.shape == (8, reps) and cycles.is_contiguous(), "cycles [8, reps] int64")
+    _check(_load_library().mad_probe_handoff_latency(_ptr(buf), buf.numel() * buf.element_size(), _ptr(cycles),
+                                                     reps, _stream(buf.device)))
