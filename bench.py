@@ -143,13 +143,13 @@ def mfma_workload(torch, mad, kind):
         Hkv, d, T = 8, 128, 5
         L = 32768 + T
         for B, Hq in ((4, 32), (1, 64)):
-            k, vt = rn(B, Hkv, 32776, d), rn(B, Hkv, d, 32776)
+            k, v = rn(B, Hkv, 32776, d), rn(B, Hkv, 32776, d)
             q = rn(B, T, Hq, d)
             out, lse = torch.empty_like(q), torch.empty(B, T, Hq, device="cuda")
             ws = torch.zeros(mad.workspace_bytes(mad.MAD_OP_VERIFY, B, Hq, Hkv, d, T), dtype=torch.uint8,
                              device="cuda")
             for _ in range(4):
-                mad.verify_attn(q, k, vt, [L] * B, out, lse, ws=ws)
+                mad.verify_attn(q, mad.KV(k, v, [L] * B), out, lse, ws=ws)
             torch.cuda.synchronize()
             print(f"verify: 4 launches, B{B} {Hq}/{Hkv}, {4 * B * Hq * T * L * d} flop each", flush=True)
     else:
@@ -557,30 +557,40 @@ def main():
     torch.cuda.empty_cache()
 
     # -------------------------------------------------------------- verify ----
+    # the verifier's cache in its natural layout (rows of d, mad_verify_attn), and
+    # the same kernels over a transposed V cache (mad_verify_attn_vt)
     ver_res = {}
     for name, B, Hq, sets in (("8b_layer_b4", 4, 32, 1), ("70b_layer_b1", 1, 64, 3)):
         Hkv, d, T, cap = 8, 128, 5, 32776
         L = 32768 + T
         ks = [torch.randn(B, Hkv, cap, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
-        vts = [torch.randn(B, Hkv, d, cap, device="cuda").to(torch.bfloat16) for _ in range(sets)]
+        vs = [torch.randn(B, Hkv, cap, d, device="cuda").to(torch.bfloat16) for _ in range(sets)]
         qv = torch.randn(B, T, Hq, d, device="cuda").to(torch.bfloat16)
         ov = torch.empty_like(qv)
         lv = torch.empty(B, T, Hq, device="cuda")
         wsv = torch.zeros(mad.workspace_bytes(mad.MAD_OP_VERIFY, B, Hq, Hkv, d, T), dtype=torch.uint8,
                           device="cuda")
         reps = max(3, 6 // sets) * sets
-        fns = [lambda j=j: mad.verify_attn(qv, ks[j % sets], vts[j % sets], [L] * B, ov, lv, ws=wsv)
-               for j in range(reps)]
-        g = graph_of(torch, lambda: [f() for f in fns])
-        g.replay()
-        t = time_graph(torch, g, reps=2) / reps
         nbytes = kv_bytes(L, Hkv, d) * B
         flops = 4.0 * B * Hq * T * L * d
-        ver_res[name] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3),
-                         "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "bytes": nbytes,
-                         "mfma_tflops": round(flops / t / 1e12, 2)}
-        log(f"verify {name}: {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
-        del ks, vts, fns, g
+        res = {}
+        for layout in ("natural", "transposed_v"):
+            if layout == "natural":
+                fns = [lambda j=j: mad.verify_attn(qv, mad.KV(ks[j % sets], vs[j % sets], [L] * B), ov, lv, ws=wsv)
+                       for j in range(reps)]
+            else:
+                vts = [v_.transpose(2, 3).contiguous() for v_ in vs]
+                fns = [lambda j=j: mad.verify_attn_vt(qv, ks[j % sets], vts[j % sets], [L] * B, ov, lv, ws=wsv)
+                       for j in range(reps)]
+            g = graph_of(torch, lambda: [f() for f in fns])
+            g.replay()
+            t = time_graph(torch, g, reps=2) / reps
+            res[layout] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3),
+                           "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "mfma_tflops": round(flops / t / 1e12, 2)}
+            log(f"verify {name} ({layout} V): {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
+            del fns, g
+        ver_res[name] = dict(res["natural"], bytes=nbytes, transposed_v=res["transposed_v"])
+        del ks, vs, vts
     torch.cuda.empty_cache()
 
     # -------------------------------------------------------------- accept ----

@@ -196,23 +196,33 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
 
 /*
  * Target verify attention (Sec. 2.1: the target scores the drafted block in
- * one parallel pass; Sec. 3.3: over its full KV cache).  The T = gamma+1 new
- * tokens' K/V are already stored at rows len[b]-T .. len[b]-1; query t sees
- * rows 0 .. len[b]-T+t (the prefix and new tokens 0..t).
- *   q     device [B][T][Hq][d], BF16      out device [B][T][Hq][d], BF16
- *   lse   device fp32 [B][T][Hq] or NULL
- *   k     device keys, rows of d:    k  + b*seq_stride + h*head_stride + i*d
- *   vt    device values TRANSPOSED, one run of cap keys per feature:
- *                                    vt + b*seq_stride + h*head_stride + c*cap + i
- *         (the verifier's V cache is kept key-contiguous per feature so that
- *         both products of attention feed the matrix cores straight from HBM)
- *   len   HOST int32[B], T <= len[b] <= cap; cap a multiple of 8
- * T * G <= MAD_MAX_VERIFY_ROWS; d in {64, 128}; dtype BF16 only.
+ * one parallel pass; Sec. 3.3: over its full KV cache, which the compact draft
+ * memory leaves unchanged).  The T = gamma+1 new tokens' K/V are already
+ * stored at rows len[b]-T .. len[b]-1; query t sees rows 0 .. len[b]-T+t (the
+ * prefix and new tokens 0..t).
+ *   q    device [B][T][Hq][d], BF16        out  device [B][T][Hq][d], BF16
+ *   lse  device fp32 [B][T][Hq] or NULL
+ *   kv   the verifier's cache as it is: a linear mad_kv_view (start NULL),
+ *        K and V rows of d elements, kv->len[b] in [T, cap]
+ * T * G <= MAD_MAX_VERIFY_ROWS; d in {64, 128}; dtype BF16 only (both products
+ * run on the matrix cores; MAD_ENOTSUP otherwise).  Workspace MAD_OP_VERIFY.
  */
 int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
-                    const void *k, const void *vt, int64_t seq_stride, int64_t head_stride,
-                    int32_t cap, const int32_t *len,
-                    void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
+                    const mad_kv_view *kv, void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * The same verify attention for a verifier that keeps its V cache transposed,
+ * one run of cap keys per feature (key-contiguous), so that the A operand of
+ * the PV product (8 consecutive keys of one feature) is one 16-byte load:
+ *   k   device keys, rows of d:      k  + b*seq_stride + h*head_stride + i*d
+ *   vt  device values TRANSPOSED:    vt + b*seq_stride + h*head_stride + c*cap + i
+ *   len HOST int32[B], T <= len[b] <= cap; cap a multiple of 8
+ * Everything else as mad_verify_attn.
+ */
+int mad_verify_attn_vt(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
+                       const void *k, const void *vt, int64_t seq_stride, int64_t head_stride,
+                       int32_t cap, const int32_t *len,
+                       void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Greedy accept/reject (Sec. 2.1; greedy decoding at temperature 0, Sec. 4.1).

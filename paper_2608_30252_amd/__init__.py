@@ -11,6 +11,7 @@ Entry points (same names as the C ABI, without the ``mad_`` prefix):
     draft_decode_attn   draft decode attention over sink+slots | window ring (+ append)
     memory_update       mirrored K/V projection + RoPE + append of new memory slots
     verify_attn         target (gamma+1)-query verify attention over the full KV
+                        (verify_attn_vt: the same over a transposed V cache)
     accept_greedy       greedy accept/reject
 """
 import ctypes
@@ -53,8 +54,9 @@ def _load_library():
     kvp = ctypes.POINTER(_KVView)
     lib.mad_draft_decode_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, vp, vp, vp, sz, vp]
     lib.mad_memory_update.argtypes = [vp, vp, _i32p, _u8p, i, i, i, i, i, i, d, kvp, vp]
-    lib.mad_verify_attn.argtypes = [vp, i, i, i, i, i, i, f, vp, vp, ctypes.c_int64, ctypes.c_int64,
-                                    ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
+    lib.mad_verify_attn.argtypes = [vp, i, i, i, i, i, i, f, kvp, vp, vp, vp, sz, vp]
+    lib.mad_verify_attn_vt.argtypes = [vp, i, i, i, i, i, i, f, vp, vp, ctypes.c_int64, ctypes.c_int64,
+                                       ctypes.c_int32, _i32p, vp, vp, vp, sz, vp]
     lib.mad_accept_greedy.argtypes = [vp, i, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_accept_stochastic.argtypes = [vp, vp, vp, vp, i, i, i, vp, vp, vp, sz, vp]
     lib.mad_draft_step_attn.argtypes = [vp, i, i, i, i, i, f, kvp, kvp, vp, vp, _u8p, vp, vp, vp, sz, vp]
@@ -71,7 +73,7 @@ def _load_library():
     lib.mad_workspace_bytes.restype = sz
     lib.mad_last_error.restype = ctypes.c_char_p
     lib.mad_version.restype = ctypes.c_char_p
-    for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
+    for fn in ("mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_verify_attn_vt", "mad_accept_greedy",
                "mad_accept_stochastic", "mad_draft_step_attn", "mad_draft_decode_attn_noalloc",
                "mad_memory_prefill_attn",
                "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu", "mad_probe_stream_read",
@@ -323,30 +325,61 @@ def memory_update(x: torch.Tensor, w_kv: torch.Tensor, pos, mem: KV, fire=None, 
     _check(rc)
 
 
-def verify_attn(q: torch.Tensor, k: torch.Tensor, vt: torch.Tensor, length, out=None, lse=None,
-                scale: Optional[float] = None, ws: Optional[torch.Tensor] = None):
+def _verify_out(q, out, lse, scale):
+    _need(q.dim() == 4, "q must be [B, T, Hq, d]")
+    B, T, Hq, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=q.device)
+    _need(out.shape == q.shape and out.dtype == q.dtype, "out must match q")
+    _need(lse.shape == (B, T, Hq) and lse.dtype == torch.float32, "lse must be float32 [B, T, Hq]")
+    _contiguous(q=q, out=out, lse=lse)
+    _same_device(q.device, out=out, lse=lse)
+    return out, lse, (d ** -0.5 if scale is None else scale)
+
+
+def verify_attn(q: torch.Tensor, kv: KV, out=None, lse=None, scale: Optional[float] = None,
+                ws: Optional[torch.Tensor] = None):
+    """q [B, T, Hq, d]; kv: the verifier's cache as it is, K and V [B, Hkv, cap, d]
+    (rows of d), kv.length[b] rows valid with the T new tokens at len-T..len-1.
+    Returns (out [B, T, Hq, d], lse [B, T, Hq])."""
+    B, T, Hq, d = q.shape
+    Hkv = kv.k.shape[1]
+    _need(kv.start is None, "the verifier's cache is linear (no ring start)")
+    out, lse, scale = _verify_out(q, out, lse, scale)
+    view = kv.view(B, Hkv, d, q.dtype, q.device, "kv")
+    nbytes = workspace_bytes(MAD_OP_VERIFY, B, Hq, Hkv, d, T)
+    w = _ws_for(q.device, nbytes, ws)
+    rc = _load_library().mad_verify_attn(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), ctypes.byref(view),
+                                         _ptr(out), _ptr(lse), _ptr(w), w.numel(), _stream(q.device))
+    _check(rc)
+    return out, lse
+
+
+def verify_attn_vt(q: torch.Tensor, k: torch.Tensor, vt: torch.Tensor, length, out=None, lse=None,
+                   scale: Optional[float] = None, ws: Optional[torch.Tensor] = None):
     """q [B, T, Hq, d]; k [B, Hkv, cap, d]; vt [B, Hkv, d, cap] (values stored
     key-contiguous per feature); the T new tokens sit at rows len-T..len-1.
     Returns (out [B, T, Hq, d], lse [B, T, Hq])."""
     B, T, Hq, d = q.shape
     Hkv, cap = k.shape[1], k.shape[2]
-    if vt.shape != (B, Hkv, d, cap):
-        raise ValueError(f"vt must be [B, Hkv, d, cap] = {(B, Hkv, d, cap)}, got {tuple(vt.shape)}")
+    if vt.shape != (B, Hkv, d, cap) or k.shape != (B, Hkv, cap, d):
+        raise ValueError(f"k must be [B, Hkv, cap, d] and vt [B, Hkv, d, cap] = {(B, Hkv, d, cap)}")
     if k.stride(3) != 1 or k.stride(2) != d or vt.stride(3) != 1 or vt.stride(2) != cap:
         raise ValueError("k rows and vt feature runs must be contiguous")
     if k.stride(0) != vt.stride(0) or k.stride(1) != vt.stride(1):
         raise ValueError("k and vt must share sequence and head strides")
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, T, Hq), dtype=torch.float32, device=q.device)
-    if scale is None:
-        scale = d ** -0.5
+    _need(k.dtype == q.dtype and vt.dtype == q.dtype, "k, vt and q share the dtype")
+    _need(len(length) == B, "length needs one entry per sequence")
+    out, lse, scale = _verify_out(q, out, lse, scale)
+    _same_device(q.device, k=k, vt=vt)
     nbytes = workspace_bytes(MAD_OP_VERIFY, B, Hq, Hkv, d, T)
     w = _ws_for(q.device, nbytes, ws)
-    rc = _load_library().mad_verify_attn(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), _ptr(k), _ptr(vt),
-                             k.stride(0) if B > 1 else 0, k.stride(1), cap, _host_i32(length, B),
-                             _ptr(out), _ptr(lse), _ptr(w), w.numel(), _stream(q.device))
+    rc = _load_library().mad_verify_attn_vt(_ptr(q), B, T, Hq, Hkv, d, _dtype_code(q), float(scale), _ptr(k),
+                                            _ptr(vt), k.stride(0) if B > 1 else 0, k.stride(1), cap,
+                                            _host_i32(length, B), _ptr(out), _ptr(lse), _ptr(w), w.numel(),
+                                            _stream(q.device))
     _check(rc)
     return out, lse
 

@@ -320,20 +320,29 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
     return hip_status(mad::launch_update(a, dtype, (hipStream_t)stream), "memory update launch");
 }
 
-int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale, const void *k,
-                    const void *vt, int64_t seq_stride, int64_t head_stride, int32_t cap, const int32_t *len,
-                    void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The verify attention over either V layout; K and V share the strides.
+int verify_impl(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale, const void *k,
+                const void *v, bool vnat, int64_t seq_stride, int64_t head_stride, int32_t cap, const int32_t *len,
+                void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
     int rc = check_heads(B, Hq, Hkv, d, dtype);
     if (rc) return rc;
-    if (dtype != MAD_BF16) return fail(MAD_ENOTSUP, "verify attention runs in bf16 only");
+    if (dtype != MAD_BF16) return fail(MAD_ENOTSUP, "verify attention runs in bf16 only (matrix cores)");
     const int G = Hq / Hkv;
     if (T < 1 || T * G > MAD_MAX_VERIFY_ROWS)
         return fail(MAD_EINVAL, "T=%d: T*G=%d must be in [1, %d]", T, T * G, MAD_MAX_VERIFY_ROWS);
-    if (!q || !k || !vt || !out || !len) return fail(MAD_EINVAL, "null q, k, vt, out or len");
-    if (!aligned16(q) || !aligned16(k) || !aligned16(vt) || !aligned16(out))
-        return fail(MAD_EINVAL, "q/k/vt/out not 16-byte aligned");
+    if (!q || !k || !v || !out || !len) return fail(MAD_EINVAL, "null q, k, v, out or len");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+        return fail(MAD_EINVAL, "q/k/v/out not 16-byte aligned");
     if (!(scale > 0.f) || scale != scale) return fail(MAD_EINVAL, "scale must be positive");
-    if (cap < 8 || cap % 8) return fail(MAD_EINVAL, "cap=%d must be a positive multiple of 8", cap);
+    if (vnat) {
+        if (cap < 1) return fail(MAD_EINVAL, "cap=%d", cap);
+    } else if (cap < 8 || cap % 8) {
+        return fail(MAD_EINVAL, "cap=%d must be a positive multiple of 8 (transposed V)", cap);
+    }
     if (head_stride < (int64_t)cap * d || head_stride % 8 || seq_stride < 0 || seq_stride % 8)
         return fail(MAD_EINVAL, "bad strides (seq %lld, head %lld) for cap %d, d %d", (long long)seq_stride,
                     (long long)head_stride, cap, d);
@@ -345,12 +354,13 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
     if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
     if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
     if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
-    mad::VerifyPlan p = mad::plan_verify(B, Hkv, G, T, len);
+    mad::VerifyPlan p = mad::plan_verify(B, Hkv, G, T, len, vnat);
     mad::VerifyArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
     a.k = k;
-    a.vt = vt;
+    a.vt = v;
+    a.vnat = vnat ? 1 : 0;
     a.out = out;
     a.lse = lse;
     a.seq = seq_stride;
@@ -372,6 +382,26 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
     a.part_rows = T * G;
     for (int b = 0; b < B; ++b) a.len[b] = len[b];
     return hip_status(mad::launch_verify(a, (hipStream_t)stream), "verify launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
+                    const mad_kv_view *kv, void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    if (!kv) return fail(MAD_EINVAL, "null kv");
+    if (kv->start) return fail(MAD_EINVAL, "kv: the verifier's cache is linear (start must be NULL)");
+    if (!kv->len) return fail(MAD_EINVAL, "kv: null len");
+    return verify_impl(q, B, T, Hq, Hkv, d, dtype, scale, kv->k, kv->v, true, kv->seq_stride, kv->head_stride,
+                       kv->cap, kv->len, out, lse, ws, ws_bytes, stream);
+}
+
+int mad_verify_attn_vt(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale, const void *k,
+                       const void *vt, int64_t seq_stride, int64_t head_stride, int32_t cap, const int32_t *len,
+                       void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    return verify_impl(q, B, T, Hq, Hkv, d, dtype, scale, k, vt, false, seq_stride, head_stride, cap, len, out, lse,
+                       ws, ws_bytes, stream);
 }
 
 int mad_memory_prefill_attn(const void *q_raw, const void *q_slot, int B, int Hq, int Hkv, int d, int dtype,

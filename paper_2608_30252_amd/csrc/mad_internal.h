@@ -75,7 +75,7 @@ constexpr int kVerifyTargetWGs = 256;   // workgroups the split count aims at (o
 constexpr int kVerifyMaxSplits = 128;
 
 struct VerifyArgs {
-    const void *q, *k, *vt;
+    const void *q, *k, *vt;   // vt: V in natural rows [cap][d] when vnat, else one run of cap keys per feature
     void *out;
     float *lse;
     int64_t seq, head;    // element strides of sequences and KV heads (K and V^T alike)
@@ -83,6 +83,7 @@ struct VerifyArgs {
     float *part_ml;       // [units][n_splits][part_rows][2] (max, sum)
     float scale_log2;
     int cap, Hq, Hkv, G, T, d, units, n_splits, chunk, part_rows;
+    int vnat;             // 1: V stored in natural rows
     int len[kMaxB];
 };
 
@@ -122,7 +123,7 @@ struct VerifyPlan {
     int units, n_splits, chunk;
 };
 
-VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len);
+VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len, bool vnat);
 size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T);
 void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml);
 hipError_t launch_verify(const VerifyArgs &a, hipStream_t st);

@@ -10,9 +10,13 @@
 //   * S^T = K Q^T takes K rows as the A operand.  Key rows are assigned to the
 //     A rows with a fixed permutation so that the S^T accumulator already holds,
 //     in every lane, the 8 consecutive keys that the next product needs;
-//   * O^T = V^T P^T takes the values from the verifier's key-contiguous V cache
-//     (one run of cap keys per feature), 8 keys = 16 bytes a lane, and the
-//     probabilities from the lane's own scores (rounded to bf16);
+//   * O^T = V^T P^T takes its A operand (8 consecutive keys of one feature)
+//     either from the verifier's V cache in its natural layout (rows of d
+//     features: staged in LDS as they are, 16-byte chunks XOR-swizzled by row,
+//     and read back with two transposing LDS reads, ds_read_b64_tr_b16) or from
+//     a key-contiguous V^T cache (one run of cap keys per feature: 16 bytes a
+//     lane straight from memory); the probabilities come from the lane's own
+//     scores (rounded to bf16);
 //   * online softmax per query row: the row's 8 scores sit in one lane, the
 //     row max needs two cross-lane exchanges.
 // Each wave of a workgroup streams its own 32-key slabs (K rows and V^T
@@ -68,6 +72,7 @@ __global__ __launch_bounds__(256) void verify_split_kernel(const VerifyArgs a) {
     const int k1 = min(len, k0 + a.chunk);
     const int cap = a.cap;
     const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
+    // V: natural rows [cap][D] (VNAT) or one run of cap keys per feature [D][cap]
     const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
     const int lr = lane & 15, lg = lane >> 4;   // row within a 16-block, lane group
 
@@ -293,8 +298,17 @@ struct VerifyLdsCfg {
 };
 
 __device__ __forceinline__ int vk_swz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
+// natural V rows: 16-byte chunk c of key row k sits at chunk c ^ vn_swz(k); a
+// transposing read of 16 lanes covers rows k0 .. k0+3 (k0 a multiple of 4) x
+// two adjacent chunks, and XOR with 2 (k mod 4) puts the eight (row, chunk)
+// pairs on distinct banks
+__device__ __forceinline__ int vn_swz(int k) { return (k & 3) << 1; }
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4s_t lds_read_tr16(const unsigned char *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s_t *)(p));
+}
 
-template <int D, int NB>
+template <int D, int NB, bool VNAT>
 __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) {
     using C = VerifyLdsCfg<D>;
     constexpr int KST = D / 32, DB = D / 16, CPR = D / 8;
@@ -308,6 +322,7 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
     const int k1 = min(len, k0 + a.chunk);
     const int cap = a.cap;
     const bf16_t *K = reinterpret_cast<const bf16_t *>(a.k) + b * a.seq + c * a.head;
+    // V: natural rows [cap][D] (VNAT) or one run of cap keys per feature [D][cap]
     const bf16_t *VT = reinterpret_cast<const bf16_t *>(a.vt) + b * a.seq + c * a.head;
     const int lr = lane & 15, lg = lane >> 4;
     // waves 0 .. 2 NB - 1 compute (row block wave % NB, key half wave / NB), so
@@ -346,11 +361,16 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
             const int kr = cidx / CPR, slot = cidx % CPR;
             const int key = min(kb + kr, len - 1);   // rows past len: a valid row, masked
             lds_stream16(K + (size_t)key * D + (slot ^ vk_swz(kr)) * 8, st + inst * 1024);
-            // V^T: feature cidx / 8, LDS slot cidx % 8 holds key chunk slot ^ (f & 7)
-            const int f = cidx >> 3, vs = cidx & 7;
-            int kc = kb + ((vs ^ (f & 7)) << 3);
-            if (kc + 8 > cap) kc = cap - 8;          // chunks past the cache: any valid chunk (zeroed when used)
-            lds_stream16(VT + (size_t)f * cap + kc, st + C::KBYTES + inst * 1024);
+            if constexpr (VNAT) {
+                // V rows like K rows (the same clamp), chunk slot holds global chunk slot ^ vn_swz(row)
+                lds_stream16(VT + (size_t)key * D + (slot ^ vn_swz(kr)) * 8, st + C::KBYTES + inst * 1024);
+            } else {
+                // V^T: feature cidx / 8, LDS slot cidx % 8 holds key chunk slot ^ (f & 7)
+                const int f = cidx >> 3, vs = cidx & 7;
+                int kc = kb + ((vs ^ (f & 7)) << 3);
+                if (kc + 8 > cap) kc = cap - 8;          // chunks past the cache: any valid chunk (zeroed when used)
+                lds_stream16(VT + (size_t)f * cap + kc, st + C::KBYTES + inst * 1024);
+            }
         }
     };
 
@@ -417,19 +437,36 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
             #pragma unroll
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
         }
-        #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            const int f = db * 16 + lr;
-            u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + C::KBYTES + f * C::VROW + (((4 * kh + lg) ^ (f & 7)) << 4));
-            if (kg + 8 > len) {   // values of keys past len may be anything: zero them
-                #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int kk = kg + 2 * e;
-                    if (kk >= len) w[e] = 0u;
-                    else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
-                }
+        if constexpr (VNAT) {
+            // A = V^T rows (features db*16 + lr), keys 32 kh + 8 lg .. +7, from
+            // the transposing reads of key rows 32 kh + 8 lg + {0..3} and {4..7}
+            // (rows past len hold the clamped row len - 1, weighted 0)
+            const unsigned char *sv = st + C::KBYTES;
+            const int tr_row = 32 * kh + 8 * lg + (lr >> 2), tr_byte = 8 * (lr & 3);
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int byte = db * 32 + tr_byte, chunk = byte >> 4, half = byte & 8;
+                const int r0 = tr_row, r1 = tr_row + 4;
+                const v4s_t lo = lds_read_tr16(sv + r0 * C::RB + ((chunk ^ vn_swz(r0)) << 4) + half);
+                const v4s_t hi = lds_read_tr16(sv + r1 * C::RB + ((chunk ^ vn_swz(r1)) << 4) + half);
+                const bf16x8_v vf = __builtin_bit_cast(bf16x8_v, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[db], 0, 0, 0);
             }
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_v, w), pf, o[db], 0, 0, 0);
+        } else {
+            #pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int f = db * 16 + lr;
+                u32x4_v w = *reinterpret_cast<const u32x4_v *>(st + C::KBYTES + f * C::VROW + (((4 * kh + lg) ^ (f & 7)) << 4));
+                if (kg + 8 > len) {   // values of keys past len may be anything: zero them
+                    #pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kk = kg + 2 * e;
+                        if (kk >= len) w[e] = 0u;
+                        else if (kk + 1 >= len) w[e] &= 0x0000ffffu;
+                    }
+                }
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_v, w), pf, o[db], 0, 0, 0);
+            }
         }
     };
 
@@ -549,7 +586,7 @@ __global__ __launch_bounds__(D) void verify_merge_kernel(const VerifyArgs a) {
 
 // ------------------------------------------------------------------ host ----
 
-VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len) {
+VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len, bool vnat) {
     VerifyPlan p;
     p.units = B * Hkv;
     int n_max = 0;
@@ -559,7 +596,7 @@ VerifyPlan plan_verify(int B, int Hkv, int G, int T, const int *len) {
     if (ns < 1) ns = 1;
     int chunk = (n_max + ns - 1) / ns;
     // whole slabs: 4 x 32 keys for the register-resident kernel, 64 for the LDS-staged one
-    const int gran = ((T * G + 15) / 16 >= kVerifyLdsMinNb) ? 64 : 128;
+    const int gran = (vnat || (T * G + 15) / 16 >= kVerifyLdsMinNb) ? 64 : 128;
     chunk = (chunk + gran - 1) / gran * gran;
     if (chunk < gran) chunk = gran;
     p.chunk = chunk;
@@ -590,8 +627,13 @@ void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_
 
 template <int D, int NB>
 static hipError_t launch_split(const VerifyArgs &a, hipStream_t st) {
+    if (a.vnat) {
+        hipLaunchKernelGGL((verify_lds_kernel<D, NB, true>), dim3((unsigned)(a.units * a.n_splits)),
+                           dim3(64 * VerifyLdsCfg<D>::NWV), VerifyLdsCfg<D>::SMEM, st, a);
+        return hipGetLastError();
+    }
     if (NB >= kVerifyLdsMinNb) {
-        hipLaunchKernelGGL((verify_lds_kernel<D, NB>), dim3((unsigned)(a.units * a.n_splits)),
+        hipLaunchKernelGGL((verify_lds_kernel<D, NB, false>), dim3((unsigned)(a.units * a.n_splits)),
                            dim3(64 * VerifyLdsCfg<D>::NWV), VerifyLdsCfg<D>::SMEM, st, a);
         return hipGetLastError();
     }

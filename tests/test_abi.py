@@ -26,7 +26,7 @@ def mad():
 
 def test_every_declared_symbol_is_exported(mad):
     names = _declared_functions()
-    assert {"mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_accept_greedy",
+    assert {"mad_draft_decode_attn", "mad_memory_update", "mad_verify_attn", "mad_verify_attn_vt", "mad_accept_greedy",
             "mad_workspace_bytes", "mad_last_error", "mad_version"} <= set(names)
     lib = ctypes.CDLL(mad.LIB_PATH)
     for n in names:
@@ -118,9 +118,9 @@ def test_verify_and_accept_validation(mad):
     lib = mad._load_library()
     ln = (ctypes.c_int32 * 1)(100)
     def ver(T=5, Hq=32, Hkv=8, d=128, dtype=mad.MAD_BF16, cap=128, head=128 * 128, ln_=ln):
-        return lib.mad_verify_attn(ctypes.c_void_p(1 << 20), 1, T, Hq, Hkv, d, dtype, 0.088, ctypes.c_void_p(1 << 21),
-                                   ctypes.c_void_p(1 << 22), 0, head, cap, ln_, ctypes.c_void_p(1 << 23), None,
-                                   None, 0, None)
+        return lib.mad_verify_attn_vt(ctypes.c_void_p(1 << 20), 1, T, Hq, Hkv, d, dtype, 0.088,
+                                      ctypes.c_void_p(1 << 21), ctypes.c_void_p(1 << 22), 0, head, cap, ln_,
+                                      ctypes.c_void_p(1 << 23), None, None, 0, None)
     assert ver(dtype=mad.MAD_F32) == mad.MAD_ENOTSUP
     assert ver(T=0) == mad.MAD_EINVAL
     assert ver(T=5, Hq=128, Hkv=8) == mad.MAD_EINVAL                 # T*G = 80 > 64
@@ -129,6 +129,17 @@ def test_verify_and_accept_validation(mad):
     assert ver(ln_=(ctypes.c_int32 * 1)(3)) == mad.MAD_EINVAL        # len < T
     assert ver(ln_=(ctypes.c_int32 * 1)(200)) == mad.MAD_EINVAL      # len > cap
     assert ver() == mad.MAD_EWS                                      # workspace missing
+    # the natural layout: a linear mad_kv_view (rows of d); any cap
+    def vnat(cap=100, start=None, ln_=ln, dtype=mad.MAD_BF16, head=100 * 128, kv=True):
+        view = mad._KVView(1 << 21, 1 << 22, 0, head, cap, start, ln_)
+        return lib.mad_verify_attn(ctypes.c_void_p(1 << 20), 1, 5, 32, 8, 128, dtype, 0.088,
+                                   ctypes.byref(view) if kv else None, ctypes.c_void_p(1 << 23), None, None, 0, None)
+    assert vnat() == mad.MAD_EWS                                     # cap 100 is fine here; workspace missing
+    assert vnat(kv=False) == mad.MAD_EINVAL
+    assert vnat(start=(ctypes.c_int32 * 1)(0)) == mad.MAD_EINVAL     # the verifier's cache is linear
+    assert vnat(dtype=mad.MAD_F32) == mad.MAD_ENOTSUP
+    assert vnat(ln_=(ctypes.c_int32 * 1)(101)) == mad.MAD_EINVAL     # len > cap
+    assert vnat(head=64) == mad.MAD_EINVAL
     acc = lambda B=1, T=5, V=128256, dtype=mad.MAD_F32, draft=1 << 21: lib.mad_accept_greedy(
         ctypes.c_void_p(1 << 20), dtype, ctypes.c_void_p(draft) if draft else None, B, T, V,
         ctypes.c_void_p(1 << 22), ctypes.c_void_p(1 << 23), None, 0, None)

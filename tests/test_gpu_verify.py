@@ -1,9 +1,10 @@
-"""GPU parity of mad_verify_attn against the fp64 oracle.
+"""GPU parity of the verify attention against the fp64 oracle.
 
-K is stored [B][Hkv][cap][d]; V is stored key-contiguous per feature,
-[B][Hkv][d][cap] (the verifier's cache layout).  The oracle reads the same
-values in natural layout.  Query t of the T new tokens sees rows
-0 .. len-T+t.  Tolerances: see parity.py.
+mad_verify_attn reads the verifier's cache as it is, K and V in rows of d
+([B][Hkv][cap][d]); mad_verify_attn_vt reads a V cache stored key-contiguous
+per feature ([B][Hkv][d][cap]).  The oracle reads the same values in natural
+layout.  Query t of the T new tokens sees rows 0 .. len-T+t.  Tolerances: see
+parity.py.
 """
 import numpy as np
 import pytest
@@ -12,6 +13,8 @@ import torch
 from parity import abs_score_verify, check_lse, check_out, to_np
 
 pytestmark = pytest.mark.gpu
+
+LAYOUTS = ("natural", "transposed_v")
 
 
 def _inputs(B, T, Hq, Hkv, d, cap, seed):
@@ -23,11 +26,14 @@ def _inputs(B, T, Hq, Hkv, d, cap, seed):
     return q, k, v
 
 
-def _run(q, k, v, length):
+def _run(q, k, v, length, layout="natural"):
     import paper_2608_30252_amd as mad
     dev = torch.device("cuda")
-    vt = v.transpose(-1, -2).contiguous()
-    out, lse = mad.verify_attn(q.to(dev), k.to(dev), vt.to(dev), length)
+    if layout == "natural":
+        out, lse = mad.verify_attn(q.to(dev), mad.KV(k.to(dev), v.to(dev), list(length)))
+    else:
+        vt = v.transpose(-1, -2).contiguous()
+        out, lse = mad.verify_attn_vt(q.to(dev), k.to(dev), vt.to(dev), length)
     torch.cuda.synchronize()
     return out.cpu(), lse.cpu()
 
@@ -64,25 +70,37 @@ def _make_peaky(q, k, length, c):
     return targets
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("Hq,Hkv,d,T", [(32, 8, 128, 5), (64, 8, 128, 5), (32, 8, 64, 6), (16, 1, 128, 4),
                                         (8, 8, 128, 1), (16, 16, 64, 2), (64, 4, 64, 4), (32, 2, 128, 4)])
-def test_small_shapes(Hq, Hkv, d, T):
+def test_small_shapes(Hq, Hkv, d, T, layout):
     B, cap = 2, 520
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=Hq + d + T)
     length = [517, 300]
-    out, lse = _run(q, k, v, length)
+    out, lse = _run(q, k, v, length, layout)
     _check(q, k, v, length, out, lse)
 
 
-def test_edge_lengths():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_edge_lengths(layout):
     B, T, Hq, Hkv, d, cap = 3, 5, 32, 8, 128, 64
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=40)
     length = [5, 64, 37]          # only the new tokens; full capacity; ragged
-    out, lse = _run(q, k, v, length)
+    out, lse = _run(q, k, v, length, layout)
     _check(q, k, v, length, out, lse)
 
 
-def test_stale_values_past_len_do_not_leak():
+def test_natural_layout_any_capacity():
+    # the natural layout takes any cache capacity (here not a multiple of 8) and odd lengths
+    B, T, Hq, Hkv, d, cap = 2, 5, 32, 8, 64, 301
+    q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=46)
+    length = [301, 77]
+    out, lse = _run(q, k, v, length, "natural")
+    _check(q, k, v, length, out, lse)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_stale_values_past_len_do_not_leak(layout):
     """Rows past len in the cache may hold anything (here: inf/NaN bit
     patterns); the output must not depend on them."""
     B, T, Hq, Hkv, d, cap = 1, 5, 32, 8, 128, 136
@@ -91,7 +109,7 @@ def test_stale_values_past_len_do_not_leak():
     k2, v2 = k.clone(), v.clone()
     k2[:, :, 101:] = float("nan")
     v2[:, :, 101:] = float("inf")
-    out, lse = _run(q, k2, v2, length)
+    out, lse = _run(q, k2, v2, length, layout)
     _check(q, k, v, length, out, lse)
 
 
@@ -108,23 +126,25 @@ def test_future_new_tokens_do_not_affect_earlier_queries():
     assert not torch.equal(out_a[:, 3:].view(torch.int16), out_b[:, 3:].view(torch.int16))
 
 
-def test_70b_shaped_layer_full_size():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_70b_shaped_layer_full_size(layout):
     # 64 query / 8 KV heads, d 128, batch 1, 32768-token prefix + 5 new tokens
     B, T, Hq, Hkv, d = 1, 5, 64, 8, 128
     length = [32768 + T]
     cap = 32776
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=43)
-    out, lse = _run(q, k, v, length)
+    out, lse = _run(q, k, v, length, layout)
     _check(q, k, v, length, out, lse)
 
 
-def test_8b_shaped_layer_full_size():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_8b_shaped_layer_full_size(layout):
     # 32 query / 8 KV heads, d 128, batch 4, 32768-token prefix + 5 new tokens; every sequence checked
     B, T, Hq, Hkv, d = 4, 5, 32, 8, 128
     length = [32768 + T] * B
     cap = 32776
     q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=44)
-    out, lse = _run(q, k, v, length)
+    out, lse = _run(q, k, v, length, layout)
     _check(q, k, v, length, out, lse)
 
 
