@@ -4,7 +4,9 @@ Each case fills the memory segment, the window ring and the new token with
 seeded values, runs the kernel through the C ABI, and compares with the
 oracle's attention over the key list the ABI defines:
     mem rows [0, mlen) ++ ring rows (start + i) % cap, i < wlen ++ new token.
-The same bf16 (or fp32) values feed both sides.  Tolerances: see parity.py.
+The same bf16 (or fp32) values feed both sides.  Every buffer the kernel
+writes is surrounded by sentinel bands checked after the call.  Tolerances:
+see parity.py.
 """
 import numpy as np
 import pytest
@@ -48,12 +50,32 @@ def _case(dtype, B, Hq, Hkv, d, mlen, wlen, wcap, wstart, new=True, seed=0, mcap
                     continue
                 q[b, h] = (peaky * kt.float()).to(dtype)
                 targets[(b, h)] = kt.double().numpy()
-    g = {n: t.to(dev) for n, t in dict(q=q, mk=mk, mv=mv, wk=wk, wv=wv, kn=kn, vn=vn).items()}
+    g = {n: t.to(dev) for n, t in dict(q=q, mk=mk, mv=mv, kn=kn, vn=vn).items()}
+    # every buffer the kernel writes (output, lse, the ring it appends to) sits
+    # between two 4 KiB sentinel bands that must come back untouched
+    guards = []
+
+    def guarded(t, fill):
+        pad = 4096 // t.element_size()
+        buf = torch.full((t.numel() + 2 * pad,), fill, dtype=t.dtype, device=dev)
+        view = buf[pad:pad + t.numel()].view(t.shape)
+        view.copy_(t)
+        guards.append((buf, pad, t.numel(), buf.clone()))
+        return view
+
+    g["wk"], g["wv"] = guarded(wk.to(dev), -77.0), guarded(wv.to(dev), -77.0)
     wk_before, wv_before = g["wk"].clone(), g["wv"].clone()
     memkv = mad.KV(g["mk"], g["mv"], mlen) if mem else None
     win = mad.KV(g["wk"], g["wv"], wlen, wstart)
-    out, lse = mad.draft_decode_attn(g["q"], memkv, win, g["kn"] if new else None, g["vn"] if new else None)
+    out = guarded(torch.full_like(g["q"], 3.0), 3.0)
+    lse = guarded(torch.full((B, Hq), 5.0, device=dev), 5.0)
+    mad.draft_decode_attn(g["q"], memkv, win, g["kn"] if new else None, g["vn"] if new else None, out, lse)
     torch.cuda.synchronize()
+    for buf, pad, n_, before in guards:
+        for band in (slice(0, pad), slice(pad + n_, 2 * pad + n_)):
+            a_, b_ = buf[band], before[band]
+            assert torch.equal(a_.view(torch.int16) if a_.element_size() == 2 else a_.view(torch.int32),
+                               b_.view(torch.int16) if b_.element_size() == 2 else b_.view(torch.int32)), "guard band"
 
     # oracle key lists per sequence
     import oracle

@@ -144,11 +144,11 @@ def test_batched_sixteen_ragged_sequences_staggered_updates():
     512-token window.  Every draft token is one decode launch for all 16
     sequences (per-sequence memory lengths and ring offsets); after it, one
     memory-update launch for the batch with fire[b] set for the sequences
-    whose block ended (staggered by the prefix).  64 tokens per sequence
-    (16 rounds of gamma = 4): every sequence crosses one boundary.  Checked
-    against the oracle: every 8th token's outputs for all sequences, the
-    token after each sequence's update (it reads the new slots), and every
-    materialised slot row."""
+    whose block ended (staggered by the prefix).  512 tokens per sequence
+    (128 rounds of gamma = 4, the batched drafting workload's length): every
+    sequence crosses eight boundaries.  Checked against the oracle: every
+    16th token's outputs for all sequences, the token after each sequence's
+    update (it reads the new slots), and every materialised slot row."""
     import oracle
     from oracle.masw_sets import MaswSets
     import paper_2608_30252_amd as mad
@@ -157,7 +157,7 @@ def test_batched_sixteen_ragged_sequences_staggered_updates():
 
     dev = torch.device("cuda")
     dtype = torch.bfloat16
-    B, Hq, Hkv, d, S, W, r, u, N = 16, 32, 8, 64, 0, 512, 16, 4, 64
+    B, Hq, Hkv, d, S, W, r, u, N = 16, 32, 8, 64, 0, 512, 16, 4, 512
     D = Hq * d
     scale = d ** -0.5
     P = np.random.default_rng(44).integers(8192, 32768, B).tolist()
@@ -200,7 +200,7 @@ def test_batched_sixteen_ragged_sequences_staggered_updates():
                                          mad.KV(g_rk, g_rv, [v.win_len for v in views], [v.win_start for v in views]),
                                          kn.to(dev), vn.to(dev), scale=scale)
         after_update = [b for b in range(B) if pos[b] - 1 in updated_at.get(b, ())]
-        rows = list(range(B)) if t % 8 == 7 else after_update
+        rows = list(range(B)) if t % 16 == 15 else after_update
         if rows:
             n = np.zeros(len(rows), dtype=np.int64)
             nmax = max(sets.raw_view(pos[b]).size() for b in rows)
