@@ -141,12 +141,21 @@ __host__ __device__ inline double rope_reduce(double a) {
     const double n = rint(a * 0.15915494309189535);            // 1 / (2 pi)
     return fma(-n, 2.4492935982947064e-16, fma(-n, 6.283185307179586, a));
 }
-__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
+// The rotation in two parts, so that a kernel can take the cosine and sine
+// before the pair is known; the products are fused explicitly so that every
+// kernel rounds the rotation the same way.
+__device__ __forceinline__ void rope_cs(int pos, double theta, float *c, float *s) {
     const double r = rope_reduce((double)pos * theta);
-    float s, c;
-    sincosf((float)r, &s, &c);
-    *k0 = y0 * c - y1 * s;
-    *k1 = y1 * c + y0 * s;
+    sincosf((float)r, s, c);
+}
+__device__ __forceinline__ void rope_apply(float y0, float y1, float c, float s, float *k0, float *k1) {
+    *k0 = fmaf(y0, c, -(y1 * s));
+    *k1 = fmaf(y1, c, y0 * s);
+}
+__device__ __forceinline__ void rope_rotate(float y0, float y1, int pos, double theta, float *k0, float *k1) {
+    float c, s;
+    rope_cs(pos, theta, &c, &s);
+    rope_apply(y0, y1, c, s, k0, k1);
 }
 
 // ---- cross-workgroup hand-off without cache maintenance -------------------
