@@ -320,8 +320,8 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
                 vp = row_src(tb + row, true);
             }
             // K: LDS slot `slot` of row `row` holds global chunk slot ^ (row & SW)
-            lds_stream16(reinterpret_cast<const uint4 *>(kp) + (slot ^ (row & C::SW)), st + inst * 1024);
-            lds_stream16(reinterpret_cast<const uint4 *>(vp) + slot, st + NSUB * 8192 + inst * 1024);
+            lds_stream16_nt(reinterpret_cast<const uint4 *>(kp) + (slot ^ (row & C::SW)), st + inst * 1024);
+            lds_stream16_nt(reinterpret_cast<const uint4 *>(vp) + slot, st + NSUB * 8192 + inst * 1024);
         }
     };
 

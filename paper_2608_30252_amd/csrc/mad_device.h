@@ -280,6 +280,15 @@ __device__ __forceinline__ void lds_stream16(const void *src, void *lds_base) {
     asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
                  : "=&s"(saved) : "v"(src), "s"(m) : "memory");
 }
+// The same load with the non-temporal hint, for data read once per launch (the
+// key/value streams): measured 6-9 % faster than the plain form on the
+// bandwidth-bound verify attention and on the compact decode layer.
+__device__ __forceinline__ void lds_stream16_nt(const void *src, void *lds_base) {
+    const uint32_t m = __builtin_amdgcn_readfirstlane(lds_addr(lds_base));
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved) : "v"(src), "s"(m) : "memory");
+}
 // Load N dwords at a wave-uniform address through the scalar cache (s_load).
 template <int N>
 __device__ __forceinline__ void load_uniform_dwords(const void *p, uint32_t (&out)[N]) {

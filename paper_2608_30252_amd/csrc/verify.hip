@@ -360,16 +360,16 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
             // K: row cidx / CPR, LDS slot cidx % CPR holds global chunk slot ^ swz(row)
             const int kr = cidx / CPR, slot = cidx % CPR;
             const int key = min(kb + kr, len - 1);   // rows past len: a valid row, masked
-            lds_stream16(K + (size_t)key * D + (slot ^ vk_swz(kr)) * 8, st + inst * 1024);
+            lds_stream16_nt(K + (size_t)key * D + (slot ^ vk_swz(kr)) * 8, st + inst * 1024);
             if constexpr (VNAT) {
                 // V rows like K rows (the same clamp), chunk slot holds global chunk slot ^ vn_swz(row)
-                lds_stream16(VT + (size_t)key * D + (slot ^ vn_swz(kr)) * 8, st + C::KBYTES + inst * 1024);
+                lds_stream16_nt(VT + (size_t)key * D + (slot ^ vn_swz(kr)) * 8, st + C::KBYTES + inst * 1024);
             } else {
                 // V^T: feature cidx / 8, LDS slot cidx % 8 holds key chunk slot ^ (f & 7)
                 const int f = cidx >> 3, vs = cidx & 7;
                 int kc = kb + ((vs ^ (f & 7)) << 3);
                 if (kc + 8 > cap) kc = cap - 8;          // chunks past the cache: any valid chunk (zeroed when used)
-                lds_stream16(VT + (size_t)f * cap + kc, st + C::KBYTES + inst * 1024);
+                lds_stream16_nt(VT + (size_t)f * cap + kc, st + C::KBYTES + inst * 1024);
             }
         }
     };
