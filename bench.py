@@ -320,6 +320,16 @@ def time_graph(torch, g, reps=1):
     return e0.elapsed_time(e1) * 1e-3 / reps   # seconds per replay
 
 
+def time_cycled(torch, fns, launches=64, reps=5):
+    """Median device time per launch of `launches` calls cycling through fns
+    (one call per rotated buffer set), captured in one graph so that the
+    graph's own launch cost is spread over many kernels, as in a decode loop."""
+    g = graph_of(torch, lambda: [fns[i % len(fns)]() for i in range(launches)])
+    g.replay()
+    ts = sorted(time_graph(torch, g) for _ in range(reps))
+    return ts[len(ts) // 2] / launches
+
+
 def mean_launch_seconds(torch, launches, reps=3):
     """Mean device time per launch: the launches are captured in one HIP graph
     and replayed back to back between two HIP events on the replaying stream.
@@ -544,16 +554,14 @@ def main():
         posl = [[16 * (2048 + 4 * b + i) for i in range(n_new)] for b in range(B)]
         fns = [lambda j=j: mad.memory_update(xs[j], ws_[j], posl, mad.KV(mks[j], mvs[j], [1024] * B))
                for j in range(sets)]
-        g = graph_of(torch, lambda: [f() for f in fns])
-        g.replay()
-        t = time_graph(torch, g, reps=4) / sets
+        t = time_cycled(torch, fns)
         nbytes = 2 * Hkv * d * D * 2 + B * n_new * D * 2 + B * n_new * 2 * Hkv * d * 2
         flops = 2.0 * B * n_new * D * 2 * Hkv * d
         upd_res[name] = {"rows": B * n_new, "us": round(t * 1e6, 3), "tbps": round(nbytes / t / 1e12, 3),
                          "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "tflops": round(flops / t / 1e12, 3),
                          "mfma_frac_of_bf16_peak": round(flops / t / PEAK_BF16, 6), "bytes": nbytes}
         log(f"memory update {name}: {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
-        del xs, ws_, mks, mvs, fns, g
+        del xs, ws_, mks, mvs, fns
     torch.cuda.empty_cache()
 
     # -------------------------------------------------------------- verify ----
@@ -582,13 +590,11 @@ def main():
                 vts = [v_.transpose(2, 3).contiguous() for v_ in vs]
                 fns = [lambda j=j: mad.verify_attn_vt(qv, ks[j % sets], vts[j % sets], [L] * B, ov, lv, ws=wsv)
                        for j in range(reps)]
-            g = graph_of(torch, lambda: [f() for f in fns])
-            g.replay()
-            t = time_graph(torch, g, reps=2) / reps
+            t = time_cycled(torch, fns, launches=24)
             res[layout] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3),
                            "hbm_frac": round(nbytes / t / PEAK_HBM, 4), "mfma_tflops": round(flops / t / 1e12, 2)}
             log(f"verify {name} ({layout} V): {t * 1e6:.2f} us, {nbytes / t / 1e12:.3f} TB/s")
-            del fns, g
+            del fns
         ver_res[name] = dict(res["natural"], bytes=nbytes, transposed_v=res["transposed_v"])
         del ks, vs, vts
     torch.cuda.empty_cache()
@@ -604,13 +610,11 @@ def main():
         wsa = torch.zeros(mad.workspace_bytes(mad.MAD_OP_ACCEPT, B, 1, 1, 64, T, V), dtype=torch.uint8,
                           device="cuda")
         fns = [lambda j=j: mad.accept_greedy(lg[j], dr, na, nx, ws=wsa) for j in range(4)]
-        g = graph_of(torch, lambda: [f() for f in fns])
-        g.replay()
-        t = time_graph(torch, g, reps=4) / 4
+        t = time_cycled(torch, fns)
         nbytes = B * T * V * 4
         acc_res[name] = {"us": round(t * 1e6, 2), "tbps": round(nbytes / t / 1e12, 3), "bytes": nbytes}
         log(f"accept {name}: {t * 1e6:.2f} us")
-        del lg, fns, g
+        del lg, fns
         # stochastic accept/reject with caller uniforms: reads the drafted tokens'
         # probabilities, then one target row (and one draft row) of the vocabulary
         ps = [torch.softmax(torch.randn(B, T, V, device="cuda"), -1) for _ in range(4)]
@@ -619,12 +623,10 @@ def main():
         wss = torch.zeros(mad.workspace_bytes(mad.MAD_OP_ACCEPT_STOCH, B, 1, 1, 64, T, V), dtype=torch.uint8,
                           device="cuda")
         fns = [lambda j=j: mad.accept_stochastic(ps[j], qs[j], dr, uu, na, nx, ws=wss) for j in range(4)]
-        g = graph_of(torch, lambda: [f() for f in fns])
-        g.replay()
-        t = time_graph(torch, g, reps=4) / 4
+        t = time_cycled(torch, fns)
         acc_res[name + "_stochastic"] = {"us": round(t * 1e6, 2), "bytes_max": B * 2 * V * 4}
         log(f"accept {name} stochastic: {t * 1e6:.2f} us")
-        del ps, qs, fns, g
+        del ps, qs, fns
 
     # ------------------------------------------------ draft layer, end to end ----
     lay_res = draft_layer_bench(torch, mad, K)
