@@ -849,6 +849,20 @@ def device_probes(torch, mad):
         stream[nwg] = size / t
         log(f"stream probe ({nwg} workgroups): {size / t / 1e12:.3f} TB/s")
     del bufs
+    # one CU reading L2-resident data: 256 workgroups (one per CU) all read the
+    # same 128 KB or 512 KB; the difference of the two launch times over the
+    # difference of bytes is the per-CU rate, by waves per workgroup
+    shr = torch.empty(512 << 10, dtype=torch.uint8, device="cuda")
+    l2 = {}
+    for threads in (256, 512, 1024):
+        ts = {}
+        for kb in (128, 512):
+            src = shr[:kb << 10]
+            ts[kb] = time_cycled(torch, [lambda s_=src, t_=threads: mad.probe_shared_read(s_, sink, 256, t_)])
+        l2[str(threads // 64)] = {"us_128k": round(ts[128] * 1e6, 2), "us_512k": round(ts[512] * 1e6, 2),
+                                  "cu_gbps": round((384 << 10) / (ts[512] - ts[128]) / 1e9, 1)}
+    del shr
+    log(f"L2-resident read per CU (by waves per workgroup): {l2}")
     g = graph_of(torch, lambda: [mad.probe_empty(256, 256) for _ in range(64)])
     g.replay()
     t_empty = time_graph(torch, g, reps=3) / 64
@@ -868,6 +882,7 @@ def device_probes(torch, mad):
             "stream_read_by_workgroups": {str(k): round(v / 1e12, 3) for k, v in stream.items()},
             "stream_workload": "nontemporal 16-byte loads, 8 in flight per thread, 256 threads per workgroup, "
                                "256 MiB per launch over four buffers (1 GiB)",
+            "l2_resident_read_per_cu": l2,
             "empty_launch_us": round(t_empty * 1e6, 3), "handoff_latency_ns": lat,
             "shader_clock_ghz": round(float(ghz), 3)}, peak
 

@@ -352,6 +352,11 @@ int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *
  *   range, 8 nontemporal 16-byte loads in flight per thread; the HBM read
  *   bandwidth a plain streaming kernel reaches.  sink: device unsigned, written only if an xor of the data
  *   hits one particular value (keeps the loads), may be NULL.
+ * mad_probe_shared_read: every one of n_workgroups workgroups of `threads`
+ *   threads (a multiple of 64, at most 1024) reads the same `bytes` (a
+ *   multiple of 16; src 16-byte aligned), 16 loads of 16 bytes in flight per
+ *   thread; after the first touch the data is L2-resident, so the launch time
+ *   gives the rate at which one CU reads from L2.  sink as above.
  * mad_probe_empty: an empty kernel of n_workgroups x threads (the launch floor).
  * mad_probe_handoff_latency: one thread times, in shader-clock cycles, `reps`
  *   repetitions (reps >= 2) of: row 0 a plain store until acknowledged; 1 a
@@ -364,6 +369,8 @@ int mad_rmsnorm_swiglu(const void *x, const void *gamma, float eps, const void *
  * Errors: MAD_EINVAL for bad arguments, MAD_EHIP for a failed launch.
  */
 int mad_probe_stream_read(const void *src, size_t bytes, unsigned *sink, int n_workgroups, void *stream);
+int mad_probe_shared_read(const void *src, size_t bytes, unsigned *sink, int n_workgroups, int threads,
+                          void *stream);
 int mad_probe_empty(int n_workgroups, int threads, void *stream);
 int mad_probe_handoff_latency(void *buf, size_t buf_bytes, unsigned long long *cycles, int reps, void *stream);
 

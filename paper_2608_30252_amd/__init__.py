@@ -67,6 +67,7 @@ def _load_library():
     lib.mad_linear_residual.argtypes = [vp, vp, vp, i, i, i, vp, vp]
     lib.mad_rmsnorm_swiglu.argtypes = [vp, vp, f, vp, i, i, i, vp, vp]
     lib.mad_probe_stream_read.argtypes = [vp, sz, vp, i, vp]
+    lib.mad_probe_shared_read.argtypes = [vp, sz, vp, i, i, vp]
     lib.mad_probe_empty.argtypes = [i, i, vp]
     lib.mad_probe_handoff_latency.argtypes = [vp, sz, vp, i, vp]
     lib.mad_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
@@ -77,7 +78,7 @@ def _load_library():
                "mad_accept_stochastic", "mad_draft_step_attn", "mad_draft_decode_attn_noalloc",
                "mad_memory_prefill_attn",
                "mad_rmsnorm_qkv_rope", "mad_linear_residual", "mad_rmsnorm_swiglu", "mad_probe_stream_read",
-               "mad_probe_empty", "mad_probe_handoff_latency"):
+               "mad_probe_shared_read", "mad_probe_empty", "mad_probe_handoff_latency"):
         getattr(lib, fn).restype = ctypes.c_int
     _LIB = lib
     return lib
@@ -550,6 +551,14 @@ def probe_stream_read(src: torch.Tensor, sink: Optional[torch.Tensor] = None, n_
     _need(src.is_contiguous() and src.numel() * src.element_size() % 16 == 0, "src: contiguous, bytes % 16 == 0")
     _check(_load_library().mad_probe_stream_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink),
                                                  n_workgroups, _stream(src.device)))
+
+
+def probe_shared_read(src: torch.Tensor, sink: Optional[torch.Tensor] = None, n_workgroups: int = 256,
+                      threads: int = 256):
+    """Every workgroup reads all bytes of a contiguous device tensor (L2-resident after the first touch)."""
+    _need(src.is_contiguous() and src.numel() * src.element_size() % 16 == 0, "src: contiguous, bytes % 16 == 0")
+    _check(_load_library().mad_probe_shared_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink),
+                                                 n_workgroups, threads, _stream(src.device)))
 
 
 def probe_empty(n_workgroups: int = 256, threads: int = 256, device=None):

@@ -1,7 +1,8 @@
 // probe.hip -- measurement aids for the benchmark (not part of the attention
 // path): the HBM read bandwidth the device reaches with a plain streaming
-// kernel, the cost of an empty launch, and the latency of the memory
-// operations a cross-workgroup hand-off is built from.  The decode kernels'
+// kernel, the rate at which one CU reads L2-resident data, the cost of an
+// empty launch, and the latency of the memory operations a cross-workgroup
+// hand-off is built from.  The decode kernels'
 // fractions of peak are reported against the published 8 TB/s and against the
 // streaming figure measured here.
 #include "mad_device.h"
@@ -28,6 +29,28 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const uint4 *src, size
         }
         #pragma unroll
         for (int i = 0; i < 8; ++i) acc ^= v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+    }
+    if (acc == 0x9e3779b9u && sink) sink[0] = acc;
+}
+
+// Shared read: every workgroup reads the same bytes (16-byte loads into
+// registers, consecutive threads on consecutive 16 bytes, 16 loads in flight
+// per thread).  After the first touch the data is L2-resident, so the time
+// per launch gives the rate at which one CU pulls L2-resident data, by the
+// number of waves of its workgroup.
+__global__ __launch_bounds__(1024) void shared_read_kernel(const uint4 *src, size_t n16, unsigned *sink) {
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    const size_t nt = blockDim.x;
+    uint32_t acc = 0;
+    for (size_t base = threadIdx.x; base < n16; base += 16 * nt) {
+        u4v v[16];
+        #pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const size_t idx = base + (size_t)i * nt;
+            v[i] = idx < n16 ? *reinterpret_cast<const u4v *>(src + idx) : u4v{0u, 0u, 0u, 0u};
+        }
+        #pragma unroll
+        for (int i = 0; i < 16; ++i) acc ^= v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
     }
     if (acc == 0x9e3779b9u && sink) sink[0] = acc;
 }
@@ -71,6 +94,16 @@ int mad_probe_stream_read(const void *src, size_t bytes, unsigned *sink, int n_w
     if (!src || bytes < 16 || bytes % 16 || ((uintptr_t)src & 15u) || n_workgroups < 1) return MAD_EINVAL;
     hipLaunchKernelGGL(mad::stream_read_kernel, dim3((unsigned)n_workgroups), dim3(256), 0, (hipStream_t)stream,
                        reinterpret_cast<const uint4 *>(src), bytes / 16, sink);
+    return hipGetLastError() == hipSuccess ? MAD_OK : MAD_EHIP;
+}
+
+int mad_probe_shared_read(const void *src, size_t bytes, unsigned *sink, int n_workgroups, int threads,
+                          void *stream) {
+    if (!src || bytes < 16 || bytes % 16 || ((uintptr_t)src & 15u) || n_workgroups < 1 || threads < 64 ||
+        threads > 1024 || threads % 64)
+        return MAD_EINVAL;
+    hipLaunchKernelGGL(mad::shared_read_kernel, dim3((unsigned)n_workgroups), dim3((unsigned)threads), 0,
+                       (hipStream_t)stream, reinterpret_cast<const uint4 *>(src), bytes / 16, sink);
     return hipGetLastError() == hipSuccess ? MAD_OK : MAD_EHIP;
 }
 
