@@ -364,6 +364,26 @@ def traffic_from_profile(sources, bytes_default=None):
     return t.get("traffic_bytes_per_launch")
 
 
+def trace_percentiles(sources, kernel="mad::decode_kernel<mad::bf16_t, 64, 4, 1>", grid=192):
+    """The headline kernel's row of the committed rocprofv3 trace summary
+    (per-kernel start/end timestamps, no inter-kernel gaps), if that trace was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "bench_kernel_trace.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    if f"source_sha256: {source_digest(*sources)}" not in text:
+        return None
+    for line in text.splitlines():
+        if not line.startswith(kernel):
+            continue
+        f = line[len(kernel):].split()   # grid, wg, calls, mean, p10, median, p90
+        if len(f) == 7 and int(f[0]) == grid:
+            return {"calls": int(f[2]), "mean_us": float(f[3]), "p10_us": float(f[4]), "median_us": float(f[5]),
+                    "p90_us": float(f[6]), "source": "profiles/bench_kernel_trace.md (rocprofv3 kernel trace)"}
+    return None
+
+
 def main():
     args = parse()
     if args.summarize_trace:
@@ -448,7 +468,8 @@ def main():
                 "kernel": "mad::decode_kernel<bf16_t, 64, 4, 1>", "bytes_per_launch": int(bytes_launch),
                 "mean_launch_us": round(t_launch * 1e6, 3),
                 "frac_of_stream_probe": round(achieved / stream_peak, 4),
-                "stream_probe_gbps": round(stream_peak / 1e9, 1), "launch_distribution": dist}
+                "stream_probe_gbps": round(stream_peak / 1e9, 1), "launch_distribution": dist,
+                "trace_distribution": trace_percentiles(DECODE_SOURCES)}
     del model
     torch.cuda.empty_cache()
 
