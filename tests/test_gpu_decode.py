@@ -170,6 +170,24 @@ def test_ragged_batch_bf16():
     _case(torch.bfloat16, B, 32, 8, 64, mlen, wlen, 544, start, seed=8, mcap=1024)
 
 
+def test_maximum_batch_ragged_bf16():
+    # the largest batch the ABI takes (64 sequences, 512 units), ragged memories and windows,
+    # some sequences with an empty memory or window
+    B = 64
+    rng = np.random.default_rng(64)
+    mlen = rng.integers(0, 201, B).tolist()
+    wlen = rng.integers(0, 121, B).tolist()
+    mlen[0], wlen[1], mlen[2], wlen[2] = 0, 0, 0, 0
+    start = rng.integers(0, 160, B).tolist()
+    _case(torch.bfloat16, B, 32, 8, 64, mlen, wlen, 160, start, seed=64, mcap=200)
+
+
+def test_long_full_kv_reaches_the_split_cap_bf16():
+    # 131072 keys in one sequence: the split plan hits the merge buffer's cap (62 splits of a unit)
+    n = 131071
+    _case(torch.bfloat16, 1, 32, 8, 64, 0, n, n + 65, 40, seed=65, mem=False)
+
+
 def test_batched_sixteen_sequences_bench_configuration():
     # the benchmark's batched launch: 16 sequences x (1024 slots + 511 window + new), 8-wave workgroups
     _case(torch.bfloat16, 16, 32, 8, 64, 1024, 511, 576, [(37 * i) % 64 for i in range(16)], seed=12, mcap=1024)

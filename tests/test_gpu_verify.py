@@ -90,6 +90,18 @@ def test_edge_lengths(layout):
     _check(q, k, v, length, out, lse)
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_maximum_batch(layout):
+    # the largest batch the ABI takes: 64 sequences (128 units, one split each), ragged lengths
+    B, T, Hq, Hkv, d, cap = 64, 5, 8, 2, 64, 320
+    q, k, v = _inputs(B, T, Hq, Hkv, d, cap, seed=47)
+    rng = np.random.default_rng(47)
+    length = rng.integers(T, cap + 1, B).tolist()
+    length[0], length[1] = T, cap
+    out, lse = _run(q, k, v, length, layout)
+    _check(q, k, v, length, out, lse)
+
+
 def test_natural_layout_any_capacity():
     # the natural layout takes any cache capacity (here not a multiple of 8) and odd lengths
     B, T, Hq, Hkv, d, cap = 2, 5, 32, 8, 64, 301
