@@ -200,12 +200,15 @@ int mad_memory_update(const void *x, const void *w_kv, const int32_t *pos, const
  * memory leaves unchanged).  The T = gamma+1 new tokens' K/V are already
  * stored at rows len[b]-T .. len[b]-1; query t sees rows 0 .. len[b]-T+t (the
  * prefix and new tokens 0..t).
- *   q    device [B][T][Hq][d], BF16        out  device [B][T][Hq][d], BF16
+ *   q    device [B][T][Hq][d], dtype     out  device [B][T][Hq][d], dtype
  *   lse  device fp32 [B][T][Hq] or NULL
  *   kv   the verifier's cache as it is: a linear mad_kv_view (start NULL),
  *        K and V rows of d elements, kv->len[b] in [T, cap]
- * T * G <= MAD_MAX_VERIFY_ROWS; d in {64, 128}; dtype BF16 only (both products
- * run on the matrix cores; MAD_ENOTSUP otherwise).  Workspace MAD_OP_VERIFY.
+ * T * G <= MAD_MAX_VERIFY_ROWS; d in {64, 128}.  dtype BF16: both products on
+ * the matrix cores.  dtype F32: on the vector ALUs, one decode-attention launch
+ * per sequence (its T queries as the rows, query t over rows 0 .. len-T+t),
+ * all on `stream` with the same workspace.  Workspace MAD_OP_VERIFY (sized for
+ * both).
  */
 int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
                     const mad_kv_view *kv, void *out, float *lse, void *ws, size_t ws_bytes, void *stream);
@@ -217,7 +220,7 @@ int mad_verify_attn(const void *q, int B, int T, int Hq, int Hkv, int d, int dty
  *   k   device keys, rows of d:      k  + b*seq_stride + h*head_stride + i*d
  *   vt  device values TRANSPOSED:    vt + b*seq_stride + h*head_stride + c*cap + i
  *   len HOST int32[B], T <= len[b] <= cap; cap a multiple of 8
- * Everything else as mad_verify_attn.
+ * dtype BF16 only (MAD_ENOTSUP otherwise).  Everything else as mad_verify_attn.
  */
 int mad_verify_attn_vt(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, float scale,
                        const void *k, const void *vt, int64_t seq_stride, int64_t head_stride,

@@ -330,7 +330,8 @@ int verify_impl(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, 
                 void *out, float *lse, void *ws, size_t ws_bytes, void *stream) {
     int rc = check_heads(B, Hq, Hkv, d, dtype);
     if (rc) return rc;
-    if (dtype != MAD_BF16) return fail(MAD_ENOTSUP, "verify attention runs in bf16 only (matrix cores)");
+    if (dtype != MAD_BF16 && !(dtype == MAD_F32 && vnat))
+        return fail(MAD_ENOTSUP, "the transposed-V verify runs in bf16 only (matrix cores)");
     const int G = Hq / Hkv;
     if (T < 1 || T * G > MAD_MAX_VERIFY_ROWS)
         return fail(MAD_EINVAL, "T=%d: T*G=%d must be in [1, %d]", T, T * G, MAD_MAX_VERIFY_ROWS);
@@ -354,6 +355,31 @@ int verify_impl(const void *q, int B, int T, int Hq, int Hkv, int d, int dtype, 
     if (!ws) return fail(MAD_EWS, "workspace required (%zu bytes)", need);
     if (ws_bytes < need) return fail(MAD_EWS, "workspace %zu bytes < %zu", ws_bytes, need);
     if (!aligned16(ws)) return fail(MAD_EINVAL, "workspace not 16-byte aligned");
+    if (dtype == MAD_F32) {
+        // fp32 (on the vector ALUs): per sequence b, one decode launch whose T rows
+        // are the T queries, all reading b's cache (row stride 0) with query t
+        // limited to rows 0 .. len-T+t; launches on one stream, one workspace
+        const size_t qrow = (size_t)T * Hq * d * 4;
+        for (int b = 0; b < B; ++b) {
+            int32_t lens[MAD_MAX_BATCH];
+            for (int t = 0; t < T; ++t) lens[t] = len[b] - T + t + 1;
+            mad_kv_view kv;
+            memset(&kv, 0, sizeof(kv));
+            kv.k = (char *)k + (size_t)b * seq_stride * 4;
+            kv.v = (char *)v + (size_t)b * seq_stride * 4;
+            kv.seq_stride = 0;
+            kv.head_stride = head_stride;
+            kv.cap = cap;
+            kv.start = nullptr;
+            kv.len = lens;
+            unsigned char mode[MAD_MAX_BATCH] = {0};
+            rc = decode_impl((const char *)q + b * qrow, T, Hq, Hkv, d, MAD_F32, scale, &kv, nullptr, nullptr,
+                             nullptr, mode, (char *)out + b * qrow, lse ? lse + (size_t)b * T * Hq : nullptr, ws,
+                             ws_bytes, stream);
+            if (rc) return rc;
+        }
+        return MAD_OK;
+    }
     mad::VerifyPlan p = mad::plan_verify(B, Hkv, G, T, len, vnat);
     mad::VerifyArgs a;
     memset(&a, 0, sizeof(a));

@@ -614,7 +614,10 @@ size_t verify_ws_bytes(int B, int Hq, int Hkv, int d, int T) {
     const size_t units = (size_t)B * Hkv;
     const size_t rows = (size_t)T * (Hq / Hkv);
     const size_t ns = (size_t)verify_max_splits((int)units);
-    return kCounterRegionBytes + align256(units * ns * rows * d * 4) + align256(units * ns * rows * 2 * 4);
+    const size_t bf = kCounterRegionBytes + align256(units * ns * rows * d * 4) + align256(units * ns * rows * 2 * 4);
+    // fp32 verify runs the decode kernel once per sequence, its T query rows as the rows
+    const size_t f32 = decode_ws_bytes(T, Hq, Hkv, d);
+    return bf > f32 ? bf : f32;
 }
 
 void verify_ws_layout(int B, int Hq, int Hkv, int d, int T, size_t *off_o, size_t *off_ml) {

@@ -137,7 +137,8 @@ def test_verify_and_accept_validation(mad):
     assert vnat() == mad.MAD_EWS                                     # cap 100 is fine here; workspace missing
     assert vnat(kv=False) == mad.MAD_EINVAL
     assert vnat(start=(ctypes.c_int32 * 1)(0)) == mad.MAD_EINVAL     # the verifier's cache is linear
-    assert vnat(dtype=mad.MAD_F32) == mad.MAD_ENOTSUP
+    assert vnat(dtype=mad.MAD_F32) == mad.MAD_EWS                    # fp32 runs (vector ALUs); workspace missing
+    assert vnat(dtype=7) == mad.MAD_ENOTSUP
     assert vnat(ln_=(ctypes.c_int32 * 1)(101)) == mad.MAD_EINVAL     # len > cap
     assert vnat(head=64) == mad.MAD_EINVAL
     acc = lambda B=1, T=5, V=128256, dtype=mad.MAD_F32, draft=1 << 21: lib.mad_accept_greedy(

@@ -51,7 +51,7 @@ def _check(q, k, v, length, out, lse, targets=None):
                 if bb == b:
                     w = np.exp(d ** -0.5 * float(qb[0, t, h] @ kb[0, h // (Hq // k.shape[1]), j]) - lse_ref[0, t, h])
                     assert w >= 0.9, f"peaky query ({b}, {t}, {h}): target weight {w:.3f}"
-        check_out(to_np(out[b:b + 1]), o_ref, True, f"out b{b}")
+        check_out(to_np(out[b:b + 1]), o_ref, out.dtype == torch.bfloat16, f"out b{b}")
         check_lse(to_np(lse[b:b + 1]), lse_ref, abs_score_verify(qb, kb, [length[b]], d ** -0.5), d, f"lse b{b}")
 
 
@@ -99,6 +99,21 @@ def test_maximum_batch(layout):
     length = rng.integers(T, cap + 1, B).tolist()
     length[0], length[1] = T, cap
     out, lse = _run(q, k, v, length, layout)
+    _check(q, k, v, length, out, lse)
+
+
+@pytest.mark.parametrize("B,T,Hq,Hkv,d,cap", [(3, 5, 8, 2, 64, 300), (2, 4, 16, 1, 128, 133), (1, 1, 4, 4, 64, 40)])
+def test_fp32_natural_layout(B, T, Hq, Hkv, d, cap):
+    # fp32 verify (vector ALUs): every sequence against the oracle at the fp32 bar
+    from paper_2608_30252_amd import synth
+    s = 1000 * (48 + d + T)
+    q = synth.normal((B, T, Hq, d), s + 1, dtype=torch.float32)
+    k = synth.normal((B, Hkv, cap, d), s + 2, dtype=torch.float32)
+    v = synth.normal((B, Hkv, cap, d), s + 3, dtype=torch.float32)
+    length = [cap - 7 * b for b in range(B)]
+    length[-1] = max(T, length[-1] // 2)
+    out, lse = _run(q, k, v, length, "natural")
+    assert out.dtype == torch.float32
     _check(q, k, v, length, out, lse)
 
 
