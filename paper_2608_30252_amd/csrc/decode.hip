@@ -236,8 +236,9 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int units = a.units;
     const int u = blockIdx.x % units, s = a.n_splits - 1 - (int)(blockIdx.x / units);
     const int b = u / a.Hkv, c = u - b * a.Hkv;
-    const int mlen = a.mlen[b], wlen = a.wlen[b], wst = a.wstart[b];
-    const int nmode = a.kn != nullptr ? a.nmode[b] : 0;
+    const int4 sq = a.seq[b];
+    const int mlen = sq.x, wlen = sq.y, wst = sq.z;
+    const int nmode = a.kn != nullptr ? sq.w : 0;
     const bool has_new = nmode >= 1;      // the key sequence ends with the current token
     const bool appends = nmode == 2;      // ... which this row also writes into its ring
     const int n = mlen + wlen + (has_new ? 1 : 0);

@@ -141,11 +141,11 @@ int decode_impl(const void *q, int B, int Hq, int Hkv, int d, int dtype, float s
     memset(&a, 0, sizeof(a));
     int n_keys[MAD_MAX_BATCH];
     for (int b = 0; b < B; ++b) {
-        a.mlen[b] = mem ? mem->len[b] : 0;
-        a.wlen[b] = win ? win->len[b] : 0;
-        a.wstart[b] = (win && win->start) ? win->start[b] : 0;
-        n_keys[b] = a.mlen[b] + a.wlen[b] + (mode[b] ? 1 : 0);
-        a.nmode[b] = mode[b];
+        a.seq[b].x = mem ? mem->len[b] : 0;
+        a.seq[b].y = win ? win->len[b] : 0;
+        a.seq[b].z = (win && win->start) ? win->start[b] : 0;
+        a.seq[b].w = mode[b];
+        n_keys[b] = a.seq[b].x + a.seq[b].y + (mode[b] ? 1 : 0);
     }
     mad::DecodePlan p = mad::plan_decode(B, Hkv, G, d, dtype, n_keys);
     size_t need = p.n_splits > 1 ? mad::decode_ws_bytes(B, Hq, Hkv, d) : 0;

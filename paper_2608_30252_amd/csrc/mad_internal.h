@@ -40,8 +40,9 @@ struct DecodeArgs {
     float scale_log2;     // softmax scale * log2(e)
     int Hq, Hkv, units, n_splits, chunk, w_cap;
     int nsub;             // wave groups per workgroup (1 or 2)
-    int mlen[kMaxB], wstart[kMaxB], wlen[kMaxB];
-    unsigned char nmode[kMaxB];   // per row: 0 no new token, 1 attend it, 2 attend and append it
+    // per row, one 16-byte record read by a single scalar load: memory length,
+    // window length, ring start, new-token mode (0 none, 1 attend, 2 attend and append)
+    int4 seq[kMaxB];
 };
 
 struct DecodePlan {
