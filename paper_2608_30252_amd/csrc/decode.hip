@@ -9,11 +9,13 @@
 // current token) or left out, so one launch serves a raw query and the write
 // scopes of the slots made in the same pass.
 //
-// Work decomposition (split-K / flash-decoding), grid = n_splits * units
-// workgroups, units = B * Hkv; workgroup w handles unit u = w % units and key
-// range s = n_splits - 1 - w / units (the short last range, which holds the
-// new token, is dispatched first).  With units a multiple of 8 every split of
-// a unit runs on one XCD (workgroups are dealt to the 8 XCDs round-robin).
+// Work decomposition (split-K / flash-decoding): a (Hkv, B, n_splits) grid,
+// so workgroup (c, b, z) reads its row's record without first loading any
+// other argument.  It handles unit u = b * Hkv + c of the units = B * Hkv and
+// key range s = n_splits - 1 - z (the short last range, which holds the new
+// token, is dispatched first).  Workgroups are dealt to the 8 XCDs
+// round-robin by their linear id z * units + u, so with units a multiple of 8
+// every split of a unit runs on one XCD.
 //
 // A workgroup is NSUB groups of four waves.  Keys stream through LDS in
 // super-tiles of NSUB tiles, a tile being 8 KB of K + 8 KB of V (64 keys for
@@ -233,9 +235,10 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int grp = wave >> 2, wq = wave & 3;   // wave group (tile of the super-tile), wave in group
-    const int units = a.units;
-    const int u = blockIdx.x % units, s = a.n_splits - 1 - (int)(blockIdx.x / units);
-    const int b = u / a.Hkv, c = u - b * a.Hkv;
+    // grid (KV head, row, split): the row's record is read without waiting for any
+    // other argument; the last split (the one holding the new token) is dispatched first
+    const int c = blockIdx.x, b = blockIdx.y;
+    const int u = b * (int)gridDim.x + c, s = (int)gridDim.z - 1 - (int)blockIdx.z;
     const int4 sq = a.seq[b];
     const int mlen = sq.x, wlen = sq.y, wst = sq.z;
     const int nmode = a.kn != nullptr ? sq.w : 0;
@@ -636,7 +639,7 @@ size_t decode_ws_bytes(int B, int Hq, int Hkv, int d) {
 template <typename T, int D, int G, int NSUB>
 static hipError_t launch_t(const DecodeArgs &a, hipStream_t st) {
     using C = DecodeCfg<T, D, G, NSUB>;
-    dim3 grid((unsigned)(a.units * a.n_splits)), block(C::NT);
+    dim3 grid((unsigned)a.Hkv, (unsigned)(a.units / a.Hkv), (unsigned)a.n_splits), block(C::NT);
     hipLaunchKernelGGL((decode_kernel<T, D, G, NSUB>), grid, block, C::SMEM, st, a);
     return hipGetLastError();
 }
