@@ -21,7 +21,9 @@
 // partials, no merge and no workspace.  The tile's 32 input rows go through
 // LDS: a CU pulls them from L2 fastest as whole 1-KB row pieces per wave load
 // with many waves in flight, which the MFMA operand layout (16 rows per load)
-// does not give.
+// does not give; when the whole width fits LDS at once they are loaded
+// straight into it (global_load_lds_dwordx4) and the products follow them
+// block by block.
 // F32: a vector-ALU kernel, one thread per (row, rotation pair).
 #include "mad_device.h"
 #include "mad_internal.h"
@@ -40,14 +42,18 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 // bytes; rows padded by 16 bytes so the operand reads below are free of bank
 // conflicts); wave w then runs the 32-wide k-steps w, w + NW, ... of the round
 // from LDS in the MFMA register layout (lane l: row / feature l % 16, k chunk
-// l / 16), and the NW partial tiles are summed through LDS.  The next round's
-// loads are issued before this round's MFMAs.  The row tiles of one feature
+// l / 16), and the NW partial tiles are summed through LDS.  An input width of
+// at most one round (DIRECT) is loaded straight into LDS by 512-column block
+// and each block's k-steps start as soon as it has landed; wider inputs go
+// through registers, the next round's loads issued before this round's
+// MFMAs.  Both run the k-steps of a wave in the same order (bit-identical
+// results).  The row tiles of one feature
 // block are dealt to one XCD (workgroups go round-robin over the 8 XCDs, so
 // blockIdx mod 8 is kept), where they share its weight rows in L2; the order
 // affects only where data is cached, never the result.  The RoPE angles and
 // the epilogue's kernel arguments are taken at entry, while the rows are in
 // flight, and each tile row leaves as two 16-byte stores.
-template <int NW>
+template <int NW, bool DIRECT>
 __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a) {
     constexpr int KR = 2048, PITCH = 2 * KR + 16, PIECES = 32 * KR / 512, PW = PIECES / NW;
     static_assert(PIECES % NW == 0, "whole pieces per wave");
@@ -70,41 +76,73 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     const int s_row = rt * 16 + ((tid >> 1) & 15), s_b = min(s_row, R - 1) / a.n_new;
     const int s_fire = a.fire[s_b], s_mlen = a.mlen[s_b];
 
-    // piece pc = wave + NW i: row pc / 4, columns 512 (pc % 4) .. + 511 of the round
     const bf16_t *w = reinterpret_cast<const bf16_t *>(a.w);
     const bf16_t *x = reinterpret_cast<const bf16_t *>(a.x);
-    const bf16_t *src[PW];
-    #pragma unroll
-    for (int i = 0; i < PW; ++i) {
-        const int row = (wave + NW * i) >> 2;
-        src[i] = row < 16 ? w + (size_t)(hb * d + (row < 8 ? j0 + row : hd + j0 + row - 8)) * D
-                          : x + (size_t)min(rt * 16 + row - 16, R - 1) * D;
-    }
-    uint4 buf[PW];
-    auto load = [&](int r0) {
-        #pragma unroll
-        for (int i = 0; i < PW; ++i) {
-            const int col = r0 + ((wave + NW * i) & 3) * 512 + lane * 8;
-            buf[i] = col < D ? *reinterpret_cast<const uint4 *>(src[i] + col) : make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
     f32x4_v acc = f32x4_v{0.f, 0.f, 0.f, 0.f};
-    load(0);
-    for (int r0 = 0; r0 < D; r0 += KR) {
+    if constexpr (DIRECT) {
+        // one round (D <= KR): the pieces go straight from memory into LDS
+        // (global_load_lds_dwordx4: no VGPR hop, no LDS write instructions),
+        // issued by 512-column block -- wave w loads block b of rows w and
+        // w + 16 as its loads 2b and 2b + 1 -- so the products of block b start
+        // while the later blocks are still arriving.  Lanes past D load the
+        // row's last chunk again (never read) so every wave issues all PW loads
+        // and the counted waits hold.
+        static_assert(PW == 8 && NW == 16, "two rows x four column blocks per wave");
         #pragma unroll
         for (int i = 0; i < PW; ++i) {
-            const int pc = wave + NW * i;
-            *reinterpret_cast<uint4 *>(s_rows + (pc >> 2) * PITCH + (pc & 3) * 1024 + lane * 16) = buf[i];
+            const int row = wave + 16 * (i & 1), cb = i >> 1;
+            const bf16_t *rp = row < 16 ? w + (size_t)(hb * d + (row < 8 ? j0 + row : hd + j0 + row - 8)) * D
+                                        : x + (size_t)min(rt * 16 + row - 16, R - 1) * D;
+            lds_stream16(rp + min(cb * 512 + lane * 8, D - 8), s_rows + row * PITCH + cb * 1024);
         }
-        __syncthreads();
-        if (r0 + KR < D) load(r0 + KR);
-        const int nst = min(KR, D - r0) >> 5;
-        for (int t = wave; t < nst; t += NW) {
-            const bf16x8_v bv = *reinterpret_cast<const bf16x8_v *>(s_rows + c * PITCH + t * 64 + kq * 16);
-            const bf16x8_v av = *reinterpret_cast<const bf16x8_v *>(s_rows + (16 + c) * PITCH + t * 64 + kq * 16);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+        const int nst = D >> 5;
+        #pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            wait_vm(PW - 2 * (cb + 1));   // this wave's loads of blocks 0 .. cb have landed
+            __syncthreads();              // ... every wave's
+            const int t = cb * NW + wave;
+            if (t < nst) {
+                const bf16x8_v bv = *reinterpret_cast<const bf16x8_v *>(s_rows + c * PITCH + t * 64 + kq * 16);
+                const bf16x8_v av = *reinterpret_cast<const bf16x8_v *>(s_rows + (16 + c) * PITCH + t * 64 + kq * 16);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+            }
         }
-        __syncthreads();
+    } else {
+        // piece pc = wave + NW i: row pc / 4, columns 512 (pc % 4) .. + 511 of
+        // the round, through registers so the next round's loads overlap this
+        // round's products
+        const bf16_t *src[PW];
+        #pragma unroll
+        for (int i = 0; i < PW; ++i) {
+            const int row = (wave + NW * i) >> 2;
+            src[i] = row < 16 ? w + (size_t)(hb * d + (row < 8 ? j0 + row : hd + j0 + row - 8)) * D
+                              : x + (size_t)min(rt * 16 + row - 16, R - 1) * D;
+        }
+        uint4 buf[PW];
+        auto load = [&](int r0) {
+            #pragma unroll
+            for (int i = 0; i < PW; ++i) {
+                const int col = r0 + ((wave + NW * i) & 3) * 512 + lane * 8;
+                buf[i] = col < D ? *reinterpret_cast<const uint4 *>(src[i] + col) : make_uint4(0u, 0u, 0u, 0u);
+            }
+        };
+        load(0);
+        for (int r0 = 0; r0 < D; r0 += KR) {
+            #pragma unroll
+            for (int i = 0; i < PW; ++i) {
+                const int pc = wave + NW * i;
+                *reinterpret_cast<uint4 *>(s_rows + (pc >> 2) * PITCH + (pc & 3) * 1024 + lane * 16) = buf[i];
+            }
+            __syncthreads();
+            if (r0 + KR < D) load(r0 + KR);
+            const int nst = min(KR, D - r0) >> 5;
+            for (int t = wave; t < nst; t += NW) {
+                const bf16x8_v bv = *reinterpret_cast<const bf16x8_v *>(s_rows + c * PITCH + t * 64 + kq * 16);
+                const bf16x8_v av = *reinterpret_cast<const bf16x8_v *>(s_rows + (16 + c) * PITCH + t * 64 + kq * 16);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+            }
+            __syncthreads();
+        }
     }
     // lane l holds Y[row 4 (l / 16) + e][column l % 16], e < 4
     s_acc[wave][lane] = acc;
@@ -266,10 +304,15 @@ hipError_t launch_update(const UpdateArgs &a, int dtype, hipStream_t st) {
     }
     if (dtype == MAD_BF16) {
         // sixteen waves: eight 1-KB row pieces of each in flight per round
-        // (measured at 64 rows, D 2048: 5.6 us, against 5.8 with eight waves
-        // and 7.4 for loads straight into the MFMA layout)
+        // (measured at 64 rows, D 2048, through registers: 5.6 us, against
+        // 5.8 with eight waves and 7.4 for loads straight into the MFMA
+        // layout; straight into LDS by column block: 5.3 us)
         const int RT = (a.R + 15) / 16;
-        hipLaunchKernelGGL((update_rows_kernel<16>), dim3((unsigned)(2 * a.Hkv * a.d / 16 * RT)), dim3(1024), 0, st, a);
+        const dim3 grid((unsigned)(2 * a.Hkv * a.d / 16 * RT));
+        if (a.D <= 2048)
+            hipLaunchKernelGGL((update_rows_kernel<16, true>), grid, dim3(1024), 0, st, a);
+        else
+            hipLaunchKernelGGL((update_rows_kernel<16, false>), grid, dim3(1024), 0, st, a);
     } else {
         const int total = a.R * 2 * a.Hkv * (a.d / 2);
         dim3 grid((unsigned)((total + 255) / 256)), block(256);
