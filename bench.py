@@ -192,12 +192,18 @@ def summarize_trace(path):
             if "mad::" not in name:
                 continue
             short = name.split("(")[0].replace("void ", "")
-            key = (short, int(row["Grid_Size_X"]), int(row["Workgroup_Size_X"]))
+            # workgroups over all three grid dimensions (the sizes are in work-items)
+            ext = [(int(row.get(f"Grid_Size_{a}") or 1), int(row.get(f"Workgroup_Size_{a}") or 1)) for a in "XYZ"]
+            wgs, wg = 1, 1
+            for g, w in ext:
+                wgs *= g // w
+                wg *= w
+            key = (short, wgs, wg)
             groups.setdefault(key, []).append((int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3)
     print(f"{'kernel':48s} {'grid':>8s} {'wg':>5s} {'calls':>6s} {'mean_us':>8s} {'p10':>8s} {'median':>8s} {'p90':>8s}")
-    for (short, grid, wg), d in sorted(groups.items()):
+    for (short, wgs, wg), d in sorted(groups.items()):
         d.sort()
-        print(f"{short:48s} {grid // wg:8d} {wg:5d} {len(d):6d} {sum(d) / len(d):8.2f} {d[len(d) // 10]:8.2f} "
+        print(f"{short:48s} {wgs:8d} {wg:5d} {len(d):6d} {sum(d) / len(d):8.2f} {d[len(d) // 10]:8.2f} "
               f"{statistics.median(d):8.2f} {d[9 * len(d) // 10]:8.2f}")
 
 
