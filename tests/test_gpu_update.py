@@ -122,10 +122,14 @@ def test_duplicate_position_gives_identical_keys():
     assert torch.equal(mv[0, :, 0].view(torch.int16), mv[0, :, 1].view(torch.int16))
 
 
-@pytest.mark.parametrize("D,Hkv,d", [(192, 2, 64), (4096, 8, 64), (6144, 4, 128)])
+@pytest.mark.parametrize("D,Hkv,d", [(192, 2, 64), (640, 4, 64), (1536, 8, 64), (4096, 8, 64), (6144, 4, 128)])
 def test_matrix_core_kernel_input_widths(D, Hkv, d):
-    # the matrix-core kernel's k loop: an odd number of 32-wide steps (D 192: waves 0-1 take two, 2-3 one),
-    # two and three batches of steps per wave; 18 rows leave a 2-row second tile
+    # the matrix-core kernel's k loop.  Widths up to 2048 load straight into LDS
+    # by 512-column block: D 192 is a part of the first block (six 32-wide
+    # steps, so waves 6-15 take none), 640 a whole block and a part of the
+    # second, 1536 three whole blocks and an empty fourth (its loads clamped to
+    # the row's last chunk, never read).  4096 and 6144 go through registers in
+    # two and three rounds.  18 rows leave a 2-row second tile
     rng = np.random.default_rng(D)
     pos = [[int(p) + 16 * i for i in range(6)] for p in rng.integers(100, 60000, 3)]
     _case(torch.bfloat16, 3, 6, D, Hkv, d, [5, 0, 17], 32, pos, fire=[1, 1, 0], seed=30 + D // 64)
