@@ -1,6 +1,7 @@
 """Build libmad.so (HIP, gfx950) in-tree.
 
-    python -m paper_2608_30252_amd.build
+    python -m paper_2608_30252_amd.build            # the library
+    python -m paper_2608_30252_amd.build --trace    # + libmad_trace.so, the diagnostic phase-trace build
 
 Every translation unit in csrc/ is compiled by hipcc for gfx950 only and
 linked into paper_2608_30252_amd/libmad.so.  Packed-fp32 instructions are
@@ -16,6 +17,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmad.so")
 BUILD_DIR = os.path.join(HERE, "_build")
+# the same sources with the kernels' phase marks compiled in (MAD_PHASE_TRACE):
+# read by paper_2608_30252_amd/phase_trace.py, never by the product path
+TRACE_LIB = os.path.join(HERE, "libmad_trace.so")
+TRACE_BUILD_DIR = os.path.join(HERE, "_build", "trace")
 
 ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -32,11 +37,12 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR) -> str:
+def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR, defines=()) -> str:
     os.makedirs(build_dir, exist_ok=True)
     cc = hipcc()
     common = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
-              "-Wno-unused-function", "-I", os.path.join(HERE, "..", "include")] + DEVICE_FLAGS
+              "-Wno-unused-function", "-I", os.path.join(HERE, "..", "include")] + DEVICE_FLAGS + \
+             [f"-D{d}" for d in defines]
 
     def compile_one(src):
         obj = os.path.join(build_dir, os.path.basename(src) + ".o")
@@ -62,6 +68,13 @@ def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR) -> 
     return out
 
 
+def build_trace(verbose: bool = False) -> str:
+    return build(verbose, out=TRACE_LIB, build_dir=TRACE_BUILD_DIR, defines=("MAD_PHASE_TRACE",))
+
+
 if __name__ == "__main__":
     build(verbose="-v" in sys.argv)
     print(LIB)
+    if "--trace" in sys.argv:
+        build_trace(verbose="-v" in sys.argv)
+        print(TRACE_LIB)

@@ -47,6 +47,11 @@
 
 namespace mad {
 
+// phase marks of the diagnostic trace build: 0 entry, 1 partial stored and
+// acknowledged, 2 arrival counter returned, 3 (merging workgroup) partials in
+// LDS, 4 its first head merged, 5 merge done
+MAD_TRACE_BUFFER(mad_trace_decode)
+
 constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
 constexpr int kMergeLds = 65536;    // LDS that holds a unit's split partials in the merge
 
@@ -155,6 +160,7 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
     }
     wait_vm(0);
     __syncthreads();
+    MAD_TRACE(mad_trace_decode, 3);
     const float *lo = reinterpret_cast<const float *>(lds);                               // [n_splits][G][D]
     const float2 *lml = reinterpret_cast<const float2 *>(lo + (size_t)n_splits * G * D);  // [n_splits][G]
 
@@ -216,6 +222,7 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
         float accs[FPL];
         #pragma unroll
         for (int f = 0; f < FPL; ++f) accs[f] = (acc[0][f] + acc[1][f]) + (acc[2][f] + acc[3][f]);
+        if (g == 0) MAD_TRACE(mad_trace_decode, 4);
         T *og_out = out + (size_t)g * D + lane * FPL;
         if constexpr (std::is_same<T, bf16_t>::value && FPL == 2) {
             *reinterpret_cast<uint32_t *>(og_out) = pack_bf16x2(accs[0] * inv, accs[1] * inv);
@@ -231,6 +238,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     using C = DecodeCfg<T, D, G, NSUB>;
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *sStage = smem;
+    MAD_TRACE_T0();
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -249,6 +257,19 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int k1 = min(n, k0 + a.chunk);
     const int w_cap = a.w_cap;
 
+    // the unit's arrival counter, taken at entry and kept in SGPRs (the empty
+    // asm): not re-read from the arguments between a split's last partial
+    // store and its arrival.  Through the asm the pointer loses its address
+    // space, so the arrival becomes a flat atomic (same agent-scope semantics)
+    // without the compiler's wave-reduction wrapper around a one-lane atomic:
+    // 7.09 -> 7.00 us on the compact layer, where keeping it a global atomic
+    // gained nothing.  With 8 or more query heads per KV head the kernel has
+    // no SGPRs to spare for it.
+    uint64_t cnt_addr = 0;
+    if constexpr (G <= 4) {
+        cnt_addr = (uint64_t)(uintptr_t)(a.counters + (size_t)u * kCounterStride);
+        asm volatile("" : "+s"(cnt_addr));
+    }
     const T *mk = reinterpret_cast<const T *>(a.mk) + b * a.m_seq + c * a.m_head;
     const T *mv = reinterpret_cast<const T *>(a.mv) + b * a.m_seq + c * a.m_head;
     T *wk = reinterpret_cast<T *>(a.wk) + b * a.w_seq + c * a.w_head;
@@ -554,16 +575,22 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     // every head g < G belongs to exactly one active wave: the block is complete
     wait_vm_stores();
     __syncthreads();
+    MAD_TRACE_VAR(t_arrive);
+    MAD_TRACE_SET(t_arrive);   // stored after the atomic, whose wait would count the store
     __shared__ int s_last;
     if (tid == 0) {
-        unsigned *cnt = a.counters + (size_t)u * kCounterStride;
+        unsigned *cnt = G <= 4 ? reinterpret_cast<unsigned *>((uintptr_t)cnt_addr) : a.counters + (size_t)u * kCounterStride;
         const int last = arrive(cnt) == (unsigned)(n_splits - 1);
+        MAD_TRACE(mad_trace_decode, 2);
+        MAD_TRACE_SAVE_T0(mad_trace_decode);
+        MAD_TRACE_PUT(mad_trace_decode, 1, t_arrive);
         if (last) reset_counter(cnt);
         s_last = last;
     }
     __syncthreads();
     if (!s_last) return;
     merge_splits<T, D, G, C::NT>(blk, n_splits, sStage, out, a.lse ? a.lse + head0 : nullptr);
+    MAD_TRACE(mad_trace_decode, 5);
 }
 
 // ------------------------------------------------------------------ host ----

@@ -303,4 +303,68 @@ __device__ __forceinline__ void lds_load16_coherent(const void *src, void *lds_b
     __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0, 16);
 }
 
+// ---- phase trace: a diagnostic build only (-DMAD_PHASE_TRACE, libmad_trace.so) ----
+// Thread 0 of a workgroup records the device's 100 MHz constant counter
+// (s_memrealtime) at named phases of a kernel in a per-file device array of
+// kTraceSlots words per workgroup (linear workgroup id), and in the last word
+// its XCC id (high half) and hardware id register (low half).  One vector store
+// per mark.  The counter has its own origin on each XCD, so only marks taken on
+// one XCD compare.  In the product library the marks compile to nothing.
+constexpr int kTraceSlots = 8, kTraceWGs = 4096;
+#ifdef MAD_PHASE_TRACE
+__device__ __forceinline__ unsigned trace_block() {
+    return blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+}
+__device__ __forceinline__ void trace_mark(unsigned long long *buf, int slot) {
+    const unsigned b = trace_block();
+    if (threadIdx.x == 0 && b < (unsigned)kTraceWGs) buf[kTraceSlots * b + slot] = __builtin_amdgcn_s_memrealtime();
+}
+__device__ __forceinline__ void trace_ids(unsigned long long *buf) {
+    const unsigned b = trace_block();
+    if (threadIdx.x == 0 && b < (unsigned)kTraceWGs) {
+        const unsigned hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);    // HW_ID
+        const unsigned xcc = __builtin_amdgcn_s_getreg((3 << 11) | 20);   // XCC_ID
+        buf[kTraceSlots * b + kTraceSlots - 1] = ((unsigned long long)xcc << 32) | hw;
+    }
+}
+#define MAD_TRACE_BUFFER(NAME)                                                                          \
+    __device__ unsigned long long NAME[kTraceSlots * kTraceWGs];                                        \
+    extern "C" int NAME##_read(void *host, size_t bytes) {                                              \
+        if (bytes > sizeof(NAME)) return -1;                                                            \
+        return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(NAME), bytes, 0, hipMemcpyDeviceToHost);       \
+    }                                                                                                   \
+    extern "C" int NAME##_clear(void) {                                                                 \
+        static const unsigned long long zero[kTraceSlots * kTraceWGs] = {};                            \
+        return (int)hipMemcpyToSymbol(HIP_SYMBOL(NAME), zero, sizeof(zero), 0, hipMemcpyHostToDevice);  \
+    }
+// MAD_TRACE_T0 reads the counter at kernel entry into a register;
+// MAD_TRACE_SAVE_T0 stores it (slot 0) with the ids at a later point, so the
+// entry itself gains no store
+#define MAD_TRACE_T0() const unsigned long long mad_trace_t0 = __builtin_amdgcn_s_memrealtime()
+#define MAD_TRACE_SAVE_T0(NAME)                                                        \
+    do {                                                                               \
+        const unsigned b_ = trace_block();                                             \
+        if (threadIdx.x == 0 && b_ < (unsigned)kTraceWGs) NAME[kTraceSlots * b_] = mad_trace_t0; \
+        trace_ids(NAME);                                                               \
+    } while (0)
+#define MAD_TRACE(NAME, SLOT) trace_mark(NAME, SLOT)
+// a mark read now and stored later (MAD_TRACE_PUT), where a store would be
+// counted by a wait that follows it (vmcnt counts stores as well as loads)
+#define MAD_TRACE_VAR(VAR) unsigned long long VAR = 0
+#define MAD_TRACE_SET(VAR) (VAR = __builtin_amdgcn_s_memrealtime())
+#define MAD_TRACE_PUT(NAME, SLOT, VAR)                                                 \
+    do {                                                                               \
+        const unsigned b_ = trace_block();                                             \
+        if (threadIdx.x == 0 && b_ < (unsigned)kTraceWGs) NAME[kTraceSlots * b_ + (SLOT)] = (VAR); \
+    } while (0)
+#else
+#define MAD_TRACE_BUFFER(NAME)
+#define MAD_TRACE_T0() ((void)0)
+#define MAD_TRACE_SAVE_T0(NAME) ((void)0)
+#define MAD_TRACE(NAME, SLOT) ((void)0)
+#define MAD_TRACE_VAR(VAR) ((void)0)
+#define MAD_TRACE_SET(VAR) ((void)0)
+#define MAD_TRACE_PUT(NAME, SLOT, VAR) ((void)0)
+#endif
+
 }  // namespace mad

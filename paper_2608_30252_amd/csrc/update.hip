@@ -30,6 +30,10 @@
 
 namespace mad {
 
+// phase marks of the diagnostic trace build (update_rows_kernel): 0 entry,
+// 1 the first rows in LDS, 2 products done, 3 stored
+MAD_TRACE_BUFFER(mad_trace_update)
+
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
 
@@ -60,6 +64,8 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     __shared__ __attribute__((aligned(16))) unsigned char s_rows[32 * PITCH];   // rows 0-15: W, 16-31: X
     __shared__ f32x4_v s_acc[NW][64];
     __shared__ __attribute__((aligned(16))) uint16_t s_out[16][16];   // [tile row][pair | pair + 8]
+    MAD_TRACE_T0();
+    MAD_TRACE_VAR(t_rows);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int R = a.R, D = a.D, d = a.d, hd = d / 2;
     const int RT = (R + 15) >> 4;
@@ -100,6 +106,7 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
         for (int cb = 0; cb < 4; ++cb) {
             wait_vm(PW - 2 * (cb + 1));   // this wave's loads of blocks 0 .. cb have landed
             __syncthreads();              // ... every wave's
+            if (cb == 0) MAD_TRACE_SET(t_rows);
             const int t = cb * NW + wave;
             if (t < nst) {
                 const bf16x8_v bv = *reinterpret_cast<const bf16x8_v *>(s_rows + c * PITCH + t * 64 + kq * 16);
@@ -134,6 +141,7 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
                 *reinterpret_cast<uint4 *>(s_rows + (pc >> 2) * PITCH + (pc & 3) * 1024 + lane * 16) = buf[i];
             }
             __syncthreads();
+            if (r0 == 0) MAD_TRACE_SET(t_rows);
             if (r0 + KR < D) load(r0 + KR);
             const int nst = min(KR, D - r0) >> 5;
             for (int t = wave; t < nst; t += NW) {
@@ -144,6 +152,8 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
             __syncthreads();
         }
     }
+    MAD_TRACE_VAR(t_prod);
+    MAD_TRACE_SET(t_prod);
     // lane l holds Y[row 4 (l / 16) + e][column l % 16], e < 4
     s_acc[wave][lane] = acc;
     __syncthreads();
@@ -166,6 +176,11 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
                       (size_t)s_b * a.m_seq + (size_t)(s_mlen + i) * d + h * hd + j0;
         *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(&s_out[tid >> 1][8 * h]);
     }
+    // the marks are stored only now: a store earlier would be counted by the row loads' waits
+    MAD_TRACE_SAVE_T0(mad_trace_update);
+    MAD_TRACE_PUT(mad_trace_update, 1, t_rows);
+    MAD_TRACE_PUT(mad_trace_update, 2, t_prod);
+    MAD_TRACE(mad_trace_update, 3);
 }
 
 template <int RR, int NC, int KD>

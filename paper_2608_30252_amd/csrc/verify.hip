@@ -31,6 +31,10 @@
 
 namespace mad {
 
+// phase marks of the diagnostic trace build (verify_lds_kernel): 0 entry,
+// 1 the split's partial written
+MAD_TRACE_BUFFER(mad_trace_verify)
+
 constexpr int kVerifyLdsMinNb = 2;   // query row blocks from which the LDS-staged kernel is used
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
@@ -313,6 +317,7 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
     using C = VerifyLdsCfg<D>;
     constexpr int KST = D / 32, DB = D / 16, CPR = D / 8;
     extern __shared__ __align__(16) unsigned char smem[];
+    MAD_TRACE_T0();
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.x % a.units, s = blockIdx.x / a.units;
@@ -499,6 +504,7 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
         }
     }
     __syncthreads();
+    MAD_TRACE_SAVE_T0(mad_trace_verify);   // the workgroup's partial is written below; thread 0 marks it
     if (!active || kh == 1 || row >= R) return;
     const float m1 = xml[2 * row], l1 = xml[2 * row + 1];
     const float M = fmaxf(msc, m1);
@@ -521,6 +527,7 @@ __global__ __launch_bounds__(512, 1) void verify_lds_kernel(const VerifyArgs a) 
         __builtin_nontemporal_store(M, pml);
         __builtin_nontemporal_store(fmaf(w0, lt, w1 * l1), pml + 1);
     }
+    MAD_TRACE(mad_trace_verify, 1);
 }
 
 // One workgroup (D threads) per (unit, query row): log-sum-exp merge of the

@@ -33,6 +33,22 @@ def test_every_declared_symbol_is_exported(mad):
         assert hasattr(lib, n), n
 
 
+TRACE_FUNCTIONS = [f"mad_trace_{k}_{op}" for k in ("decode", "update", "verify") for op in ("read", "clear")]
+
+
+def test_phase_trace_only_in_the_trace_build(mad):
+    # the product library carries no phase marks; the diagnostic build of the
+    # same sources (MAD_PHASE_TRACE) exports a reader and a clear per kernel file
+    lib = ctypes.CDLL(mad.LIB_PATH)
+    assert not any(hasattr(lib, n) for n in TRACE_FUNCTIONS)
+    from paper_2608_30252_amd import build
+    if not os.path.exists(build.TRACE_LIB):
+        pytest.skip("libmad_trace.so not built (python -m paper_2608_30252_amd.build --trace)")
+    tlib = ctypes.CDLL(build.TRACE_LIB)
+    for n in TRACE_FUNCTIONS + _declared_functions():
+        assert hasattr(tlib, n), n
+
+
 def test_version_and_empty_error(mad):
     assert "gfx950" in mad.version()
 
