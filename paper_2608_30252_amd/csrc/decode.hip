@@ -257,18 +257,15 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int k1 = min(n, k0 + a.chunk);
     const int w_cap = a.w_cap;
 
-    // the unit's arrival counter, taken at entry and kept in SGPRs (the empty
-    // asm): not re-read from the arguments between a split's last partial
-    // store and its arrival.  Through the asm the pointer loses its address
-    // space, so the arrival becomes a flat atomic (same agent-scope semantics)
-    // without the compiler's wave-reduction wrapper around a one-lane atomic:
-    // 7.09 -> 7.00 us on the compact layer, where keeping it a global atomic
-    // gained nothing.  With 8 or more query heads per KV head the kernel has
-    // no SGPRs to spare for it.
+    // the unit's arrival counter, taken at entry and pinned in SGPRs (pin_sgpr):
+    // not re-read between a split's last partial store and its arrival, which
+    // becomes a flat atomic -- 7.09 -> 7.00 us on the compact layer (pinning
+    // it as a global pointer gained nothing).  With 8 or more query heads per
+    // KV head the kernel has no SGPRs to spare for it.
     uint64_t cnt_addr = 0;
     if constexpr (G <= 4) {
-        cnt_addr = (uint64_t)(uintptr_t)(a.counters + (size_t)u * kCounterStride);
-        asm volatile("" : "+s"(cnt_addr));
+        cnt_addr = ptr_bits(a.counters + (size_t)u * kCounterStride);
+        pin_sgpr(cnt_addr);
     }
     const T *mk = reinterpret_cast<const T *>(a.mk) + b * a.m_seq + c * a.m_head;
     const T *mv = reinterpret_cast<const T *>(a.mv) + b * a.m_seq + c * a.m_head;
@@ -579,7 +576,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     MAD_TRACE_SET(t_arrive);   // stored after the atomic, whose wait would count the store
     __shared__ int s_last;
     if (tid == 0) {
-        unsigned *cnt = G <= 4 ? reinterpret_cast<unsigned *>((uintptr_t)cnt_addr) : a.counters + (size_t)u * kCounterStride;
+        unsigned *cnt = G <= 4 ? bits_ptr<unsigned>(cnt_addr) : a.counters + (size_t)u * kCounterStride;
         const int last = arrive(cnt) == (unsigned)(n_splits - 1);
         MAD_TRACE(mad_trace_decode, 2);
         MAD_TRACE_SAVE_T0(mad_trace_decode);

@@ -181,6 +181,23 @@ __device__ __forceinline__ float load_agent(const float *p) {
     return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void wait_vm_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); /* vmcnt(0) */ }
+// Keeps a wave-uniform pointer (as an integer) in SGPRs from this point on
+// (the empty asm): the compiler neither re-reads the kernel argument it came
+// from where it is used nor knows its address space afterwards, so the
+// one-lane hand-off atomics through it are issued as flat atomics (the same
+// agent-scope semantics) without the wave-reduction wrapper the compiler puts
+// around a global atomic -- measured 0.09 us shorter on the decode arrival.
+// The value must be wave-uniform; it is taken from the first active lane
+// (readfirstlane returns int: each half goes through uint32_t, so the low
+// half is never sign-extended into the high one).
+__device__ __forceinline__ void pin_sgpr(uint64_t &v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    v = ((uint64_t)hi << 32) | (uint64_t)lo;
+    asm volatile("" : "+s"(v));
+}
+template <typename P> __device__ __forceinline__ uint64_t ptr_bits(P *p) { return (uint64_t)(uintptr_t)p; }
+template <typename P> __device__ __forceinline__ P *bits_ptr(uint64_t v) { return reinterpret_cast<P *>((uintptr_t)v); }
 __device__ __forceinline__ unsigned arrive(unsigned *counter) {
     return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
