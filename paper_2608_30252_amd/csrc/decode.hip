@@ -53,7 +53,7 @@ namespace mad {
 MAD_TRACE_BUFFER(mad_trace_decode)
 
 constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
-constexpr int kMergeLds = 65536;    // LDS that holds a unit's split partials in the merge
+constexpr int kMergeLds = 69632;    // LDS that holds a unit's split partials in the merge (64 splits at G 4, d 64)
 
 template <typename T, int D, int G, int NSUB>
 struct DecodeCfg {
@@ -254,7 +254,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const bool appends = nmode == 2;      // ... which this row also writes into its ring
     const int n = mlen + wlen + (has_new ? 1 : 0);
     const int k0 = s * a.chunk;
-    const int k1 = min(n, k0 + a.chunk);
+    const int k1 = (a.fold && s == a.n_splits - 1) ? n : min(n, k0 + a.chunk);
     const int w_cap = a.w_cap;
 
     // the unit's arrival counter, taken at entry and pinned in SGPRs (pin_sgpr):
@@ -630,13 +630,26 @@ DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_key
     if (ns < 1) ns = 1;
     // Whole super-tiles per split.  Rounding the even share down leaves a few
     // keys (e.g. the new token) for one short extra split per unit, which the
-    // grid dispatches first; when the leftover is more than a sliver the share
-    // is rounded up instead (one split fewer, the last one short).
+    // grid dispatches first -- unless the extra workgroups would not all be
+    // resident at once (two per CU), where they would start only as others
+    // finish: then the last split takes those keys (one more, mostly masked,
+    // super-tile), and every CU keeps the same share (the full 32K KV: 64
+    // splits of 512 keys, 512 workgroups, against 52 of 640 whose 416
+    // workgroups put two on some CUs and one on others).  When the leftover
+    // is more than a sliver the share is rounded up instead (one split fewer,
+    // the last one short).
     const int share = p.n_max / ns;
     const int down = share / super * super;
     int chunk;
+    p.fold = 0;
     if (down >= super && p.n_max - ns * down <= down / 8) {
         chunk = down;
+        if (p.n_max > ns * down && (int64_t)p.units * (ns + 1) > 2 * kDecodeCUs) {
+            p.n_splits = ns;
+            p.chunk = chunk;
+            p.fold = 1;
+            return p;
+        }
     } else {
         chunk = ((p.n_max + ns - 1) / ns + super - 1) / super * super;
     }

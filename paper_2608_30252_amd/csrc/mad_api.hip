@@ -175,6 +175,7 @@ int decode_impl(const void *q, int B, int Hq, int Hkv, int d, int dtype, float s
     a.n_splits = p.n_splits;
     a.nsub = p.nsub;
     a.chunk = p.chunk;
+    a.fold = p.fold;
     if (need > 0) {
         a.counters = (unsigned *)ws;
         a.part = (float *)((char *)ws + mad::kCounterRegionBytes);

@@ -40,6 +40,7 @@ struct DecodeArgs {
     float scale_log2;     // softmax scale * log2(e)
     int Hq, Hkv, units, n_splits, chunk, w_cap;
     int nsub;             // wave groups per workgroup (1 or 2)
+    int fold;             // 1: the last split runs to the end of the row (keys past n_splits * chunk)
     // per row, one 16-byte record read by a single scalar load: memory length,
     // window length, ring start, new-token mode (0 none, 1 attend, 2 attend and append)
     int4 seq[kMaxB];
@@ -47,6 +48,7 @@ struct DecodeArgs {
 
 struct DecodePlan {
     int units, n_splits, chunk, n_max, nsub;
+    int fold;   // 1: the last split also takes the few keys past n_splits * chunk
 };
 
 DecodePlan plan_decode(int B, int Hkv, int G, int d, int dtype, const int *n_keys);

@@ -183,9 +183,18 @@ def test_maximum_batch_ragged_bf16():
 
 
 def test_long_full_kv_reaches_the_split_cap_bf16():
-    # 131072 keys in one sequence: the split plan hits the merge buffer's cap (62 splits of a unit)
+    # 131072 keys in one sequence of 4 KV heads: the plan aims at 128 splits a
+    # unit and is held to the merge buffer's cap (65 splits of 4 heads x d 64)
     n = 131071
-    _case(torch.bfloat16, 1, 32, 8, 64, 0, n, n + 65, 40, seed=65, mem=False)
+    _case(torch.bfloat16, 1, 16, 4, 64, 0, n, n + 65, 40, seed=65, mem=False)
+
+
+@pytest.mark.parametrize("n", [8192, 32768])
+def test_full_kv_leftover_key_folded_into_the_last_split_bf16(n):
+    # n window keys + the new token: 64 splits of n / 64 keys would leave the
+    # token for a 65th split whose workgroups would not all be resident at
+    # once, so the last split takes it (the token is also appended)
+    _case(torch.bfloat16, 1, 32, 8, 64, 0, n, n + 64, 17, seed=66 + n // 8192, mem=False)
 
 
 def test_batched_sixteen_sequences_bench_configuration():
