@@ -194,16 +194,15 @@ def summarize_trace(path):
             short = name.split("(")[0].replace("void ", "")
             # workgroups over all three grid dimensions (the sizes are in work-items)
             ext = [(int(row.get(f"Grid_Size_{a}") or 1), int(row.get(f"Workgroup_Size_{a}") or 1)) for a in "XYZ"]
-            wgs, wg = 1, 1
-            for g, w in ext:
-                wgs *= g // w
-                wg *= w
-            key = (short, wgs, wg)
+            dims = tuple(g // w for g, w in ext)
+            wgs, wg = dims[0] * dims[1] * dims[2], ext[0][1] * ext[1][1] * ext[2][1]
+            key = (short, wgs, "x".join(str(n) for n in dims), wg)
             groups.setdefault(key, []).append((int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3)
-    print(f"{'kernel':48s} {'grid':>8s} {'wg':>5s} {'calls':>6s} {'mean_us':>8s} {'p10':>8s} {'median':>8s} {'p90':>8s}")
-    for (short, wgs, wg), d in sorted(groups.items()):
+    print(f"{'kernel':48s} {'grid':>8s} {'shape':>10s} {'wg':>5s} {'calls':>6s} {'mean_us':>8s} {'p10':>8s} {'median':>8s} "
+          f"{'p90':>8s}")
+    for (short, wgs, shape, wg), d in sorted(groups.items()):
         d.sort()
-        print(f"{short:48s} {wgs:8d} {wg:5d} {len(d):6d} {sum(d) / len(d):8.2f} {d[len(d) // 10]:8.2f} "
+        print(f"{short:48s} {wgs:8d} {shape:>10s} {wg:5d} {len(d):6d} {sum(d) / len(d):8.2f} {d[len(d) // 10]:8.2f} "
               f"{statistics.median(d):8.2f} {d[9 * len(d) // 10]:8.2f}")
 
 
@@ -383,10 +382,10 @@ def trace_percentiles(sources, kernel="mad::decode_kernel<mad::bf16_t, 64, 4, 1>
     for line in text.splitlines():
         if not line.startswith(kernel):
             continue
-        f = line[len(kernel):].split()   # grid, wg, calls, mean, p10, median, p90
-        if len(f) == 7 and int(f[0]) == grid:
-            return {"calls": int(f[2]), "mean_us": float(f[3]), "p10_us": float(f[4]), "median_us": float(f[5]),
-                    "p90_us": float(f[6]), "source": "profiles/bench_kernel_trace.md (rocprofv3 kernel trace)"}
+        f = line[len(kernel):].split()   # grid, shape, wg, calls, mean, p10, median, p90
+        if len(f) == 8 and int(f[0]) == grid:
+            return {"calls": int(f[3]), "mean_us": float(f[4]), "p10_us": float(f[5]), "median_us": float(f[6]),
+                    "p90_us": float(f[7]), "source": "profiles/bench_kernel_trace.md (rocprofv3 kernel trace)"}
     return None
 
 
