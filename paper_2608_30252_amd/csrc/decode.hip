@@ -49,7 +49,8 @@ namespace mad {
 
 // phase marks of the diagnostic trace build: 0 entry, 1 partial stored and
 // acknowledged, 2 arrival counter returned, 3 (merging workgroup) partials in
-// LDS, 4 its first head merged, 5 merge done
+// LDS, 4 its first head merged, 5 merge done, 6 the first tiles' loads
+// issued, 8 the first tile landed
 MAD_TRACE_BUFFER(mad_trace_decode)
 
 constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
@@ -246,6 +247,17 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     // grid (KV head, row, split): the row's record is read without waiting for any
     // other argument; the last split (the one holding the new token) is dispatched first
     const int c = blockIdx.x, b = blockIdx.y;
+    // every kernel argument the prologue needs, read in one batch (one wait):
+    // left to itself the compiler spreads these reads over six dependent
+    // rounds (0.06 us on the compact layer).  With 8 or more query heads per KV
+    // head the kernel has no SGPRs to spare for it.
+    if constexpr (G <= 4) {
+        const int4 sq0 = a.seq[b];
+        asm volatile("" ::"s"(a.q), "s"(a.mk), "s"(a.mv), "s"(a.wk), "s"(a.wv), "s"(a.kn), "s"(a.vn),
+                     "s"(a.m_seq), "s"(a.m_head), "s"(a.w_seq), "s"(a.w_head), "s"(a.chunk), "s"(a.w_cap),
+                     "s"(a.n_splits), "s"(a.Hq), "s"(a.fold), "s"(sq0.x), "s"(sq0.y), "s"(sq0.z), "s"(sq0.w),
+                     "s"(gridDim.x), "s"(gridDim.z));
+    }
     const int u = b * (int)gridDim.x + c, s = (int)gridDim.z - 1 - (int)blockIdx.z;
     const int4 sq = a.seq[b];
     const int mlen = sq.x, wlen = sq.y, wst = sq.z;
@@ -361,10 +373,14 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int nst = (k1 > k0) ? (k1 - k0 + C::SUPER - 1) / C::SUPER : 0;
     int issued = 0;
     for (; issued < nst && issued < C::STAGES - 1; ++issued) issue(k0 + issued * C::SUPER, issued);
+    MAD_TRACE_VAR(t_issued);
+    MAD_TRACE_SET(t_issued);
+    MAD_TRACE_VAR(t_landed);
 
     for (int t = 0; t < nst; ++t) {
         wait_vm(4 * (issued - t - 1));
         __syncthreads();   // super-tile t is in LDS for every wave; stage (t-1) % STAGES is free
+        if (t == 0) MAD_TRACE_SET(t_landed);
         if (issued < nst) {
             issue(k0 + issued * C::SUPER, issued % C::STAGES);
             ++issued;
@@ -581,6 +597,8 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
         MAD_TRACE(mad_trace_decode, 2);
         MAD_TRACE_SAVE_T0(mad_trace_decode);
         MAD_TRACE_PUT(mad_trace_decode, 1, t_arrive);
+        MAD_TRACE_PUT(mad_trace_decode, 6, t_issued);
+        MAD_TRACE_PUT(mad_trace_decode, 8, t_landed);
         if (last) reset_counter(cnt);
         s_last = last;
     }

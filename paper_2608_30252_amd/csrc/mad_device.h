@@ -327,7 +327,7 @@ __device__ __forceinline__ void lds_load16_coherent(const void *src, void *lds_b
 // its XCC id (high half) and hardware id register (low half).  One vector store
 // per mark.  The counter has its own origin on each XCD, so only marks taken on
 // one XCD compare.  In the product library the marks compile to nothing.
-constexpr int kTraceSlots = 8, kTraceWGs = 4096;
+constexpr int kTraceSlots = 16, kTraceWGs = 4096;
 #ifdef MAD_PHASE_TRACE
 __device__ __forceinline__ unsigned trace_block() {
     return blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);

@@ -31,7 +31,8 @@
 namespace mad {
 
 // phase marks of the diagnostic trace build (update_rows_kernel): 0 entry,
-// 1 the first rows in LDS, 2 products done, 3 stored
+// 1 the first rows in LDS, 2 products done, 4 partial tiles in LDS, 5 tile
+// summed (thread 0's rows), 6 summed tile in LDS, 3 stored
 MAD_TRACE_BUFFER(mad_trace_update)
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
@@ -157,6 +158,9 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     // lane l holds Y[row 4 (l / 16) + e][column l % 16], e < 4
     s_acc[wave][lane] = acc;
     __syncthreads();
+    MAD_TRACE_VAR(t_acc);
+    MAD_TRACE_SET(t_acc);
+    MAD_TRACE_VAR(t_red);
     if (tid < 128) {
         const int r = tid >> 3, p = tid & 7, l0 = 16 * (r >> 2) + p, e = r & 3;
         float y0 = 0.f, y1 = 0.f;
@@ -168,8 +172,11 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
         if (is_k) rope_apply(y0, y1, rc, rs, &y0, &y1);
         s_out[r][p] = f32_to_bf16(y0);
         s_out[r][p + 8] = f32_to_bf16(y1);
+        MAD_TRACE_SET(t_red);
     }
     __syncthreads();
+    MAD_TRACE_VAR(t_bar);
+    MAD_TRACE_SET(t_bar);
     if (tid < 32 && s_row < R && s_fire) {
         const int h = tid & 1, i = s_row - s_b * a.n_new;
         bf16_t *dst = reinterpret_cast<bf16_t *>(is_k ? a.mk : a.mv) + (size_t)(is_k ? hb : hb - a.Hkv) * a.m_head +
@@ -180,6 +187,9 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     MAD_TRACE_SAVE_T0(mad_trace_update);
     MAD_TRACE_PUT(mad_trace_update, 1, t_rows);
     MAD_TRACE_PUT(mad_trace_update, 2, t_prod);
+    MAD_TRACE_PUT(mad_trace_update, 4, t_acc);
+    MAD_TRACE_PUT(mad_trace_update, 5, t_red);
+    MAD_TRACE_PUT(mad_trace_update, 6, t_bar);
     MAD_TRACE(mad_trace_update, 3);
 }
 

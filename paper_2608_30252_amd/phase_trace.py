@@ -33,7 +33,7 @@ import torch
 import paper_2608_30252_amd as mad
 from paper_2608_30252_amd import build as _build
 
-SLOTS, WGS = 8, 4096   # kTraceSlots, kTraceWGs of the trace build
+SLOTS, WGS = 16, 4096   # kTraceSlots, kTraceWGs of the trace build
 TICK_US = 0.01         # one tick of the 100 MHz counter
 
 
@@ -66,10 +66,12 @@ def us(t, t0):
 
 
 def report_decode(name, runs):
-    st, arr, atom, loads, head, rest, done = [], [], [], [], [], [], []
+    st, arr, atom, loads, head, rest, done, iss, land = [], [], [], [], [], [], [], [], []
     for e in runs:
         for _, r, t0 in per_xcd(e):
             st.append(us(r[:, 0].max(), t0))
+            iss.append(np.mean(r[:, 6] - r[:, 0]) * TICK_US)
+            land.append(np.mean(r[:, 8] - r[:, 0]) * TICK_US)
             arr.append(np.percentile(us(r[:, 1], t0), [0, 50, 100]))
             m = r[r[:, 5] != 0]
             for w in m:
@@ -77,7 +79,8 @@ def report_decode(name, runs):
                 rest.append(us(w[5], w[4])); done.append(us(w[5], t0))
     a = np.mean(arr, axis=0)
     print(f"{name}: {len(runs[0])} workgroups, {len(runs)} launches (times from the XCD's first start)")
-    print(f"  workgroup starts spread over {np.mean(st):.2f} us")
+    print(f"  workgroup starts spread over {np.mean(st):.2f} us; per workgroup: first loads issued "
+          f"{np.mean(iss):.2f} us after its start, first tile landed {np.mean(land):.2f} us after its start")
     print(f"  split partials stored and acknowledged: {a[0]:.2f} / {a[1]:.2f} / {a[2]:.2f} us (min / median / max)")
     print(f"  merging workgroups ({len(done) // len(runs)} a launch): arrival atomic {np.mean(atom):.2f}, "
           f"partials into LDS {np.mean(loads):.2f}, first head merged {np.mean(head):.2f}, "
@@ -86,18 +89,24 @@ def report_decode(name, runs):
 
 
 def report_update(name, runs):
-    st, rows, prod, epi, end = [], [], [], [], []
+    st, rows, prod, epi, end, acc, red, bar, sto = [], [], [], [], [], [], [], [], []
     for e in runs:
         for _, r, t0 in per_xcd(e):
             st.append(us(r[:, 0].max(), t0))
             rows.append(np.mean(r[:, 1] - r[:, 0]) * TICK_US)
             prod.append(np.mean(r[:, 2] - r[:, 1]) * TICK_US)
             epi.append(np.mean(r[:, 3] - r[:, 2]) * TICK_US)
+            acc.append(np.mean(r[:, 4] - r[:, 2]) * TICK_US)
+            red.append(np.mean(r[:, 5] - r[:, 4]) * TICK_US)
+            bar.append(np.mean(r[:, 6] - r[:, 5]) * TICK_US)
+            sto.append(np.mean(r[:, 3] - r[:, 6]) * TICK_US)
             end.append(us(r[:, 3].max(), t0))
     print(f"{name}: {len(runs[0])} workgroups, {len(runs)} launches")
     print(f"  workgroup starts spread over {np.mean(st):.2f} us; per workgroup: first rows in LDS "
           f"{np.mean(rows):.2f}, products {np.mean(prod):.2f}, reduction and stores {np.mean(epi):.2f} us; "
           f"last store {np.mean(end):.2f} us")
+    print(f"  reduction and stores: partial tiles in LDS {np.mean(acc):.2f}, summed {np.mean(red):.2f}, "
+          f"second barrier {np.mean(bar):.2f}, store issued {np.mean(sto):.2f} us")
 
 
 def report_verify(name, runs):
