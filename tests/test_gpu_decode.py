@@ -189,6 +189,13 @@ def test_long_full_kv_reaches_the_split_cap_bf16():
     _case(torch.bfloat16, 1, 16, 4, 64, 0, n, n + 65, 40, seed=65, mem=False)
 
 
+def test_folded_last_split_with_a_ragged_batch_bf16():
+    # 2 rows x 8 KV heads: 32 splits of 256 keys; row 0 (8192 + new = 8193 keys)
+    # folds its new token into the last split, row 1 (4999 + new) leaves its
+    # last splits empty
+    _case(torch.bfloat16, 2, 32, 8, 64, 0, [8192, 4999], 8192 + 64, [11, 3000], seed=70, mem=False)
+
+
 @pytest.mark.parametrize("n", [8192, 32768])
 def test_full_kv_leftover_key_folded_into_the_last_split_bf16(n):
     # n window keys + the new token: 64 splits of n / 64 keys would leave the
