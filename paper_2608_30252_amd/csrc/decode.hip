@@ -10,10 +10,11 @@
 // scopes of the slots made in the same pass.
 //
 // Work decomposition (split-K / flash-decoding): a (Hkv, B, n_splits) grid,
-// so workgroup (c, b, z) reads its row's record without first loading any
-// other argument.  It handles unit u = b * Hkv + c of the units = B * Hkv and
-// key range s = n_splits - 1 - z (the short last range, which holds the new
-// token, is dispatched first).  Workgroups are dealt to the 8 XCDs
+// so workgroup (c, b, z) finds its row's record from its own indices, in the
+// same batch of argument reads as everything else its prologue needs.  It
+// handles unit u = b * Hkv + c of the units = B * Hkv and key range
+// s = n_splits - 1 - z (the last range, which holds the new token, is
+// dispatched first).  Workgroups are dealt to the 8 XCDs
 // round-robin by their linear id z * units + u, so with units a multiple of 8
 // every split of a unit runs on one XCD.
 //
@@ -50,7 +51,7 @@ namespace mad {
 // phase marks of the diagnostic trace build: 0 entry, 1 partial stored and
 // acknowledged, 2 arrival counter returned, 3 (merging workgroup) partials in
 // LDS, 4 its first head merged, 5 merge done, 6 the first tiles' loads
-// issued, 8 the first tile landed
+// issued, 7 the first tile landed
 MAD_TRACE_BUFFER(mad_trace_decode)
 
 constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
@@ -244,8 +245,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int grp = wave >> 2, wq = wave & 3;   // wave group (tile of the super-tile), wave in group
-    // grid (KV head, row, split): the row's record is read without waiting for any
-    // other argument; the last split (the one holding the new token) is dispatched first
+    // grid (KV head, row, split); the last split (the one holding the new token) is dispatched first
     const int c = blockIdx.x, b = blockIdx.y;
     // every kernel argument the prologue needs, read in one batch (one wait):
     // left to itself the compiler spreads these reads over six dependent
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
         MAD_TRACE_SAVE_T0(mad_trace_decode);
         MAD_TRACE_PUT(mad_trace_decode, 1, t_arrive);
         MAD_TRACE_PUT(mad_trace_decode, 6, t_issued);
-        MAD_TRACE_PUT(mad_trace_decode, 8, t_landed);
+        MAD_TRACE_PUT(mad_trace_decode, 7, t_landed);
         if (last) reset_counter(cnt);
         s_last = last;
     }

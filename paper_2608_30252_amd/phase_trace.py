@@ -71,7 +71,7 @@ def report_decode(name, runs):
         for _, r, t0 in per_xcd(e):
             st.append(us(r[:, 0].max(), t0))
             iss.append(np.mean(r[:, 6] - r[:, 0]) * TICK_US)
-            land.append(np.mean(r[:, 8] - r[:, 0]) * TICK_US)
+            land.append(np.mean(r[:, 7] - r[:, 0]) * TICK_US)
             arr.append(np.percentile(us(r[:, 1], t0), [0, 50, 100]))
             m = r[r[:, 5] != 0]
             for w in m:
