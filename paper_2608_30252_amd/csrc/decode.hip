@@ -51,7 +51,7 @@ namespace mad {
 // phase marks of the diagnostic trace build: 0 entry, 1 partial stored and
 // acknowledged, 2 arrival counter returned, 3 (merging workgroup) partials in
 // LDS, 4 its first head merged, 5 merge done, 6 the first tiles' loads
-// issued, 7 the first tile landed
+// issued, 7 the first tile landed, 8 the prologue's kernel arguments read
 MAD_TRACE_BUFFER(mad_trace_decode)
 
 constexpr int kTileBytes = 16384;   // 8 KB of K + 8 KB of V
@@ -258,6 +258,8 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
                      "s"(a.n_splits), "s"(a.Hq), "s"(a.fold), "s"(sq0.x), "s"(sq0.y), "s"(sq0.z), "s"(sq0.w),
                      "s"(gridDim.x), "s"(gridDim.z));
     }
+    MAD_TRACE_VAR(t_args);
+    MAD_TRACE_SET(t_args);
     const int u = b * (int)gridDim.x + c, s = (int)gridDim.z - 1 - (int)blockIdx.z;
     const int4 sq = a.seq[b];
     const int mlen = sq.x, wlen = sq.y, wst = sq.z;
@@ -599,6 +601,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
         MAD_TRACE_PUT(mad_trace_decode, 1, t_arrive);
         MAD_TRACE_PUT(mad_trace_decode, 6, t_issued);
         MAD_TRACE_PUT(mad_trace_decode, 7, t_landed);
+        MAD_TRACE_PUT(mad_trace_decode, 8, t_args);
         if (last) reset_counter(cnt);
         s_last = last;
     }

@@ -66,12 +66,13 @@ def us(t, t0):
 
 
 def report_decode(name, runs):
-    st, arr, atom, loads, head, rest, done, iss, land = [], [], [], [], [], [], [], [], []
+    st, arr, atom, loads, head, rest, done, iss, land, args = [], [], [], [], [], [], [], [], [], []
     for e in runs:
         for _, r, t0 in per_xcd(e):
             st.append(us(r[:, 0].max(), t0))
             iss.append(np.mean(r[:, 6] - r[:, 0]) * TICK_US)
             land.append(np.mean(r[:, 7] - r[:, 0]) * TICK_US)
+            args.append(np.mean(r[:, 8] - r[:, 0]) * TICK_US)
             arr.append(np.percentile(us(r[:, 1], t0), [0, 50, 100]))
             m = r[r[:, 5] != 0]
             for w in m:
@@ -79,8 +80,9 @@ def report_decode(name, runs):
                 rest.append(us(w[5], w[4])); done.append(us(w[5], t0))
     a = np.mean(arr, axis=0)
     print(f"{name}: {len(runs[0])} workgroups, {len(runs)} launches (times from the XCD's first start)")
-    print(f"  workgroup starts spread over {np.mean(st):.2f} us; per workgroup: first loads issued "
-          f"{np.mean(iss):.2f} us after its start, first tile landed {np.mean(land):.2f} us after its start")
+    print(f"  workgroup starts spread over {np.mean(st):.2f} us; per workgroup, after its start: kernel "
+          f"arguments read {np.mean(args):.2f}, first loads issued {np.mean(iss):.2f}, first tile landed "
+          f"{np.mean(land):.2f} us")
     print(f"  split partials stored and acknowledged: {a[0]:.2f} / {a[1]:.2f} / {a[2]:.2f} us (min / median / max)")
     print(f"  merging workgroups ({len(done) // len(runs)} a launch): arrival atomic {np.mean(atom):.2f}, "
           f"partials into LDS {np.mean(loads):.2f}, first head merged {np.mean(head):.2f}, "
