@@ -132,106 +132,153 @@ template <int N> __device__ __forceinline__ float group_max_b(float v, int lane)
         return read_lane(v, 63);
     }
 }
-// Sum over all 64 lanes, returned as a wave-uniform value (same scheme as
-// group_max_b; rows outside a broadcast's mask add zero).
-__device__ __forceinline__ float wave_sum_b(float v) {
-    v += xor_lane<1>(v);
-    v += xor_lane<2>(v);
-    v += xor_lane<4>(v);
-    v += xor_lane<8>(v);
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
-    return read_lane(v, 63);
+
+// Where feature f of split s sits in the split's partial row: the D/4 feature
+// quads rotated by (s mod SG) * 16 / SG places, SG = 256 / D.  The merge reads
+// feature quad fq of splits s, s + 1, ... (s mod SG = 0) with consecutive lanes
+// (lane = fq * SG + s mod SG), and with the rotation every 16 consecutive lanes
+// touch 16 different 16-byte bank groups of the LDS.
+template <int D> __device__ __forceinline__ int part_pos(int f, int s) {
+    constexpr int FQ = D / 4, SG = 64 / FQ;
+    return ((f / 4 + (s % SG) * (16 / SG)) % FQ) * 4 + f % 4;
+}
+
+// One batch of U splits of a lane, U consecutive ones of its split group (OS /
+// MS bytes apart in the o / (m, l) arrays), folded into the lane's running
+// (m, l, acc).  RAGGED: only the first `valid` are the unit's (the rest are
+// repeats of a real split read with weight 0).  FIRST: the running state is
+// still empty, so it needs no rescale.
+template <int U, bool FIRST, bool RAGGED>
+__device__ __forceinline__ void merge_batch(const float4 (&ov)[U], const float2 (&ml)[U], int valid, float &m,
+                                            float &l, float4 &acc) {
+    float mb = m;
+    #pragma unroll
+    for (int u = 0; u < U; ++u)
+        if (!RAGGED || u < valid) mb = FIRST && u == 0 ? ml[0].x : __builtin_amdgcn_fmed3f(mb, ml[u].x, INFINITY);
+    const float mr = mb == -INFINITY ? 0.f : mb;   // every weight 0 when the batch has no key
+    if constexpr (!FIRST) {
+        const float c = __builtin_amdgcn_exp2f(m - mr);
+        l *= c;
+        acc.x *= c; acc.y *= c; acc.z *= c; acc.w *= c;
+    }
+    #pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float w = __builtin_amdgcn_exp2f(ml[u].x - mr);
+        if (RAGGED && u >= valid) w = 0.f;
+        if (FIRST && u == 0) {
+            l = w * ml[u].y;
+            acc = make_float4(w * ov[u].x, w * ov[u].y, w * ov[u].z, w * ov[u].w);
+        } else {
+            l = fmaf(w, ml[u].y, l);
+            acc.x = fmaf(w, ov[u].x, acc.x);
+            acc.y = fmaf(w, ov[u].y, acc.y);
+            acc.z = fmaf(w, ov[u].z, acc.z);
+            acc.w = fmaf(w, ov[u].w, acc.w);
+        }
+    }
+    m = mb;
 }
 
 // Merge of a unit's split partials by its last-arriving workgroup (NT threads).
-//   blk   unit block in the workspace: [o: n_splits][G][D] [ml: n_splits][G][2]
+//   blk   unit block in the workspace: [o: n_splits][G][D] (features placed by
+//         part_pos) [ml: n_splits][G][2]
 //   lds   >= n_splits * G * (D + 2) * 4 bytes of LDS (16-byte aligned)
 // One round trip pulls the whole block into LDS; then each wave merges whole
-// heads on its own, with no further barrier: lanes over splits for the
-// log-sum-exp weights 2^(m_s - M) (all splits of the head in parallel, at most
-// kDecodeMaxSplits / 64 per lane), then lanes over features for
-// o = sum_s w_s o_s / L, each split's weight read back from its lane.
+// heads on its own, with no further barrier.  Lane (fq, j) = lane fq * SG + j
+// takes feature quad fq of the splits j, j + SG, j + 2 SG, ... with their
+// (m, l) pairs, every read of a batch issued at once (a batch holds up to 8
+// splits per lane; when SG divides the split count every lane has the same
+// splits at fixed offsets).  The SG lanes of a quad then take their common
+// maximum, rescale to it and sum, by DPP within the lane quad or pair; no split
+// is read one at a time.
 template <typename T, int D, int G, int NT>
 __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, unsigned char *lds, T *out, float *lse) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int FQ = D / 4;     // feature quads
+    constexpr int SG = 64 / FQ;   // split groups: 4 at d 64, 2 at d 128
+    static_assert(SG == 2 || SG == 4, "merge lane layout assumes d 64 or 128");
+    constexpr int OS = SG * G * D * 4, MS = SG * G * 8;   // bytes from split s to s + SG
+    const int fq = lane / SG, sg = lane % SG;
+    const int slot = (fq + sg * (16 / SG)) % FQ;          // where quad fq sits in split sg's rows
     const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
     for (int off = wave * 1024; off < nbytes; off += NT * 16) {
         if (off + lane * 16 < nbytes)
             lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, lds + off);
     }
+    const int ml_base = n_splits * G * D * 4;
+    const int per_lane = n_splits / SG;   // whole batches of every lane when SG divides n_splits
+    const bool even = per_lane * SG == n_splits && (per_lane <= 8 || per_lane % 8 == 0);
     wait_vm(0);
     __syncthreads();
     MAD_TRACE(mad_trace_decode, 3);
-    const float *lo = reinterpret_cast<const float *>(lds);                               // [n_splits][G][D]
-    const float2 *lml = reinterpret_cast<const float2 *>(lo + (size_t)n_splits * G * D);  // [n_splits][G]
 
-    constexpr int SPL = kDecodeMaxSplits / 64;
-    constexpr int FPL = D / 64;   // features per lane
-    constexpr int SB = 16;        // splits whose rows are read together
-    constexpr int NA = 4;         // independent accumulators per feature (short dependency chains)
     for (int g = wave; g < G; g += NT / 64) {
-        float2 ml[SPL];
-        float mloc = -INFINITY;
-        #pragma unroll
-        for (int i = 0; i < SPL; ++i) {
-            const int sp = lane + 64 * i;
-            ml[i] = sp < n_splits ? lml[sp * G + g] : make_float2(-INFINITY, 0.f);
-            mloc = fmaxf(mloc, ml[i].x);
-        }
-        const float M = group_max_b<64>(mloc, lane);
-        float w[SPL], lsum = 0.f;
-        #pragma unroll
-        for (int i = 0; i < SPL; ++i) {
-            w[i] = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml[i].x - M);
-            lsum = fmaf(w[i], ml[i].y, lsum);
-        }
-        const float L = wave_sum_b(lsum);
-        const float inv = L > 0.f ? 1.f / L : 0.f;
-        if (lse && lane == 0) lse[g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
-
-        float acc[NA][FPL];
-        #pragma unroll
-        for (int k = 0; k < NA; ++k)
-            #pragma unroll
-            for (int f = 0; f < FPL; ++f) acc[k][f] = 0.f;
-        const float *og = lo + (size_t)g * D + lane * FPL;
-        #pragma unroll
-        for (int i = 0; i < SPL; ++i) {
-            const int s0 = 64 * i;
-            if (s0 >= n_splits) break;
-            const int cnt = n_splits - s0 < 64 ? n_splits - s0 : 64;
-            int j = 0;
-            for (; j + SB <= cnt; j += SB) {
-                float ov[SB][FPL], ws[SB];
+        const unsigned char *po = lds + ((size_t)(sg * G + g) * D + slot * 4) * 4;   // split sg, head g, quad fq
+        const unsigned char *pm = lds + ml_base + (size_t)(sg * G + g) * 8;
+        float m = -INFINITY, l = 0.f;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        auto even_run = [&](auto u_const) {   // per_lane == U, or whole batches of U == 8
+            constexpr int U = decltype(u_const)::value;
+            for (int b = 0; b < per_lane; b += U) {
+                float2 ml[U];
+                float4 ov[U];
                 #pragma unroll
-                for (int k = 0; k < SB; ++k) {
-                    ws[k] = read_lane(w[i], j + k);
-                    #pragma unroll
-                    for (int f = 0; f < FPL; ++f) ov[k][f] = og[(size_t)(s0 + j + k) * G * D + f];
+                for (int u = 0; u < U; ++u) {
+                    ml[u] = *reinterpret_cast<const float2 *>(pm + (size_t)(b + u) * MS);
+                    ov[u] = *reinterpret_cast<const float4 *>(po + (size_t)(b + u) * OS);
                 }
-                #pragma unroll
-                for (int k = 0; k < SB; ++k)
-                    #pragma unroll
-                    for (int f = 0; f < FPL; ++f) acc[k % NA][f] = fmaf(ws[k], ov[k][f], acc[k % NA][f]);
+                if (b == 0) merge_batch<U, true, false>(ov, ml, U, m, l, acc);
+                else merge_batch<U, false, false>(ov, ml, U, m, l, acc);
             }
-            for (; j < cnt; ++j) {
-                const float ws = read_lane(w[i], j);
-                #pragma unroll
-                for (int f = 0; f < FPL; ++f) acc[0][f] = fmaf(ws, og[(size_t)(s0 + j) * G * D + f], acc[0][f]);
+        };
+        if (even) {
+            switch (per_lane) {
+                case 1: even_run(std::integral_constant<int, 1>()); break;
+                case 2: even_run(std::integral_constant<int, 2>()); break;
+                case 3: even_run(std::integral_constant<int, 3>()); break;
+                case 4: even_run(std::integral_constant<int, 4>()); break;
+                case 5: even_run(std::integral_constant<int, 5>()); break;
+                case 6: even_run(std::integral_constant<int, 6>()); break;
+                case 7: even_run(std::integral_constant<int, 7>()); break;
+                default: even_run(std::integral_constant<int, 8>()); break;
             }
-        }
-        float accs[FPL];
-        #pragma unroll
-        for (int f = 0; f < FPL; ++f) accs[f] = (acc[0][f] + acc[1][f]) + (acc[2][f] + acc[3][f]);
-        if (g == 0) MAD_TRACE(mad_trace_decode, 4);
-        T *og_out = out + (size_t)g * D + lane * FPL;
-        if constexpr (std::is_same<T, bf16_t>::value && FPL == 2) {
-            *reinterpret_cast<uint32_t *>(og_out) = pack_bf16x2(accs[0] * inv, accs[1] * inv);
         } else {
-            #pragma unroll
-            for (int f = 0; f < FPL; ++f) Elem<T>::store1(og_out + f, accs[f] * inv);
+            // any split count: batches of 8 per lane, reads past the unit's
+            // splits clamped to its last split and weighted 0
+            constexpr int U = 8;
+            const int mine = (n_splits - sg + SG - 1) / SG;   // this lane's splits
+            for (int b = 0; b * SG < n_splits; b += U) {
+                float2 ml[U];
+                float4 ov[U];
+                #pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int sp = min(sg + SG * (b + u), n_splits - 1);
+                    ml[u] = *reinterpret_cast<const float2 *>(lds + ml_base + (size_t)(sp * G + g) * 8);
+                    ov[u] = *reinterpret_cast<const float4 *>(lds + ((size_t)(sp * G + g) * D + slot * 4) * 4);
+                }
+                merge_batch<U, false, true>(ov, ml, mine - b, m, l, acc);
+            }
         }
+        // the SG lanes of a feature quad: common maximum, rescale, sums
+        const float M = group_max<SG>(m);
+        const float c = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+        const float L = group_sum<SG>(l * c);
+        acc.x = group_sum<SG>(acc.x * c);
+        acc.y = group_sum<SG>(acc.y * c);
+        acc.z = group_sum<SG>(acc.z * c);
+        acc.w = group_sum<SG>(acc.w * c);
+        const float inv = L > 0.f ? __builtin_amdgcn_rcpf(L) : 0.f;
+        if (g == 0) MAD_TRACE(mad_trace_decode, 4);
+        if (sg == 0) {
+            T *og = out + (size_t)g * D + 4 * fq;
+            if constexpr (std::is_same<T, bf16_t>::value) {
+                *reinterpret_cast<uint2 *>(og) = make_uint2(pack_bf16x2(acc.x * inv, acc.y * inv),
+                                                            pack_bf16x2(acc.z * inv, acc.w * inv));
+            } else {
+                *reinterpret_cast<float4 *>(og) = make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+            }
+        }
+        if (lse && lane == 0) lse[g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
     }
 }
 
@@ -557,7 +604,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
             } else {
                 // partial of this split: unit block = [o: n_splits][G][D] [ml: n_splits][G][2]
                 float *po = blk + ((size_t)s * G + g) * D;
-                if (pv_ks == 0) store_agent2(po + 2 * pv_dp, o_acc[hi][0], o_acc[hi][1]);
+                if (pv_ks == 0) store_agent2(po + part_pos<D>(2 * pv_dp, s), o_acc[hi][0], o_acc[hi][1]);
                 if (lane == 0) store_agent2(blk + (size_t)n_splits * G * D + ((size_t)s * G + g) * 2, mm, l);
             }
         }
@@ -581,7 +628,7 @@ __global__ __launch_bounds__(256 * NSUB, NSUB == 4 ? 1 : 2) void decode_kernel(c
                 Elem<T>::store1(out + idx, L > 0.f ? O / L : 0.f);
                 if (a.lse && idx % D == 0) a.lse[head0 + g] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
             } else {
-                store_agent(blk + (size_t)s * G * D + idx, O);
+                store_agent(blk + ((size_t)s * G + g) * D + part_pos<D>(idx % D, s), O);
                 if (idx % D == 0) store_agent2(blk + (size_t)n_splits * G * D + ((size_t)s * G + g) * 2, M, L);
             }
         }

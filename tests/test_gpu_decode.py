@@ -204,6 +204,13 @@ def test_full_kv_leftover_key_folded_into_the_last_split_bf16(n):
     _case(torch.bfloat16, 1, 32, 8, 64, 0, n, n + 64, 17, seed=66 + n // 8192, mem=False)
 
 
+@pytest.mark.parametrize("n", [768, 1280, 1792])
+def test_twelve_twenty_and_twenty_eight_splits_bf16(n):
+    # n keys per row (slots + 511 window rows + the new token) cut into 12 / 20 / 28 splits of 64:
+    # the merge's lanes then take 3 / 5 / 7 splits each
+    _case(torch.bfloat16, 1, 32, 8, 64, n - 512, 511, 576, 33, seed=80 + n // 256)
+
+
 def test_batched_sixteen_sequences_bench_configuration():
     # the benchmark's batched launch: 16 sequences x (1024 slots + 511 window + new), 8-wave workgroups
     _case(torch.bfloat16, 16, 32, 8, 64, 1024, 511, 576, [(37 * i) % 64 for i in range(16)], seed=12, mcap=1024)
