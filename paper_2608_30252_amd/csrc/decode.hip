@@ -201,10 +201,13 @@ __device__ __forceinline__ void merge_splits(const float *blk, int n_splits, uns
     const int fq = lane / SG, sg = lane % SG;
     const int slot = (fq + sg * (16 / SG)) % FQ;          // where quad fq sits in split sg's rows
     const int nbytes = (n_splits * G * (D + 2) * 4 + 15) & ~15;   // inside the 256-byte padded block
-    for (int off = wave * 1024; off < nbytes; off += NT * 16) {
-        if (off + lane * 16 < nbytes)
-            lds_load16_coherent(reinterpret_cast<const unsigned char *>(blk) + off + lane * 16, lds + off);
-    }
+    // whole 1 KB pieces, a wave-uniform trip count; lanes past the block load
+    // its last 16 bytes again into LDS past the block (never read)
+    const int npieces = (nbytes + 1023) >> 10;
+    const unsigned char *src = reinterpret_cast<const unsigned char *>(blk);
+    #pragma unroll 4
+    for (int pc = wave; pc < npieces; pc += NT / 64)
+        lds_load16_coherent(src + min(pc * 1024 + lane * 16, nbytes - 16), lds + pc * 1024);
     const int ml_base = n_splits * G * D * 4;
     const int per_lane = n_splits / SG;   // whole batches of every lane when SG divides n_splits
     const bool even = per_lane * SG == n_splits && (per_lane <= 8 || per_lane % 8 == 0);
