@@ -68,23 +68,55 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     MAD_TRACE_T0();
     MAD_TRACE_VAR(t_rows);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int R = a.R, D = a.D, d = a.d, hd = d / 2;
+    // The kernel arguments come in two batches, each read with one wait and
+    // kept as opaque copies (left to the compiler, the reads are spread over
+    // dependent rounds, and the epilogue's are issued after the last barrier):
+    // what the row loads need, here; what the epilogue needs, once the row
+    // loads are issued.
+    uint64_t xb = ptr_bits(a.x), wb = ptr_bits(a.w);
+    int R = a.R, D = a.D, d = a.d, Hkv = a.Hkv, n_new = a.n_new;
+    asm volatile("" : "+s"(xb), "+s"(wb), "+s"(R), "+s"(D), "+s"(d), "+s"(Hkv), "+s"(n_new));
+    uint64_t mkb = 0, mvb = 0;
+    int64_t m_head = 0, m_seq = 0;
+    auto epilogue_args = [&]() {
+        mkb = ptr_bits(a.mk);
+        mvb = ptr_bits(a.mv);
+        m_head = a.m_head;
+        m_seq = a.m_seq;
+        asm volatile("" : "+s"(mkb), "+s"(mvb), "+s"(m_head), "+s"(m_seq));
+    };
+    const int hd = d / 2;
     const int RT = (R + 15) >> 4;
     const int li = blockIdx.x >> 3;   // grid = (2 Hkv d / 16) feature blocks (a multiple of 8) x RT
     const int fb = 8 * (li / RT) + (blockIdx.x & 7), rt = li % RT;
     const int hb = fb / (d / 16), j0 = (fb % (d / 16)) * 8;
-    const bool is_k = hb < a.Hkv;
+    const bool is_k = hb < Hkv;
     const int c = lane & 15, kq = lane >> 4;
 
-    // thread t < 128 rotates pair t % 8 of tile row t / 8; thread t < 32 stores half t % 2 of tile row t / 2
+    // thread t < 128 rotates pair t % 8 of tile row t / 8; thread t < 32 stores half t % 2 of tile row t / 2.
+    // Its angle is taken once the row loads are issued, and its row's position
+    // comes through the scalar cache (the tile's 16 positions, a wave-uniform
+    // read) and a lane permute: a vector-memory read would need a wait that
+    // also waits for the row loads.
+    int tpos[16];
+    #pragma unroll
+    for (int i = 0; i < 16; ++i) tpos[i] = a.pos[rt * 16 + i];   // rows past R: never stored
     float rc = 1.f, rs = 0.f;
-    if (is_k && tid < 128)
-        rope_cs(a.pos[min(rt * 16 + (tid >> 3), R - 1)], rope_theta(j0 + (tid & 7), d, a.log2_base), &rc, &rs);
-    const int s_row = rt * 16 + ((tid >> 1) & 15), s_b = min(s_row, R - 1) / a.n_new;
+    auto rope_angles = [&]() {
+        if (is_k && tid < 128) {
+            int pv = 0;
+            #pragma unroll
+            for (int i = 0; i < 16; ++i)   // lane i: row i
+                asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(pv) : "s"(tpos[i]), "n"(i));
+            pv = __builtin_amdgcn_ds_bpermute(((tid >> 3) & 15) << 2, pv);
+            rope_cs(pv, rope_theta(j0 + (tid & 7), d, a.log2_base), &rc, &rs);
+        }
+    };
+    const int s_row = rt * 16 + ((tid >> 1) & 15), s_b = min(s_row, R - 1) / n_new;
     const int s_fire = a.fire[s_b], s_mlen = a.mlen[s_b];
 
-    const bf16_t *w = reinterpret_cast<const bf16_t *>(a.w);
-    const bf16_t *x = reinterpret_cast<const bf16_t *>(a.x);
+    const bf16_t *w = bits_ptr<const bf16_t>(wb);
+    const bf16_t *x = bits_ptr<const bf16_t>(xb);
     f32x4_v acc = f32x4_v{0.f, 0.f, 0.f, 0.f};
     if constexpr (DIRECT) {
         // one round (D <= KR): the pieces go straight from memory into LDS
@@ -102,6 +134,9 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
                                         : x + (size_t)min(rt * 16 + row - 16, R - 1) * D;
             lds_stream16(rp + min(cb * 512 + lane * 8, D - 8), s_rows + row * PITCH + cb * 1024);
         }
+        // the epilogue's arguments and the RoPE angles while the rows are in flight
+        epilogue_args();
+        rope_angles();
         const int nst = D >> 5;
         #pragma unroll
         for (int cb = 0; cb < 4; ++cb) {
@@ -135,6 +170,8 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
             }
         };
         load(0);
+        epilogue_args();
+        rope_angles();
         for (int r0 = 0; r0 < D; r0 += KR) {
             #pragma unroll
             for (int i = 0; i < PW; ++i) {
@@ -163,12 +200,21 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     MAD_TRACE_VAR(t_red);
     if (tid < 128) {
         const int r = tid >> 3, p = tid & 7, l0 = 16 * (r >> 2) + p, e = r & 3;
-        float y0 = 0.f, y1 = 0.f;
+        // every read first, then a pairwise sum (no serial chain of reads)
+        float v0[NW], v1[NW];
         #pragma unroll
         for (int wv = 0; wv < NW; ++wv) {
-            y0 += s_acc[wv][l0][e];
-            y1 += s_acc[wv][l0 + 8][e];
+            v0[wv] = s_acc[wv][l0][e];
+            v1[wv] = s_acc[wv][l0 + 8][e];
         }
+        #pragma unroll
+        for (int h = NW / 2; h > 0; h /= 2)
+            #pragma unroll
+            for (int wv = 0; wv < h; ++wv) {
+                v0[wv] += v0[wv + h];
+                v1[wv] += v1[wv + h];
+            }
+        float y0 = v0[0], y1 = v1[0];
         if (is_k) rope_apply(y0, y1, rc, rs, &y0, &y1);
         s_out[r][p] = f32_to_bf16(y0);
         s_out[r][p + 8] = f32_to_bf16(y1);
@@ -178,9 +224,9 @@ __global__ __launch_bounds__(64 * NW) void update_rows_kernel(const UpdateArgs a
     MAD_TRACE_VAR(t_bar);
     MAD_TRACE_SET(t_bar);
     if (tid < 32 && s_row < R && s_fire) {
-        const int h = tid & 1, i = s_row - s_b * a.n_new;
-        bf16_t *dst = reinterpret_cast<bf16_t *>(is_k ? a.mk : a.mv) + (size_t)(is_k ? hb : hb - a.Hkv) * a.m_head +
-                      (size_t)s_b * a.m_seq + (size_t)(s_mlen + i) * d + h * hd + j0;
+        const int h = tid & 1, i = s_row - s_b * n_new;
+        bf16_t *dst = bits_ptr<bf16_t>(is_k ? mkb : mvb) + (size_t)(is_k ? hb : hb - Hkv) * m_head +
+                      (size_t)s_b * m_seq + (size_t)(s_mlen + i) * d + h * hd + j0;
         *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(&s_out[tid >> 1][8 * h]);
     }
     // the marks are stored only now: a store earlier would be counted by the row loads' waits
