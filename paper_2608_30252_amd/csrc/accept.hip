@@ -261,17 +261,21 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     const int v0 = chunk * kAcceptChunk, v1 = min(V, v0 + kAcceptChunk);
     double sr = 0.0, sp = 0.0;
     if (a.vec16) {
+        // every load unconditional (a piece past the chunk reads its last
+        // piece again and is skipped below; q reads the p row when unused), so
+        // no branch -- and no wait the compiler places inside one -- splits
+        // them: all 2 NV loads are in flight together
         constexpr int NV = kAcceptChunk / (256 * 4);
         float4 pv[NV], qv[NV];
         #pragma unroll
         for (int k = 0; k < NV; ++k) {
-            const int e = v0 + (tid + 256 * k) * 4;
-            const bool in = e < v1;
-            pv[k] = in ? *reinterpret_cast<const float4 *>(pr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
-            qv[k] = in && resid ? *reinterpret_cast<const float4 *>(qr + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const int e = min(v0 + (tid + 256 * k) * 4, v1 - 4);
+            pv[k] = *reinterpret_cast<const float4 *>(pr + e);
+            qv[k] = *reinterpret_cast<const float4 *>(qr + e);
         }
         #pragma unroll
         for (int k = 0; k < NV; ++k) {
+            if (v0 + (tid + 256 * k) * 4 >= v1) continue;
             sr += draw_weight(pv[k].x, qv[k].x, resid) + draw_weight(pv[k].y, qv[k].y, resid) +
                   draw_weight(pv[k].z, qv[k].z, resid) + draw_weight(pv[k].w, qv[k].w, resid);
             sp += draw_weight(pv[k].x, 0.f, false) + draw_weight(pv[k].y, 0.f, false) +
@@ -368,8 +372,9 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     if (a.vec16 && r0 + RUN <= cend) {
         #pragma unroll
         for (int k = 0; k < RUN / 4; ++k) {
+            // q read unconditionally (the p row when the draw does not use it)
             const float4 pv = *reinterpret_cast<const float4 *>(pr + r0 + 4 * k);
-            const float4 qv = wres ? *reinterpret_cast<const float4 *>(qr + r0 + 4 * k) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 qv = *reinterpret_cast<const float4 *>(qr + r0 + 4 * k);
             w[4 * k + 0] = draw_weight(pv.x, qv.x, wres);
             w[4 * k + 1] = draw_weight(pv.y, qv.y, wres);
             w[4 * k + 2] = draw_weight(pv.z, qv.z, wres);
