@@ -48,14 +48,16 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinearArgs a) {
     __shared__ float s_sq[4][RR];
 
     // ---- input rows: thread t holds chunks t + 256 j (8 features each) ----
+    // Rows past R read row R - 1 (their results are never stored): an
+    // unconditional load, where a conditional one is waited for inside its
+    // branch, before any weight load is issued.
     const bf16_t *x = reinterpret_cast<const bf16_t *>(a.x);
     uint4 xr[RR][KD];
     #pragma unroll
     for (int r = 0; r < RR; ++r)
         #pragma unroll
         for (int j = 0; j < KD; ++j)
-            xr[r][j] = r < R ? *reinterpret_cast<const uint4 *>(x + (size_t)r * D + (tid + 256 * j) * 8)
-                             : make_uint4(0u, 0u, 0u, 0u);
+            xr[r][j] = *reinterpret_cast<const uint4 *>(x + (size_t)min(r, R - 1) * D + (tid + 256 * j) * 8);
 
     // ---- this workgroup's features and the first weight loads ----
     int col[NC];
