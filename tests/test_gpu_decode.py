@@ -226,6 +226,13 @@ def test_empty_key_set_gives_zero_and_minus_inf():
     assert torch.all(out[0].float() == 0) and torch.all(torch.isneginf(lse[0]))
 
 
+def test_empty_row_beside_a_long_one_merges_to_zero_and_minus_inf():
+    # row 0 holds no key at all while row 1's 3071 keys give every unit 24 splits:
+    # row 0's units merge 24 empty partials
+    out, lse = _case(torch.bfloat16, 2, 32, 8, 64, [0, 2048], [0, 1023], 1056, [0, 7], new=False, seed=15)
+    assert torch.all(out[0].float() == 0) and torch.all(torch.isneginf(lse[0]))
+
+
 @pytest.mark.parametrize("Hq,Hkv,d", [(8, 8, 64), (16, 8, 64), (64, 8, 128), (32, 2, 128), (16, 1, 64)])
 def test_group_sizes_and_head_dims(Hq, Hkv, d):
     _case(torch.bfloat16, 2, Hq, Hkv, d, 333, 120, 160, 90, seed=20 + Hq + d)
