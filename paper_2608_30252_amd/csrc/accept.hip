@@ -228,6 +228,10 @@ __device__ __forceinline__ double draw_weight(float p, float q, bool resid) {
     return r > 0.0 ? r : 0.0;
 }
 
+// VEC16: every row starts 16-byte aligned and V is a multiple of 4, so the
+// rows are read as float4; the element-wise form is its own instantiation so
+// that the aligned kernel carries none of its code
+template <bool VEC16>
 __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int b = blockIdx.x % a.B, chunk = blockIdx.x / a.B;
@@ -260,7 +264,7 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     // ---- this chunk's sums of the draw weights and of p_a ----
     const int v0 = chunk * kAcceptChunk, v1 = min(V, v0 + kAcceptChunk);
     double sr = 0.0, sp = 0.0;
-    if (a.vec16) {
+    if constexpr (VEC16) {
         // every load unconditional (a piece past the chunk reads its last
         // piece again and is skipped below; q reads the p row when unused), so
         // no branch -- and no wait the compiler places inside one -- splits
@@ -282,10 +286,21 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
                   draw_weight(pv[k].z, 0.f, false) + draw_weight(pv[k].w, 0.f, false);
         }
     } else {
-        for (int v = v0 + tid; v < v1; v += 256) {
-            const float pv = pr[v];
-            sr += draw_weight(pv, resid ? qr[v] : 0.f, resid);
-            sp += draw_weight(pv, 0.f, false);
+        // element by element, the loads again unconditional (an index past
+        // the chunk reads its last entry, skipped in the sums)
+        constexpr int NE = kAcceptChunk / 256;
+        float pv[NE], qv[NE];
+        #pragma unroll
+        for (int k = 0; k < NE; ++k) {
+            const int v = min(v0 + tid + 256 * k, v1 - 1);
+            pv[k] = pr[v];
+            qv[k] = qr[v];
+        }
+        #pragma unroll
+        for (int k = 0; k < NE; ++k) {
+            if (v0 + tid + 256 * k >= v1) continue;
+            sr += draw_weight(pv[k], qv[k], resid);
+            sp += draw_weight(pv[k], 0.f, false);
         }
     }
     sr = wave_sum_f64(sr);
@@ -369,22 +384,30 @@ __global__ __launch_bounds__(256) void stoch_kernel(const StochArgs a) {
     double w[RUN];
     double mine = 0.0;
     int lastpos = -1;
-    if (a.vec16 && r0 + RUN <= cend) {
+    if constexpr (VEC16) {
+        // runs start on multiples of RUN and V is a multiple of 4, so a float4
+        // piece lies wholly inside the chunk or wholly past it: a piece past
+        // it reads the chunk's last piece and gets weight 0 (a product, not a
+        // branch, so the loads stay together)
         #pragma unroll
         for (int k = 0; k < RUN / 4; ++k) {
+            const int e = min(r0 + 4 * k, cend - 4);
+            const double in = (double)(r0 + 4 * k < cend);
             // q read unconditionally (the p row when the draw does not use it)
-            const float4 pv = *reinterpret_cast<const float4 *>(pr + r0 + 4 * k);
-            const float4 qv = *reinterpret_cast<const float4 *>(qr + r0 + 4 * k);
-            w[4 * k + 0] = draw_weight(pv.x, qv.x, wres);
-            w[4 * k + 1] = draw_weight(pv.y, qv.y, wres);
-            w[4 * k + 2] = draw_weight(pv.z, qv.z, wres);
-            w[4 * k + 3] = draw_weight(pv.w, qv.w, wres);
+            const float4 pv = *reinterpret_cast<const float4 *>(pr + e);
+            const float4 qv = *reinterpret_cast<const float4 *>(qr + e);
+            w[4 * k + 0] = draw_weight(pv.x, qv.x, wres) * in;
+            w[4 * k + 1] = draw_weight(pv.y, qv.y, wres) * in;
+            w[4 * k + 2] = draw_weight(pv.z, qv.z, wres) * in;
+            w[4 * k + 3] = draw_weight(pv.w, qv.w, wres) * in;
         }
     } else {
         #pragma unroll
-        for (int i = 0; i < RUN; ++i) {
-            const int v = r0 + i;
-            w[i] = v < cend ? draw_weight(pr[v], wres ? qr[v] : 0.f, wres) : 0.0;
+        for (int i = 0; i < RUN; ++i) {   // unconditional loads (past the chunk: its last entry, weight 0)
+            const int v = min(r0 + i, cend - 1);
+            const float pv = pr[v], qv = qr[v];
+            // masked by a product, not a branch (a branch would take the loads into it)
+            w[i] = draw_weight(pv, qv, wres) * (double)(r0 + i < cend);
         }
     }
     #pragma unroll
@@ -439,7 +462,10 @@ size_t stoch_ws_bytes(int B, int V) {
 }
 
 hipError_t launch_stoch(const StochArgs &a, hipStream_t st) {
-    hipLaunchKernelGGL(stoch_kernel, dim3((unsigned)(a.B * a.n_chunks)), dim3(256), 0, st, a);
+    if (a.vec16)
+        hipLaunchKernelGGL(stoch_kernel<true>, dim3((unsigned)(a.B * a.n_chunks)), dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(stoch_kernel<false>, dim3((unsigned)(a.B * a.n_chunks)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

@@ -28,11 +28,14 @@ def _edge_distance(p_row, q_row, resid, t):
     return float(np.min(np.abs(c - t))), float(c[-1])
 
 
-def _run(B, T, V, seed, accept_bias=0.0, oob=False):
+def _run(B, T, V, seed, accept_bias=0.0, oob=False, tail=0):
     import oracle
     import paper_2608_30252_amd as mad
     rng = np.random.default_rng(seed)
     p = _dist(rng, (B, T, V), 0.5)
+    if tail:   # most of p's mass on the last `tail` entries, so the draw lands there
+        p[..., V - tail:] += 10.0
+        p = (p / p.sum(-1, keepdims=True)).astype(np.float32)
     q = _dist(rng, (B, T - 1, V), 0.5) if T > 1 else np.zeros((B, 0, V), np.float32)
     if T > 1 and accept_bias:
         q = (accept_bias * p[:, :T - 1] + (1 - accept_bias) * q).astype(np.float32)
@@ -79,6 +82,16 @@ def test_high_acceptance_and_bonus_tokens():
 def test_small_and_unaligned_vocabularies():
     for i, V in enumerate([1, 3, 7, 8191, 8192, 8193, 50001]):
         _run(3, 4, V, seed=200 + i)
+
+
+@pytest.mark.parametrize("V", [8196, 8228, 16420, 128256])
+def test_draw_in_a_ragged_last_chunk_of_an_aligned_vocabulary(V):
+    # V % 4 == 0 takes the float4 path; its last 8192-entry chunk is ragged and
+    # the draw lands in it, where runs reach past the chunk's end
+    tail = V % 8192
+    for T in (3, 1):   # a residual draw, then a draw from p alone
+        _, nx = _run(4, T, V, seed=V + T, tail=tail)
+        assert (nx >= V - tail).all(), nx
 
 
 def test_out_of_range_drafted_token_is_rejected():
